@@ -1,0 +1,184 @@
+"""Benchmark: fused NA on the 2-D 7x7 fp16 workload (B=4, H=4, 56x56, D=32), one GPU.
+
+A timed step is one pass of the fused path on that workload: na_forward then
+na_backward (Delta pre-pass, dK/dV, dQ), inputs resident in HBM.  The
+reported value is the forward's useful throughput, 4*B*H*N*ell*D FLOPs (masked
+halo work is not credited) divided by the forward kernel's average duration,
+measured with HIP events on the launch stream inside the timed steps;
+ms_per_step is the whole forward+backward step.
+
+Prints one JSON line.  --gpus above 1 is refused: this build runs on one GPU.
+"""
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+import torch  # noqa: E402
+
+import workloads  # noqa: E402
+
+WORKLOAD = "2d_fp16_56x56_k7"
+PEAK_FP16_TFLOPS = 2516.6   # MI355X dense fp16 MFMA
+PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+PMC_FILE = os.path.join(ROOT, "profiles", "na_fwd_kernel.2d_fp16_56x56_k7.pmc.txt")
+FWD_SOURCES = ["na_fwd.hip", "na_common.h", "na_stage.h", "na_index.h"]
+
+
+def fwd_source_digest():
+    h = hashlib.sha256()
+    for name in FWD_SOURCES:
+        with open(os.path.join(ROOT, "paper_2403_04690_amd", "csrc", name), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic():
+    """HBM bytes per forward launch from committed rocprofv3 counter runs, or None if stale."""
+    if not os.path.exists(PMC_FILE):
+        return None
+    vals = {}
+    with open(PMC_FILE) as f:
+        for line in f:
+            if ":" in line and not line.startswith("#"):
+                key, val = line.split(":", 1)
+                vals[key.strip()] = val.strip()
+    if vals.get("source_digest") != fwd_source_digest():
+        return None
+    try:
+        return int(float(vals["hbm_bytes_per_launch"]))
+    except (KeyError, ValueError):
+        return None
+
+
+def cpu_baseline(problem, x, budget_s):
+    """The fp64 oracle's forward on the full workload, repeated for about budget_s seconds."""
+    import oracle
+
+    f = lambda t: t.double().numpy()
+    q, k, v = f(x["q"]), f(x["k"]), f(x["v"])
+    reps, t0 = 0, time.perf_counter()
+    while True:
+        oracle.forward(q, k, v, problem.kernel_size, problem.dilation, problem.softmax_scale)
+        reps += 1
+        el = time.perf_counter() - t0
+        if el >= budget_s or reps >= 10000:
+            break
+    return {
+        "value": problem.fwd_flops() * reps / el / 1e12,
+        "unit": "TFLOP/s",
+        "cores": oracle.num_threads(),
+        "kind": "oracle",
+        "sample": f"full {WORKLOAD} forward (all {problem.batch * problem.heads * problem.tokens}"
+                  f" queries) x {reps} repetitions in {el:.1f} s, fp64",
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py: this build runs on exactly one GPU; --gpus {args.gpus} is not supported",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import paper_2403_04690_amd as na
+
+    na.load_library()
+    dev = torch.device("cuda", 0)
+    p = workloads.CONFIGS[WORKLOAD]
+    x = workloads.make_inputs(p, seed=0, with_grad=True)
+    q, k, v, g = (x[n].to(dev) for n in ("q", "k", "v", "dout"))
+    out = torch.empty_like(q)
+    lse = torch.empty(q.shape[:-1], dtype=torch.float32, device=dev)
+    dq, dk, dv = torch.empty_like(q), torch.empty_like(k), torch.empty_like(v)
+    ws = torch.empty(na.workspace_bytes(p.extents, p.batch, p.heads), dtype=torch.uint8,
+                     device=dev)
+    ks, ds, sc = p.kernel_size, p.dilation, p.softmax_scale
+
+    def step(e0=None, e1=None, e2=None):
+        if e0 is not None:
+            e0.record()
+        na.forward(q, k, v, ks, ds, sc, out=out, lse=lse)
+        if e1 is not None:
+            e1.record()
+        na.backward(q, k, v, out, lse, g, ks, ds, sc, workspace=ws, dq=dq, dk=dk, dv=dv)
+        if e2 is not None:
+            e2.record()
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    K = args.steps
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(K)]
+    ev_end = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    # Give the host a head start (a GPU-side spin before the first step) so the
+    # launches below queue up and the GPU runs the K steps back to back.
+    torch.cuda._sleep(int(2e7))
+    for i in range(K):
+        step(*ev[i])
+    ev_end.record()
+    torch.cuda.synchronize()
+
+    fwd_ms = sum(ev[i][0].elapsed_time(ev[i][1]) for i in range(K)) / K
+    bwd_ms = sum(ev[i][1].elapsed_time(ev[i][2]) for i in range(K)) / K
+    step_ms = ev[0][0].elapsed_time(ev_end) / K
+
+    fwd_tflops = p.fwd_flops() / (fwd_ms * 1e-3) / 1e12
+    fwd_bytes = p.fwd_bytes()
+    achieved_gbs = fwd_bytes / (fwd_ms * 1e-3) / 1e9
+    traffic = measured_traffic()
+
+    result = {
+        "metric": "fused NA fwd TFLOP/s and % of MFMA peak (2-D 7x7 fp16); fwd+bwd ms",
+        "value": round(fwd_tflops, 3),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": args.warmup,
+        "ms_per_step": round(step_ms, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f16",
+        "data": "synthetic: iid N(0,1) q, k, v, dO (torch CPU generator, seed 0), rounded to fp16",
+        "config": {
+            "workload": WORKLOAD,
+            "rank": p.rank, "batch": p.batch, "heads": p.heads, "extents": list(p.extents),
+            "head_dim": p.head_dim, "kernel_size": list(p.kernel_size),
+            "dilation": list(p.dilation), "step": "na_forward + na_backward",
+        },
+        "fwd_ms": round(fwd_ms, 5),
+        "bwd_ms": round(bwd_ms, 5),
+        "fwd_bwd_ms": round(step_ms, 5),
+        "mfma_peak_frac": round(fwd_tflops / PEAK_FP16_TFLOPS, 5),
+        "roofline": {
+            "kernel": "na_fwd_kernel",
+            "bound": "hbm",
+            "achieved": round(achieved_gbs, 1),
+            "peak": PEAK_HBM_GBS,
+            "unit": "GB/s",
+            "frac": round(achieved_gbs / PEAK_HBM_GBS, 4),
+            "traffic": traffic,
+            "algorithmic_bytes_per_launch": fwd_bytes,
+        },
+    }
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline(p, x, args.cpu_seconds)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,132 @@
+/*
+ * na.h -- C ABI of the fused neighborhood-attention (NA) library for MI355X
+ * (gfx950).  Shared object: paper_2403_04690_amd/libna.so.
+ *
+ * Operation (Faster Neighborhood Attention, arXiv 2403.04690):
+ *   Each query token of a rank-r token space (r = 1, 2, 3) attends to its
+ *   k_a nearest same-group tokens along every axis a (Sec. 1, caption of Fig.
+ *   "neighborhoodattention", Sec. 2).  The window is centred on the query
+ *   where possible and shifted, never truncated, at borders, so each query has
+ *   exactly prod_a k_a neighbours.  Dilation d_a splits axis a into the d_a
+ *   sub-lattices x = g (mod d_a), each an independent non-dilated problem
+ *   (Sec. 3.4).  Inside a group of n tokens, the window of position p starts
+ *   at clamp(p - floor(k/2), 0, n - k).
+ *   The attention itself is Eq. 1 restricted to that neighbourhood, computed
+ *   fused (Sec. 3.3, Fig. "fna-vis"): scores, mask, online softmax and the
+ *   product with V in one kernel; no attention weights reach global memory.
+ *
+ * Conventions shared by every entry point:
+ *   - q, k, v, out, dout, dq, dk, dv: contiguous [B, H, X_1 .. X_r, D] arrays
+ *     of `dtype` in device memory, axis X_1 outermost (3-D is T, H, W).
+ *   - logsumexp: contiguous [B, H, X_1 .. X_r] fp32 in device memory, natural
+ *     log, scale included: lse = log sum_j exp(scale * q.k_j).
+ *   - Every device pointer must be 16-byte aligned.
+ *   - The caller owns all memory (including the backward workspace); the
+ *     library never allocates or frees device memory, keeps no global state
+ *     and is re-entrant.
+ *   - Calls are asynchronous and stream-ordered on `stream` (a hipStream_t;
+ *     NULL means the legacy default stream).  Problem validation is
+ *     synchronous and happens before any launch: a non-NA_OK status means
+ *     nothing was launched.  NA_ERR_HIP reports a failed launch.
+ *   - B * H * N == 0 (empty batch or heads) is a no-op returning NA_OK.
+ *   - Supported: rank 1..3, head_dim in {32, 64, 128}, any k_a >= 1 and
+ *     d_a >= 1 with k_a * d_a <= X_a, fp32 / fp16 / bf16.  N * D must stay
+ *     below 2^31 and B * H below 2^31.
+ */
+#ifndef NA_H_
+#define NA_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Same type as hipStream_t (struct ihipStream_t*). */
+struct ihipStream_t;
+typedef struct ihipStream_t* na_stream_t;
+
+typedef enum { NA_FP32 = 0, NA_FP16 = 1, NA_BF16 = 2 } na_dtype;
+
+typedef enum {
+    NA_OK = 0,
+    NA_ERR_NULL = 1,                  /* a required pointer is NULL */
+    NA_ERR_RANK = 2,                  /* rank not in 1..3 */
+    NA_ERR_SHAPE = 3,                 /* extent < 1, batch/heads < 0, or size limits exceeded */
+    NA_ERR_KERNEL_SIZE = 4,           /* kernel_size[a] < 1 */
+    NA_ERR_DILATION = 5,              /* dilation[a] < 1 */
+    NA_ERR_WINDOW_EXCEEDS_EXTENT = 6, /* kernel_size[a] * dilation[a] > extents[a] */
+    NA_ERR_HEAD_DIM = 7,              /* head_dim not in {32, 64, 128} */
+    NA_ERR_DTYPE = 8,                 /* dtype not an na_dtype value */
+    NA_ERR_ALIGNMENT = 9,             /* a device pointer is not 16-byte aligned */
+    NA_ERR_WORKSPACE = 10,            /* backward workspace missing or too small */
+    NA_ERR_HIP = 11,                  /* a HIP launch or query failed */
+    NA_ERR_SCALE = 12                 /* scale is not finite */
+} na_status;
+
+/* Human-readable text for a status code (static storage, never NULL). */
+const char* na_status_string(na_status status);
+
+/* Library version as major * 10000 + minor * 100 + patch. */
+int na_version(void);
+
+/*
+ * Host-only check of the problem description used by every entry point
+ * (rank, extents, kernel_size, dilation, batch, heads, head_dim, dtype,
+ * scale).  Touches no device and no pointer.
+ */
+na_status na_validate(int rank, const int64_t* extents, const int32_t* kernel_size,
+                      const int32_t* dilation, int64_t batch, int64_t heads, int64_t head_dim,
+                      na_dtype dtype, float scale);
+
+/*
+ * Fused NA forward (Sec. 3.3): out = softmax(scale * q k^T restricted to each
+ * query's neighbourhood) v, and logsumexp per query (kept for the backward,
+ * which recomputes the probabilities from it instead of storing them).
+ *   extents[rank], kernel_size[rank], dilation[rank]: per axis, outermost first.
+ *   scale: softmax scale (1/sqrt(head_dim) in Eq. 1; any finite value).
+ */
+na_status na_forward(int rank, const int64_t* extents, const int32_t* kernel_size,
+                     const int32_t* dilation, int64_t batch, int64_t heads, int64_t head_dim,
+                     na_dtype dtype, float scale, const void* q, const void* k, const void* v,
+                     void* out, float* logsumexp, na_stream_t stream);
+
+/* Bytes of device workspace na_backward needs (the per-query Delta = dO.O, fp32). */
+size_t na_backward_workspace_bytes(int rank, const int64_t* extents, int64_t batch, int64_t heads);
+
+/*
+ * Fused NA backward: gradients of out with respect to q, k and v given
+ * dout, from the saved out and logsumexp of na_forward on the same inputs.
+ * Built from the operators of Sec. 3.1: dP = PN(dO, V), dA = P * (dP - Delta),
+ * dQ = scale * NN(dA, K) over each query's neighbourhood, and dK = scale *
+ * IN(dA, Q), dV = IN(P, dO) over each key's inverse neighbourhood.
+ *   dq, dk, dv are fully overwritten.  workspace: device memory of at least
+ *   na_backward_workspace_bytes(...) bytes, 16-byte aligned, owned by the
+ *   caller; its contents on entry do not matter.  Deterministic: the same
+ *   inputs give bit-identical gradients.
+ */
+na_status na_backward(int rank, const int64_t* extents, const int32_t* kernel_size,
+                      const int32_t* dilation, int64_t batch, int64_t heads, int64_t head_dim,
+                      na_dtype dtype, float scale, const void* q, const void* k, const void* v,
+                      const void* out, const float* logsumexp, const void* dout, void* dq,
+                      void* dk, void* dv, void* workspace, size_t workspace_bytes,
+                      na_stream_t stream);
+
+/*
+ * Test hook: evaluates on the device, with the same index functions the
+ * kernels use, the per-axis neighbourhood summary of the problem.  Each output
+ * is a device int32 array of sum_a extents[a] entries, axis 0 first:
+ *   start[x]  = first (smallest) neighbour coordinate of query coordinate x,
+ *   inv_lo[j] = smallest query coordinate whose window contains key j,
+ *   inv_hi[j] = largest query coordinate whose window contains key j.
+ */
+na_status na_debug_windows(int rank, const int64_t* extents, const int32_t* kernel_size,
+                           const int32_t* dilation, int32_t* start, int32_t* inv_lo,
+                           int32_t* inv_hi, na_stream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* NA_H_ */

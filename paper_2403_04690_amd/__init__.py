@@ -1,0 +1,208 @@
+"""Fused neighborhood attention for MI355X (gfx950): Python binding of libna.so.
+
+Every computation runs in the HIP kernels of ``libna.so``; this module only
+checks tensor arguments and passes device pointers, sizes and the current
+stream through the C ABI declared in ``include/na.h``.  PyTorch supplies
+device memory and streams.  If the library is missing, every call raises.
+
+Neighborhood attention (Faster Neighborhood Attention, arXiv 2403.04690):
+each query attends to its k_a nearest same-group tokens along every axis a
+(window centred where possible, shifted at borders, never truncated), with
+dilation d_a splitting each axis into d_a interleaved sub-lattices.
+"""
+import ctypes
+import math
+import os
+
+import torch
+
+__all__ = ["NAError", "forward", "backward", "na_attention", "debug_windows", "validate",
+           "workspace_bytes", "library_path", "load_library", "DTYPES"]
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+_LIB_PATH = os.path.join(_PKG, "libna.so")
+_lib = None
+
+DTYPES = {torch.float32: 0, torch.float16: 1, torch.bfloat16: 2}
+
+_i64p = ctypes.POINTER(ctypes.c_int64)
+_i32p = ctypes.POINTER(ctypes.c_int32)
+_vp = ctypes.c_void_p
+
+
+class NAError(RuntimeError):
+    """A non-OK status returned by libna.so."""
+
+    def __init__(self, status, text):
+        super().__init__(f"libna: {text} (status {status})")
+        self.status = status
+
+
+def library_path():
+    return _LIB_PATH
+
+
+def load_library():
+    """Load libna.so (built by paper_2403_04690_amd/build.py); raise if it is absent."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(_LIB_PATH):
+        raise RuntimeError(
+            f"libna.so not found at {_LIB_PATH}: build it first "
+            "(python -c 'import __graft_entry__ as g; g.build()')")
+    lib = ctypes.CDLL(_LIB_PATH)
+    prob = [ctypes.c_int, _i64p, _i32p, _i32p, ctypes.c_int64, ctypes.c_int64, ctypes.c_int64,
+            ctypes.c_int, ctypes.c_float]
+    lib.na_status_string.argtypes = [ctypes.c_int]
+    lib.na_status_string.restype = ctypes.c_char_p
+    lib.na_version.restype = ctypes.c_int
+    lib.na_validate.argtypes = prob
+    lib.na_validate.restype = ctypes.c_int
+    lib.na_forward.argtypes = prob + [_vp] * 6
+    lib.na_forward.restype = ctypes.c_int
+    lib.na_backward_workspace_bytes.argtypes = [ctypes.c_int, _i64p, ctypes.c_int64, ctypes.c_int64]
+    lib.na_backward_workspace_bytes.restype = ctypes.c_size_t
+    lib.na_backward.argtypes = prob + [_vp] * 10 + [ctypes.c_size_t, _vp]
+    lib.na_backward.restype = ctypes.c_int
+    lib.na_debug_windows.argtypes = [ctypes.c_int, _i64p, _i32p, _i32p, _vp, _vp, _vp, _vp]
+    lib.na_debug_windows.restype = ctypes.c_int
+    _lib = lib
+    return lib
+
+
+def _check(status):
+    if status != 0:
+        text = load_library().na_status_string(status).decode()
+        raise NAError(status, text)
+
+
+def _per_axis(value, rank, name):
+    vals = list(value) if isinstance(value, (list, tuple)) else [int(value)] * rank
+    if len(vals) != rank:
+        raise ValueError(f"{name} needs {rank} entries, got {len(vals)}")
+    return vals
+
+
+def _problem_arrays(extents, kernel_size, dilation):
+    rank = len(extents)
+    ext = (ctypes.c_int64 * rank)(*[int(e) for e in extents])
+    ks = (ctypes.c_int32 * rank)(*_per_axis(kernel_size, rank, "kernel_size"))
+    ds = (ctypes.c_int32 * rank)(*_per_axis(dilation, rank, "dilation"))
+    return rank, ext, ks, ds
+
+
+def _stream(device):
+    return _vp(torch.cuda.current_stream(device).cuda_stream)
+
+
+def _check_tensors(ref, *others):
+    if ref.dim() < 4:
+        raise ValueError("expected [batch, heads, X_1..X_r, head_dim] with 1 <= r <= 3")
+    if ref.dtype not in DTYPES:
+        raise TypeError(f"unsupported dtype {ref.dtype}")
+    for t in (ref,) + others:
+        if not t.is_cuda:
+            raise ValueError("tensors must live on a GPU")
+        if not t.is_contiguous():
+            raise ValueError("tensors must be contiguous")
+    for t in others:
+        if t.dtype != ref.dtype or t.shape != ref.shape or t.device != ref.device:
+            raise ValueError("q, k, v (and grads) must share dtype, shape and device")
+
+
+def validate(extents, kernel_size, dilation, batch, heads, head_dim, dtype, scale):
+    """Host-only validation through na_validate; raises NAError on a bad problem."""
+    lib = load_library()
+    rank, ext, ks, ds = _problem_arrays(extents, kernel_size, dilation)
+    _check(lib.na_validate(rank, ext, ks, ds, batch, heads, head_dim, DTYPES[dtype], scale))
+
+
+def workspace_bytes(extents, batch, heads):
+    lib = load_library()
+    rank = len(extents)
+    ext = (ctypes.c_int64 * rank)(*[int(e) for e in extents])
+    return int(lib.na_backward_workspace_bytes(rank, ext, batch, heads))
+
+
+def forward(q, k, v, kernel_size, dilation=1, scale=None, out=None, lse=None):
+    """Fused NA forward.  Returns (out, logsumexp); logsumexp is fp32 [B, H, X..]."""
+    lib = load_library()
+    _check_tensors(q, k, v)
+    B, H, D = q.shape[0], q.shape[1], q.shape[-1]
+    extents = tuple(q.shape[2:-1])
+    rank, ext, ks, ds = _problem_arrays(extents, kernel_size, dilation)
+    if scale is None:
+        scale = 1.0 / math.sqrt(D)
+    if out is None:
+        out = torch.empty_like(q)
+    if lse is None:
+        lse = torch.empty(q.shape[:-1], dtype=torch.float32, device=q.device)
+    _check_tensors(q, out)
+    if lse.dtype != torch.float32 or lse.shape != q.shape[:-1] or not lse.is_contiguous():
+        raise ValueError("lse must be a contiguous fp32 tensor of shape q.shape[:-1]")
+    _check(lib.na_forward(rank, ext, ks, ds, B, H, D, DTYPES[q.dtype], float(scale),
+                          q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(),
+                          lse.data_ptr(), _stream(q.device)))
+    return out, lse
+
+
+def backward(q, k, v, out, lse, dout, kernel_size, dilation=1, scale=None, workspace=None,
+             dq=None, dk=None, dv=None):
+    """Fused NA backward.  Returns (dq, dk, dv)."""
+    lib = load_library()
+    _check_tensors(q, k, v, out, dout)
+    B, H, D = q.shape[0], q.shape[1], q.shape[-1]
+    extents = tuple(q.shape[2:-1])
+    rank, ext, ks, ds = _problem_arrays(extents, kernel_size, dilation)
+    if scale is None:
+        scale = 1.0 / math.sqrt(D)
+    if lse.dtype != torch.float32 or lse.shape != q.shape[:-1] or not lse.is_contiguous():
+        raise ValueError("lse must be a contiguous fp32 tensor of shape q.shape[:-1]")
+    dq = torch.empty_like(q) if dq is None else dq
+    dk = torch.empty_like(k) if dk is None else dk
+    dv = torch.empty_like(v) if dv is None else dv
+    _check_tensors(q, dq, dk, dv)
+    need = int(lib.na_backward_workspace_bytes(rank, ext, B, H))
+    if workspace is None:
+        workspace = torch.empty(max(need, 16), dtype=torch.uint8, device=q.device)
+    _check(lib.na_backward(rank, ext, ks, ds, B, H, D, DTYPES[q.dtype], float(scale),
+                           q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(),
+                           lse.data_ptr(), dout.data_ptr(), dq.data_ptr(), dk.data_ptr(),
+                           dv.data_ptr(), workspace.data_ptr(), workspace.numel(),
+                           _stream(q.device)))
+    return dq, dk, dv
+
+
+def debug_windows(extents, kernel_size, dilation, device="cuda"):
+    """Per-axis window starts and inverse ranges computed on the device (int32, concatenated)."""
+    lib = load_library()
+    rank, ext, ks, ds = _problem_arrays(extents, kernel_size, dilation)
+    total = int(sum(extents))
+    start = torch.empty(total, dtype=torch.int32, device=device)
+    ilo = torch.empty_like(start)
+    ihi = torch.empty_like(start)
+    _check(lib.na_debug_windows(rank, ext, ks, ds, start.data_ptr(), ilo.data_ptr(),
+                                ihi.data_ptr(), _stream(start.device)))
+    return start, ilo, ihi
+
+
+class _NAFunction(torch.autograd.Function):
+    @staticmethod
+    def forward(ctx, q, k, v, kernel_size, dilation, scale):
+        out, lse = forward(q, k, v, kernel_size, dilation, scale)
+        ctx.save_for_backward(q, k, v, out, lse)
+        ctx.cfg = (kernel_size, dilation, scale)
+        return out
+
+    @staticmethod
+    def backward(ctx, dout):
+        q, k, v, out, lse = ctx.saved_tensors
+        kernel_size, dilation, scale = ctx.cfg
+        dq, dk, dv = backward(q, k, v, out, lse, dout.contiguous(), kernel_size, dilation, scale)
+        return dq, dk, dv, None, None, None
+
+
+def na_attention(q, k, v, kernel_size, dilation=1, scale=None):
+    """Autograd-aware fused neighborhood attention on [B, H, X_1..X_r, D] tensors."""
+    return _NAFunction.apply(q, k, v, kernel_size, dilation, scale)

@@ -1,0 +1,669 @@
+// na_bwd.hip -- fused neighborhood-attention backward for gfx950.
+//
+// The backward pass is built from the three operators of Sec. 3.1, each run
+// fused so that no attention weight reaches global memory:
+//   PN  dP = dO V^T        (PN applied to the output gradient and V)
+//   NN  dQ = scale dA K    over each query's neighbourhood
+//   IN  dK = scale dA^T Q, dV = P^T dO  over each key's inverse neighbourhood
+// with dA = P * (dP - Delta), Delta = rowsum(dO * O), and P recomputed from
+// the logsumexp saved by the forward pass.  Three launches, no atomics, so the
+// result is deterministic:
+//   na_delta_kernel  Delta per query (bandwidth pass)
+//   na_dkdv_kernel   one workgroup per key tile; its queries are the union of
+//                    the tile's inverse neighbourhoods (Sec. 3.1: the relation
+//                    is not symmetric and a key may be attended by up to
+//                    k + floor(k/2) queries per axis)
+//   na_dq_kernel     one workgroup per query tile over its key halo, like the
+//                    forward pass
+#include "na_launch.h"
+#include "na_stage.h"
+
+namespace na {
+
+// ---------------------------------------------------------------------------
+// Delta = sum_c dO[c] * O[c] per query row, fp32.
+// ---------------------------------------------------------------------------
+template <int D, typename T>
+__global__ __launch_bounds__(256) void na_delta_kernel(const T* __restrict__ o,
+                                                       const T* __restrict__ dout,
+                                                       float* __restrict__ delta, int64_t rows) {
+    constexpr int kVec = Tr<T>::kVec;
+    constexpr int kLanes = D / kVec;  // lanes per row
+    constexpr int kRowsPerBlock = 256 / kLanes;
+    const int sub = threadIdx.x % kLanes;
+    const int64_t row = (int64_t)blockIdx.x * kRowsPerBlock + threadIdx.x / kLanes;
+    float acc = 0.f;
+    if (row < rows) {
+        const T* po = o + row * D + sub * kVec;
+        const T* pg = dout + row * D + sub * kVec;
+        if constexpr (sizeof(T) == 2) {
+            const typename Tr<T>::x8 a = ld_x8<T>(po), b = ld_x8<T>(pg);
+#pragma unroll
+            for (int j = 0; j < 8; ++j) acc += (float)a[j] * (float)b[j];
+        } else {
+            const f32x4 a = ld16<f32x4>(po), b = ld16<f32x4>(pg);
+#pragma unroll
+            for (int j = 0; j < 4; ++j) acc += a[j] * b[j];
+        }
+    }
+#pragma unroll
+    for (int w = 1; w < kLanes; w <<= 1) acc += __shfl_xor(acc, w, kWave);
+    if (row < rows && sub == 0) delta[row] = acc;
+}
+
+// ---------------------------------------------------------------------------
+// dQ: query-major, over each query tile's key halo.
+// ---------------------------------------------------------------------------
+template <int R, int D, typename T, int QM, int SB>
+struct DqCfg {
+    static constexpr int kThreads = 4 * kWave;
+    static constexpr int kKeys = SB * 16;
+    static constexpr int kRow = RowLayout<T, D>::kRow;
+    static constexpr int kCol = ColLayout<kKeys>::kCol;
+    static constexpr int kKElems = kKeys * kRow;    // K rows
+    static constexpr int kVElems = kKeys * kRow;    // V rows
+    static constexpr int kKtElems = D * kCol;       // K transposed
+    static constexpr int kBufElems = kKElems + kVElems + kKtElems;
+    static constexpr size_t kLdsBytes = 2 * kBufElems * sizeof(T);
+    static constexpr int kKS = D / 32;
+    static constexpr int kDB = D / 16;
+    using Stg = Stager<T, D, kKeys, kThreads>;
+};
+
+template <int R, int D, typename T, int QM, int SB>
+__global__ __launch_bounds__(256) void na_dq_kernel(Geo g, const T* __restrict__ qg,
+                                                    const T* __restrict__ kg,
+                                                    const T* __restrict__ vg,
+                                                    const T* __restrict__ dog,
+                                                    const float* __restrict__ lseg,
+                                                    const float* __restrict__ deltag,
+                                                    T* __restrict__ dqg, float scale_log2,
+                                                    float scale) {
+    using C = DqCfg<R, D, T, QM, SB>;
+    using x8 = typename Tr<T>::x8;
+    extern __shared__ __align__(16) unsigned char smem_raw[];
+    T* smem = reinterpret_cast<T*>(smem_raw);
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = uniform(tid >> 6);
+    const int col = lane & 15;
+    const int grp = lane >> 4;
+
+    const int bid = xcd_remap(blockIdx.x, g.nwg);
+    const int tile = bid % g.ntiles;
+    const int rest = bid / g.ntiles;
+    const int gidx = rest % g.ngroups;
+    const int bh = rest / g.ngroups;
+
+    int gc[kMaxRank], tc[kMaxRank];
+    unravel<R>(gidx, g.d, gc);
+    unravel<R>(tile, g.nt, tc);
+
+    int n[kMaxRank], to[kMaxRank];
+    Box<R> halo;
+#pragma unroll
+    for (int a = 0; a < R; ++a) {
+        n[a] = group_len(g.L[a], g.d[a], gc[a]);
+        to[a] = tc[a] * g.T[a];
+        if (to[a] >= n[a]) return;
+        const int last = min(to[a] + g.T[a], n[a]) - 1;
+        halo.lo[a] = win_start(to[a], n[a], g.k[a]);
+        halo.E[a] = win_start(last, n[a], g.k[a]) + g.k[a] - halo.lo[a];
+    }
+    halo.finish();
+
+    const size_t slice = (size_t)bh * g.N * D;
+    const T* kb = kg + slice;
+    const T* vb = vg + slice;
+
+    int wc[kMaxRank], wo[kMaxRank];
+    unravel<R>(wave, g.WGd, wc);
+    bool wave_live = true;
+    WaveRange<R> wr;
+#pragma unroll
+    for (int a = 0; a < R; ++a) {
+        wo[a] = to[a] + wc[a] * g.WT[a];
+        if (wo[a] >= n[a]) wave_live = false;
+        const int f = min(wo[a], n[a] - 1);
+        const int l = min(wo[a] + g.WT[a], n[a]) - 1;
+        const int sf = win_start(f, n[a], g.k[a]), sl = win_start(l, n[a], g.k[a]);
+        wr.lo[a] = sf - halo.lo[a];
+        wr.hi[a] = sl + g.k[a] - halo.lo[a];
+        wr.flo[a] = sl - halo.lo[a];
+        wr.fhi[a] = sf + g.k[a] - halo.lo[a];
+    }
+
+    int qs[QM][kMaxRank];
+    bool qvalid[QM];
+    size_t qoff[QM];
+    x8 qf[QM][C::kKS], gf[QM][C::kKS];
+    float lse2[QM], dlt[QM];
+#pragma unroll
+    for (int m = 0; m < QM; ++m) {
+        int c[kMaxRank];
+        unravel<R>(m * 16 + col, g.WT, c);
+        bool ok = wave_live;
+        int tok = 0;
+#pragma unroll
+        for (int a = 0; a < R; ++a) {
+            int p = wo[a] + c[a];
+            if (p >= n[a]) ok = false;
+            p = min(p, n[a] - 1);
+            qs[m][a] = win_start(p, n[a], g.k[a]) - halo.lo[a];
+            tok += (gc[a] + g.d[a] * p) * g.ts[a];
+        }
+        qvalid[m] = ok;
+        qoff[m] = slice + (size_t)tok * D;
+#pragma unroll
+        for (int s = 0; s < C::kKS; ++s) {
+            qf[m][s] = ok ? ld_x8<T>(qg + qoff[m] + s * 32 + grp * 8) : zero_x8<T>();
+            gf[m][s] = ok ? ld_x8<T>(dog + qoff[m] + s * 32 + grp * 8) : zero_x8<T>();
+        }
+        lse2[m] = ok ? lseg[qoff[m] / D] * kLog2e : 0.f;
+        dlt[m] = ok ? deltag[qoff[m] / D] : 0.f;
+    }
+
+    typename C::Stg kst, vst;
+    auto load_stage = [&](int s) {
+        auto tok_of = [&](int row, bool& ok) {
+            return halo.token(g, gc, s * SB + (row >> 4), row & 15, ok);
+        };
+        kst.load(kb, tid, tok_of);
+        vst.load(vb, tid, tok_of);
+    };
+    auto store_stage = [&](int buf) {
+        T* base = smem + buf * C::kBufElems;
+        kst.store_rows(base, C::kRow, tid);
+        vst.store_rows(base + C::kKElems, C::kRow, tid);
+        kst.store_cols(base + C::kKElems + C::kVElems, C::kCol, tid);
+    };
+
+    f32x4 dqacc[QM][C::kDB];
+#pragma unroll
+    for (int m = 0; m < QM; ++m)
+#pragma unroll
+        for (int db = 0; db < C::kDB; ++db) dqacc[m][db] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    const int nst = (halo.nb + SB - 1) / SB;
+    load_stage(0);
+    store_stage(0);
+    __syncthreads();
+
+    for (int s = 0; s < nst; ++s) {
+        if (s + 1 < nst) load_stage(s + 1);
+        const T* ks = smem + (s & 1) * C::kBufElems;
+        const T* vs = ks + C::kKElems;
+        const T* kt = vs + C::kVElems;
+
+        if (wave_live) {
+#pragma unroll 1
+            for (int tp = 0; tp < SB / 2; ++tp) {
+                bool rel[2], full[2];
+                int boc[2][kMaxRank], bin0[2];
+#pragma unroll
+                for (int bi = 0; bi < 2; ++bi)
+                    wr.test(halo, s * SB + tp * 2 + bi, boc[bi], bin0[bi], rel[bi], full[bi]);
+                if (!rel[0] && !rel[1]) continue;
+
+                // S^T = K Q^T and dP^T = V dO^T
+                f32x4 sacc[QM][2], pacc[QM][2];
+#pragma unroll
+                for (int bi = 0; bi < 2; ++bi) {
+#pragma unroll
+                    for (int m = 0; m < QM; ++m) {
+                        sacc[m][bi] = f32x4{0.f, 0.f, 0.f, 0.f};
+                        pacc[m][bi] = f32x4{0.f, 0.f, 0.f, 0.f};
+                    }
+                    if (!rel[bi]) continue;
+                    const int row = (tp * 2 + bi) * 16 + col;
+#pragma unroll
+                    for (int st = 0; st < C::kKS; ++st) {
+                        const x8 kf = ld_x8<T>(ks + row * C::kRow + st * 32 + grp * 8);
+                        const x8 vf = ld_x8<T>(vs + row * C::kRow + st * 32 + grp * 8);
+#pragma unroll
+                        for (int m = 0; m < QM; ++m) {
+                            sacc[m][bi] = Tr<T>::mma(kf, qf[m][st], sacc[m][bi]);
+                            pacc[m][bi] = Tr<T>::mma(vf, gf[m][st], pacc[m][bi]);
+                        }
+                    }
+                }
+
+                // dA^T = P^T (dP^T - Delta), P recomputed from the logsumexp
+                x8 dsf[QM];
+#pragma unroll
+                for (int m = 0; m < QM; ++m) {
+                    float ds[2][4];
+#pragma unroll
+                    for (int bi = 0; bi < 2; ++bi) {
+                        bool outer_ok = rel[bi];
+#pragma unroll
+                        for (int a = 0; a < R - 1; ++a)
+                            outer_ok = outer_ok && (unsigned)(boc[bi][a] - qs[m][a]) < (unsigned)g.k[a];
+                        const int base = bin0[bi] + grp * 4 - qs[m][R - 1];
+#pragma unroll
+                        for (int r = 0; r < 4; ++r) {
+                            const bool ok = full[bi] ||
+                                            (outer_ok && (unsigned)(base + r) < (unsigned)g.k[R - 1]);
+                            const float p = ok ? fast_exp2(sacc[m][bi][r] * scale_log2 - lse2[m]) : 0.f;
+                            ds[bi][r] = p * (pacc[m][bi][r] - dlt[m]);
+                        }
+                    }
+                    dsf[m] = x8{Tr<T>::cvt(ds[0][0]), Tr<T>::cvt(ds[0][1]), Tr<T>::cvt(ds[0][2]),
+                                Tr<T>::cvt(ds[0][3]), Tr<T>::cvt(ds[1][0]), Tr<T>::cvt(ds[1][1]),
+                                Tr<T>::cvt(ds[1][2]), Tr<T>::cvt(ds[1][3])};
+                }
+
+                // dQ^T += K^T dA^T
+#pragma unroll
+                for (int db = 0; db < C::kDB; ++db) {
+                    const T* krow = kt + (db * 16 + col) * C::kCol + tp * 32 + grp * 4;
+                    const x8 kf = cat_x4<T>(ld_x4<T>(krow), ld_x4<T>(krow + 16));
+#pragma unroll
+                    for (int m = 0; m < QM; ++m) dqacc[m][db] = Tr<T>::mma(kf, dsf[m], dqacc[m][db]);
+                }
+            }
+        }
+
+        if (s + 1 < nst) store_stage((s + 1) & 1);
+        __syncthreads();
+    }
+
+#pragma unroll
+    for (int m = 0; m < QM; ++m) {
+        if (!qvalid[m]) continue;
+#pragma unroll
+        for (int db = 0; db < C::kDB; ++db)
+            st_x4<T>(dqg + qoff[m] + db * 16 + grp * 4, dqacc[m][db] * scale);
+    }
+}
+
+// ---------------------------------------------------------------------------
+// dK, dV: key-major, over the union of the key tile's inverse neighbourhoods.
+// ---------------------------------------------------------------------------
+template <int R, int D, typename T, int KM, int SB>
+struct DkvCfg {
+    static constexpr int kThreads = 4 * kWave;
+    static constexpr int kRows = SB * 16;  // queries per stage
+    static constexpr int kRow = RowLayout<T, D>::kRow;
+    static constexpr int kCol = ColLayout<kRows>::kCol;
+    static constexpr int kQElems = kRows * kRow;   // Q rows
+    static constexpr int kGElems = kRows * kRow;   // dO rows
+    static constexpr int kQtElems = D * kCol;      // Q transposed
+    static constexpr int kGtElems = D * kCol;      // dO transposed
+    static constexpr int kTElems = kQElems + kGElems + kQtElems + kGtElems;
+    // fp32 lse (base 2) and Delta per staged query follow the element tiles
+    static constexpr size_t kBufBytes = kTElems * sizeof(T) + 2 * kRows * sizeof(float);
+    static constexpr size_t kLdsBytes = 2 * kBufBytes;
+    static constexpr int kKS = D / 32;
+    static constexpr int kDB = D / 16;
+    using Stg = Stager<T, D, kRows, kThreads>;
+};
+
+template <int R, int D, typename T, int KM, int SB>
+__global__ __launch_bounds__(256) void na_dkdv_kernel(Geo g, const T* __restrict__ qg,
+                                                      const T* __restrict__ kg,
+                                                      const T* __restrict__ vg,
+                                                      const T* __restrict__ dog,
+                                                      const float* __restrict__ lseg,
+                                                      const float* __restrict__ deltag,
+                                                      T* __restrict__ dkg, T* __restrict__ dvg,
+                                                      float scale_log2, float scale) {
+    using C = DkvCfg<R, D, T, KM, SB>;
+    using x8 = typename Tr<T>::x8;
+    extern __shared__ __align__(16) unsigned char smem_raw[];
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = uniform(tid >> 6);
+    const int col = lane & 15;  // key column of this lane
+    const int grp = lane >> 4;
+
+    const int bid = xcd_remap(blockIdx.x, g.nwg);
+    const int tile = bid % g.ntiles;
+    const int rest = bid / g.ntiles;
+    const int gidx = rest % g.ngroups;
+    const int bh = rest / g.ngroups;
+
+    int gc[kMaxRank], tc[kMaxRank];
+    unravel<R>(gidx, g.d, gc);
+    unravel<R>(tile, g.nt, tc);
+
+    // key tile [to, last] and the box of queries attending to it
+    int n[kMaxRank], to[kMaxRank];
+    Box<R> ibox;
+#pragma unroll
+    for (int a = 0; a < R; ++a) {
+        n[a] = group_len(g.L[a], g.d[a], gc[a]);
+        to[a] = tc[a] * g.T[a];
+        if (to[a] >= n[a]) return;
+        const int last = min(to[a] + g.T[a], n[a]) - 1;
+        ibox.lo[a] = inv_lo(to[a], n[a], g.k[a]);
+        ibox.E[a] = inv_hi(last, n[a], g.k[a]) + 1 - ibox.lo[a];
+    }
+    ibox.finish();
+
+    const size_t slice = (size_t)bh * g.N * D;
+    const T* qb = qg + slice;
+    const T* gb = dog + slice;
+    const float* lb = lseg + (size_t)bh * g.N;
+    const float* db_ = deltag + (size_t)bh * g.N;
+
+    // this wave's key sub-box: the queries that attend to any / all of its keys
+    int wc[kMaxRank], wo[kMaxRank];
+    unravel<R>(wave, g.WGd, wc);
+    bool wave_live = true;
+    WaveRange<R> wr;
+#pragma unroll
+    for (int a = 0; a < R; ++a) {
+        wo[a] = to[a] + wc[a] * g.WT[a];
+        if (wo[a] >= n[a]) wave_live = false;
+        const int f = min(wo[a], n[a] - 1);
+        const int l = min(wo[a] + g.WT[a], n[a]) - 1;
+        wr.lo[a] = inv_lo(f, n[a], g.k[a]) - ibox.lo[a];
+        wr.hi[a] = inv_hi(l, n[a], g.k[a]) + 1 - ibox.lo[a];
+        wr.flo[a] = inv_lo(l, n[a], g.k[a]) - ibox.lo[a];
+        wr.fhi[a] = inv_hi(f, n[a], g.k[a]) + 1 - ibox.lo[a];
+    }
+
+    // per-lane keys: group coordinates, K and V fragments
+    int kc[KM][kMaxRank];
+    bool kvalid[KM];
+    size_t koff[KM];
+    x8 kf[KM][C::kKS], vf[KM][C::kKS];
+#pragma unroll
+    for (int m = 0; m < KM; ++m) {
+        int c[kMaxRank];
+        unravel<R>(m * 16 + col, g.WT, c);
+        bool ok = wave_live;
+        int tok = 0;
+#pragma unroll
+        for (int a = 0; a < R; ++a) {
+            int p = wo[a] + c[a];
+            if (p >= n[a]) ok = false;
+            p = min(p, n[a] - 1);
+            kc[m][a] = p;
+            tok += (gc[a] + g.d[a] * p) * g.ts[a];
+        }
+        kvalid[m] = ok;
+        koff[m] = slice + (size_t)tok * D;
+#pragma unroll
+        for (int s = 0; s < C::kKS; ++s) {
+            kf[m][s] = ok ? ld_x8<T>(kg + koff[m] + s * 32 + grp * 8) : zero_x8<T>();
+            vf[m][s] = ok ? ld_x8<T>(vg + koff[m] + s * 32 + grp * 8) : zero_x8<T>();
+        }
+    }
+
+    typename C::Stg qst, gst;
+    float lse_reg = 0.f, dlt_reg = 0.f;
+    auto load_stage = [&](int s) {
+        auto tok_of = [&](int row, bool& ok) {
+            return ibox.token(g, gc, s * SB + (row >> 4), row & 15, ok);
+        };
+        qst.load(qb, tid, tok_of);
+        gst.load(gb, tid, tok_of);
+        if (tid < C::kRows) {
+            bool ok;
+            const int tok = tok_of(tid, ok);
+            lse_reg = ok ? lb[tok] * kLog2e : 0.f;
+            dlt_reg = ok ? db_[tok] : 0.f;
+        }
+    };
+    auto buf_base = [&](int buf) { return smem_raw + buf * C::kBufBytes; };
+    auto store_stage = [&](int buf) {
+        T* base = reinterpret_cast<T*>(buf_base(buf));
+        qst.store_rows(base, C::kRow, tid);
+        gst.store_rows(base + C::kQElems, C::kRow, tid);
+        qst.store_cols(base + C::kQElems + C::kGElems, C::kCol, tid);
+        gst.store_cols(base + C::kQElems + C::kGElems + C::kQtElems, C::kCol, tid);
+        float* fl = reinterpret_cast<float*>(base + C::kTElems);
+        if (tid < C::kRows) {
+            fl[tid] = lse_reg;
+            fl[C::kRows + tid] = dlt_reg;
+        }
+    };
+
+    f32x4 dkacc[KM][C::kDB], dvacc[KM][C::kDB];
+#pragma unroll
+    for (int m = 0; m < KM; ++m)
+#pragma unroll
+        for (int d = 0; d < C::kDB; ++d) {
+            dkacc[m][d] = f32x4{0.f, 0.f, 0.f, 0.f};
+            dvacc[m][d] = f32x4{0.f, 0.f, 0.f, 0.f};
+        }
+
+    const int nst = (ibox.nb + SB - 1) / SB;
+    load_stage(0);
+    store_stage(0);
+    __syncthreads();
+
+    for (int s = 0; s < nst; ++s) {
+        if (s + 1 < nst) load_stage(s + 1);
+        const T* qs = reinterpret_cast<const T*>(buf_base(s & 1));
+        const T* gs = qs + C::kQElems;
+        const T* qt = gs + C::kGElems;
+        const T* gt = qt + C::kQtElems;
+        const float* ls = reinterpret_cast<const float*>(qs + C::kTElems);
+        const float* dls = ls + C::kRows;
+
+        if (wave_live) {
+#pragma unroll 1
+            for (int tp = 0; tp < SB / 2; ++tp) {
+                bool rel[2], full[2];
+                int boc[2][kMaxRank], bin0[2];
+#pragma unroll
+                for (int bi = 0; bi < 2; ++bi)
+                    wr.test(ibox, s * SB + tp * 2 + bi, boc[bi], bin0[bi], rel[bi], full[bi]);
+                if (!rel[0] && !rel[1]) continue;
+
+                // S = Q K^T and dP = dO V^T (rows: queries, columns: this wave's keys)
+                f32x4 sacc[KM][2], pacc[KM][2];
+#pragma unroll
+                for (int bi = 0; bi < 2; ++bi) {
+#pragma unroll
+                    for (int m = 0; m < KM; ++m) {
+                        sacc[m][bi] = f32x4{0.f, 0.f, 0.f, 0.f};
+                        pacc[m][bi] = f32x4{0.f, 0.f, 0.f, 0.f};
+                    }
+                    if (!rel[bi]) continue;
+                    const int row = (tp * 2 + bi) * 16 + col;
+#pragma unroll
+                    for (int st = 0; st < C::kKS; ++st) {
+                        const x8 qa = ld_x8<T>(qs + row * C::kRow + st * 32 + grp * 8);
+                        const x8 ga = ld_x8<T>(gs + row * C::kRow + st * 32 + grp * 8);
+#pragma unroll
+                        for (int m = 0; m < KM; ++m) {
+                            sacc[m][bi] = Tr<T>::mma(qa, kf[m][st], sacc[m][bi]);
+                            pacc[m][bi] = Tr<T>::mma(ga, vf[m][st], pacc[m][bi]);
+                        }
+                    }
+                }
+
+                // per-query window starts of the 2 x 4 queries this lane holds
+                int qwin[2][4];
+                bool qin[2][4];
+                int owin[2][kMaxRank];
+#pragma unroll
+                for (int bi = 0; bi < 2; ++bi) {
+#pragma unroll
+                    for (int a = 0; a < R - 1; ++a)
+                        owin[bi][a] = win_start(ibox.lo[a] + boc[bi][a], n[a], g.k[a]);
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) {
+                        const int qi = bin0[bi] + grp * 4 + r;
+                        qin[bi][r] = qi < ibox.E[R - 1];
+                        qwin[bi][r] = win_start(min(ibox.lo[R - 1] + qi, n[R - 1] - 1), n[R - 1],
+                                                g.k[R - 1]);
+                    }
+                }
+
+                x8 pf[KM], dsf[KM];
+#pragma unroll
+                for (int m = 0; m < KM; ++m) {
+                    float p[2][4], ds[2][4];
+#pragma unroll
+                    for (int bi = 0; bi < 2; ++bi) {
+                        bool outer_ok = rel[bi];
+#pragma unroll
+                        for (int a = 0; a < R - 1; ++a)
+                            outer_ok = outer_ok && (unsigned)(kc[m][a] - owin[bi][a]) < (unsigned)g.k[a];
+                        const int srow = (tp * 2 + bi) * 16 + grp * 4;
+#pragma unroll
+                        for (int r = 0; r < 4; ++r) {
+                            const bool ok =
+                                full[bi] || (outer_ok && qin[bi][r] &&
+                                             (unsigned)(kc[m][R - 1] - qwin[bi][r]) < (unsigned)g.k[R - 1]);
+                            const float pv =
+                                ok ? fast_exp2(sacc[m][bi][r] * scale_log2 - ls[srow + r]) : 0.f;
+                            p[bi][r] = pv;
+                            ds[bi][r] = pv * (pacc[m][bi][r] - dls[srow + r]);
+                        }
+                    }
+                    pf[m] = x8{Tr<T>::cvt(p[0][0]), Tr<T>::cvt(p[0][1]), Tr<T>::cvt(p[0][2]),
+                               Tr<T>::cvt(p[0][3]), Tr<T>::cvt(p[1][0]), Tr<T>::cvt(p[1][1]),
+                               Tr<T>::cvt(p[1][2]), Tr<T>::cvt(p[1][3])};
+                    dsf[m] = x8{Tr<T>::cvt(ds[0][0]), Tr<T>::cvt(ds[0][1]), Tr<T>::cvt(ds[0][2]),
+                                Tr<T>::cvt(ds[0][3]), Tr<T>::cvt(ds[1][0]), Tr<T>::cvt(ds[1][1]),
+                                Tr<T>::cvt(ds[1][2]), Tr<T>::cvt(ds[1][3])};
+                }
+
+                // dV^T += dO^T P and dK^T += Q^T dA
+#pragma unroll
+                for (int d = 0; d < C::kDB; ++d) {
+                    const int line = (d * 16 + col) * C::kCol + tp * 32 + grp * 4;
+                    const x8 ga = cat_x4<T>(ld_x4<T>(gt + line), ld_x4<T>(gt + line + 16));
+                    const x8 qa = cat_x4<T>(ld_x4<T>(qt + line), ld_x4<T>(qt + line + 16));
+#pragma unroll
+                    for (int m = 0; m < KM; ++m) {
+                        dvacc[m][d] = Tr<T>::mma(ga, pf[m], dvacc[m][d]);
+                        dkacc[m][d] = Tr<T>::mma(qa, dsf[m], dkacc[m][d]);
+                    }
+                }
+            }
+        }
+
+        if (s + 1 < nst) store_stage((s + 1) & 1);
+        __syncthreads();
+    }
+
+#pragma unroll
+    for (int m = 0; m < KM; ++m) {
+        if (!kvalid[m]) continue;
+#pragma unroll
+        for (int d = 0; d < C::kDB; ++d) {
+            st_x4<T>(dkg + koff[m] + d * 16 + grp * 4, dkacc[m][d] * scale);
+            st_x4<T>(dvg + koff[m] + d * 16 + grp * 4, dvacc[m][d]);
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// host-side launches
+// ---------------------------------------------------------------------------
+template <class K>
+static hipError_t set_lds(K kern, size_t bytes) {
+    if (bytes <= 65536) return hipSuccess;
+    return hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                               hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
+}
+
+template <int R, int D, typename T, int QM, int KM>
+static hipError_t launch_bwd_inst(const Geo& gq, const Geo& gk, const void* q, const void* k,
+                                  const void* v, const void* o, const float* lse, const void* dout,
+                                  void* dq, void* dk, void* dv, float* delta, float scale,
+                                  hipStream_t stream) {
+    constexpr int SBQ = sizeof(T) == 4 ? 2 : 4;
+    constexpr int SBK = (sizeof(T) == 4 || D == 128) ? 2 : 4;
+    const T* tq = static_cast<const T*>(q);
+    const T* tk = static_cast<const T*>(k);
+    const T* tv = static_cast<const T*>(v);
+    const T* tg = static_cast<const T*>(dout);
+
+    // Delta
+    {
+        constexpr int kLanes = D / Tr<T>::kVec;
+        constexpr int kRowsPerBlock = 256 / kLanes;
+        const int64_t rows = (int64_t)gq.BH * gq.N;
+        const int64_t blocks = (rows + kRowsPerBlock - 1) / kRowsPerBlock;
+        hipLaunchKernelGGL((na_delta_kernel<D, T>), dim3((unsigned)blocks), dim3(256), 0, stream,
+                           static_cast<const T*>(o), tg, delta, rows);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    // dK, dV
+    {
+        using C = DkvCfg<R, D, T, KM, SBK>;
+        auto kern = na_dkdv_kernel<R, D, T, KM, SBK>;
+        hipError_t e = set_lds(kern, C::kLdsBytes);
+        if (e != hipSuccess) return e;
+        hipLaunchKernelGGL(kern, dim3(gk.nwg), dim3(C::kThreads), C::kLdsBytes, stream, gk, tq,
+                           tk, tv, tg, lse, delta, static_cast<T*>(dk), static_cast<T*>(dv),
+                           scale * kLog2e, scale);
+        e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    // dQ
+    {
+        using C = DqCfg<R, D, T, QM, SBQ>;
+        auto kern = na_dq_kernel<R, D, T, QM, SBQ>;
+        hipError_t e = set_lds(kern, C::kLdsBytes);
+        if (e != hipSuccess) return e;
+        hipLaunchKernelGGL(kern, dim3(gq.nwg), dim3(C::kThreads), C::kLdsBytes, stream, gq, tq,
+                           tk, tv, tg, lse, delta, static_cast<T*>(dq), scale * kLog2e, scale);
+        return hipGetLastError();
+    }
+}
+
+template <int R, int D, typename T>
+static hipError_t launch_bwd_m(const Geo& gq, const Geo& gk, int qm, int km, const void* q,
+                               const void* k, const void* v, const void* o, const float* lse,
+                               const void* dout, void* dq, void* dk, void* dv, float* delta,
+                               float scale, hipStream_t s) {
+    if (qm == 1 && km == 1)
+        return launch_bwd_inst<R, D, T, 1, 1>(gq, gk, q, k, v, o, lse, dout, dq, dk, dv, delta, scale, s);
+    if (qm == 1)
+        return launch_bwd_inst<R, D, T, 1, 2>(gq, gk, q, k, v, o, lse, dout, dq, dk, dv, delta, scale, s);
+    if (km == 1)
+        return launch_bwd_inst<R, D, T, 2, 1>(gq, gk, q, k, v, o, lse, dout, dq, dk, dv, delta, scale, s);
+    return launch_bwd_inst<R, D, T, 2, 2>(gq, gk, q, k, v, o, lse, dout, dq, dk, dv, delta, scale, s);
+}
+
+template <int R, typename T>
+static hipError_t launch_bwd_d(const Geo& gq, const Geo& gk, int D, int qm, int km, const void* q,
+                               const void* k, const void* v, const void* o, const float* lse,
+                               const void* dout, void* dq, void* dk, void* dv, float* delta,
+                               float scale, hipStream_t s) {
+    switch (D) {
+        case 32: return launch_bwd_m<R, 32, T>(gq, gk, qm, km, q, k, v, o, lse, dout, dq, dk, dv, delta, scale, s);
+        case 64: return launch_bwd_m<R, 64, T>(gq, gk, qm, km, q, k, v, o, lse, dout, dq, dk, dv, delta, scale, s);
+        case 128: return launch_bwd_m<R, 128, T>(gq, gk, qm, km, q, k, v, o, lse, dout, dq, dk, dv, delta, scale, s);
+    }
+    return hipErrorInvalidValue;
+}
+
+template <typename T>
+static hipError_t launch_bwd_r(const Geo& gq, const Geo& gk, int rank, int D, int qm, int km,
+                               const void* q, const void* k, const void* v, const void* o,
+                               const float* lse, const void* dout, void* dq, void* dk, void* dv,
+                               float* delta, float scale, hipStream_t s) {
+    switch (rank) {
+        case 1: return launch_bwd_d<1, T>(gq, gk, D, qm, km, q, k, v, o, lse, dout, dq, dk, dv, delta, scale, s);
+        case 2: return launch_bwd_d<2, T>(gq, gk, D, qm, km, q, k, v, o, lse, dout, dq, dk, dv, delta, scale, s);
+        case 3: return launch_bwd_d<3, T>(gq, gk, D, qm, km, q, k, v, o, lse, dout, dq, dk, dv, delta, scale, s);
+    }
+    return hipErrorInvalidValue;
+}
+
+hipError_t launch_backward(const Geo& gq, const Geo& gk, int rank, int D, int dtype, int qm,
+                           int km, const void* q, const void* k, const void* v, const void* o,
+                           const float* lse, const void* dout, void* dq, void* dk, void* dv,
+                           float* delta, float scale, hipStream_t s) {
+    switch (dtype) {
+        case 0: return launch_bwd_r<float>(gq, gk, rank, D, qm, km, q, k, v, o, lse, dout, dq, dk, dv, delta, scale, s);
+        case 1: return launch_bwd_r<_Float16>(gq, gk, rank, D, qm, km, q, k, v, o, lse, dout, dq, dk, dv, delta, scale, s);
+        case 2: return launch_bwd_r<__bf16>(gq, gk, rank, D, qm, km, q, k, v, o, lse, dout, dq, dk, dv, delta, scale, s);
+    }
+    return hipErrorInvalidValue;
+}
+
+}  // namespace na

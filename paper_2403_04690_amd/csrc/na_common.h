@@ -1,0 +1,180 @@
+// na_common.h -- shared device infrastructure of the fused NA kernels (gfx950).
+//
+// Matrix-core convention used throughout (v_mfma_f32_16x16x32_{f16,bf16}):
+//   operand A (16 x 32): lane l holds row (l % 16), contraction slots
+//                        8*(l/16) .. 8*(l/16)+7
+//   operand B (32 x 16): lane l holds column (l % 16), the same 8 slots
+//   result  C (16 x 16): lane l holds column (l % 16), rows 4*(l/16) .. +3
+// The contraction only needs A and B to agree on which real index sits in
+// each slot, so the kernels freely permute slots.  fp32 runs the same 16x16x32
+// step as eight v_mfma_f32_16x16x4_f32 instructions (one slot each).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "na_index.h"
+
+namespace na {
+
+constexpr int kWave = 64;
+constexpr int kMaxRank = 3;
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLn2 = 0.6931471805599453f;
+
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x4 __attribute__((ext_vector_type(4)));
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef int i32x2 __attribute__((ext_vector_type(2)));
+typedef int i32x4 __attribute__((ext_vector_type(4)));
+
+// Element traits: 8-slot fragments, the 16x16x32 matrix step, rounding.
+template <typename T>
+struct Tr;
+
+template <>
+struct Tr<_Float16> {
+    using x8 = f16x8;
+    using x4 = f16x4;
+    static constexpr int kVec = 8;  // elements per 16-byte access
+    __device__ static f32x4 mma(x8 a, x8 b, f32x4 c) {
+        return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0);
+    }
+    __device__ static _Float16 cvt(float x) { return (_Float16)x; }
+};
+
+template <>
+struct Tr<__bf16> {
+    using x8 = bf16x8;
+    using x4 = bf16x4;
+    static constexpr int kVec = 8;
+    __device__ static f32x4 mma(x8 a, x8 b, f32x4 c) {
+        return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+    }
+    __device__ static __bf16 cvt(float x) { return (__bf16)x; }
+};
+
+template <>
+struct Tr<float> {
+    using x8 = f32x8;
+    using x4 = f32x4;
+    static constexpr int kVec = 4;
+    __device__ static f32x4 mma(x8 a, x8 b, f32x4 c) {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) c = __builtin_amdgcn_mfma_f32_16x16x4f32(a[j], b[j], c, 0, 0, 0);
+        return c;
+    }
+    __device__ static float cvt(float x) { return x; }
+};
+
+// 16-byte vector moves (global or LDS); the element type is reinterpreted.
+template <typename V>
+__device__ __forceinline__ V ld16(const void* p) {
+    static_assert(sizeof(V) == 16, "16-byte access");
+    return *reinterpret_cast<const V*>(p);
+}
+template <typename V>
+__device__ __forceinline__ void st16(void* p, V v) {
+    static_assert(sizeof(V) == 16, "16-byte access");
+    *reinterpret_cast<V*>(p) = v;
+}
+
+// Eight consecutive elements at p (16-byte aligned) as an A/B fragment.
+template <typename T>
+__device__ __forceinline__ typename Tr<T>::x8 ld_x8(const T* p) {
+    using x8 = typename Tr<T>::x8;
+    if constexpr (sizeof(T) == 2) {
+        return __builtin_bit_cast(x8, ld16<i32x4>(p));
+    } else {
+        f32x4 a = ld16<f32x4>(p), b = ld16<f32x4>(p + 4);
+        return x8{a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
+    }
+}
+
+// Four consecutive elements at p (8-byte aligned for 16-bit, 16 for fp32).
+template <typename T>
+__device__ __forceinline__ typename Tr<T>::x4 ld_x4(const T* p) {
+    using x4 = typename Tr<T>::x4;
+    if constexpr (sizeof(T) == 2) {
+        return __builtin_bit_cast(x4, *reinterpret_cast<const i32x2*>(p));
+    } else {
+        return ld16<f32x4>(p);
+    }
+}
+
+template <typename T>
+__device__ __forceinline__ typename Tr<T>::x8 cat_x4(typename Tr<T>::x4 a, typename Tr<T>::x4 b) {
+    return typename Tr<T>::x8{a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
+}
+
+template <typename T>
+__device__ __forceinline__ typename Tr<T>::x8 zero_x8() {
+    return typename Tr<T>::x8{};
+}
+
+// Store four fp32 values rounded to T at p (8 or 16 bytes).
+template <typename T>
+__device__ __forceinline__ void st_x4(T* p, f32x4 v) {
+    if constexpr (sizeof(T) == 2) {
+        typename Tr<T>::x4 h = {Tr<T>::cvt(v[0]), Tr<T>::cvt(v[1]), Tr<T>::cvt(v[2]),
+                                Tr<T>::cvt(v[3])};
+        *reinterpret_cast<i32x2*>(p) = __builtin_bit_cast(i32x2, h);
+    } else {
+        st16<f32x4>(p, v);
+    }
+}
+
+__device__ __forceinline__ float wave_max_groups(float x) {
+    // max over the four 16-lane groups holding the same column
+    x = fmaxf(x, __shfl_xor(x, 16, kWave));
+    x = fmaxf(x, __shfl_xor(x, 32, kWave));
+    return x;
+}
+__device__ __forceinline__ float wave_sum_groups(float x) {
+    x += __shfl_xor(x, 16, kWave);
+    x += __shfl_xor(x, 32, kWave);
+    return x;
+}
+
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// Problem geometry shared by all kernels (filled on the host).  Axes beyond
+// the problem's rank are inert (extent 1, window 1, dilation 1).
+struct Geo {
+    int L[kMaxRank], k[kMaxRank], d[kMaxRank];
+    int ts[kMaxRank];    // token stride of each axis
+    int N;               // tokens per (batch, head)
+    int BH;              // batch * heads
+    int ngroups;         // prod d
+    int T[kMaxRank];     // workgroup tile (group coordinates)
+    int WT[kMaxRank];    // wave tile
+    int WGd[kMaxRank];   // waves per axis (T = WT * WGd)
+    int nt[kMaxRank];    // tiles per axis (sized for the longest group)
+    int ntiles;          // prod nt
+    int nwg;             // workgroups in the grid
+};
+
+// Workgroups are dispatched round-robin over the 8 XCDs; renumber them so
+// that each XCD receives a contiguous run of logical tiles (neighbouring tiles
+// share halo rows in that XCD's L2).
+__device__ __forceinline__ int xcd_remap(int bid, int nwg) {
+    const int q = nwg >> 3, r = nwg & 7;
+    const int x = bid & 7, slot = bid >> 3;
+    return x * q + (x < r ? x : r) + slot;
+}
+
+template <int R>
+__device__ __forceinline__ void unravel(int idx, const int* ext, int* c) {
+#pragma unroll
+    for (int a = R - 1; a >= 0; --a) {
+        c[a] = idx % ext[a];
+        idx /= ext[a];
+    }
+}
+
+__device__ __forceinline__ int uniform(int x) { return __builtin_amdgcn_readfirstlane(x); }
+
+}  // namespace na

@@ -1,0 +1,328 @@
+// na_fwd.hip -- fused neighborhood-attention forward for gfx950.
+//
+// Fused NA (Sec. 3.3, Fig. "fna-vis"): queries are tiled in their own 1-D /
+// 2-D / 3-D layout; the key/value tile is the halo that covers every
+// neighbourhood of the query tile; scores go through the NA mask and an online
+// softmax (Sec. 2) and straight into the product with V.  Only the output and
+// the per-query logsumexp are written.  Dilation is handled as extra
+// workgroups over the sub-lattices x = g (mod d) (Sec. 3.4).
+//
+// MI355X mapping:
+//   * workgroup = 4 waves = one query tile of one (batch, head, dilation
+//     group); each wave owns QM x 16 queries of it (a sub-box);
+//   * the workgroup's key halo is cut into blocks of 16 keys that run along
+//     the innermost axis; stages of SB blocks are staged in LDS,
+//     double-buffered, K row-major and V transposed, by 16-byte loads;
+//   * a wave only runs the matrix cores on blocks that intersect its own
+//     sub-box halo, and evaluates the mask only on blocks that are not inside
+//     every one of its windows;
+//   * S^T = K Q^T (16 keys x 16 queries per MFMA) leaves each query's scores
+//     in one lane column, so softmax statistics stay per lane except for a
+//     two-step cross-group max, and P^T feeds O^T = V^T P^T directly as the B
+//     operand;
+//   * scores are kept in base 2 (scale * log2 e folded into one multiply).
+#include "na_launch.h"
+#include "na_stage.h"
+
+namespace na {
+
+template <int R, int D, typename T, int QM, int SB>
+struct FwdCfg {
+    static constexpr int kThreads = 4 * kWave;
+    static constexpr int kKeys = SB * 16;  // keys per stage
+    static constexpr int kKRow = RowLayout<T, D>::kRow;
+    static constexpr int kVCol = ColLayout<kKeys>::kCol;
+    static constexpr int kKElems = kKeys * kKRow;
+    static constexpr int kVElems = D * kVCol;
+    static constexpr int kBufElems = kKElems + kVElems;
+    static constexpr size_t kLdsBytes = 2 * kBufElems * sizeof(T);
+    static constexpr int kKS = D / 32;  // contraction steps over D
+    static constexpr int kDB = D / 16;  // 16-wide blocks of D
+    using Stg = Stager<T, D, kKeys, kThreads>;
+};
+
+template <int R, int D, typename T, int QM, int SB>
+__global__ __launch_bounds__(256) void na_fwd_kernel(Geo g, const T* __restrict__ qg,
+                                                     const T* __restrict__ kg,
+                                                     const T* __restrict__ vg, T* __restrict__ og,
+                                                     float* __restrict__ lseg, float scale_log2) {
+    using C = FwdCfg<R, D, T, QM, SB>;
+    using x8 = typename Tr<T>::x8;
+    extern __shared__ __align__(16) unsigned char smem_raw[];
+    T* smem = reinterpret_cast<T*>(smem_raw);
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = uniform(tid >> 6);
+    const int col = lane & 15;  // query column of this lane
+    const int grp = lane >> 4;  // 16-lane group
+
+    // ---- workgroup -> (bh, dilation group, tile) ----
+    const int bid = xcd_remap(blockIdx.x, g.nwg);
+    const int tile = bid % g.ntiles;
+    const int rest = bid / g.ntiles;
+    const int gidx = rest % g.ngroups;
+    const int bh = rest / g.ngroups;
+
+    int gc[kMaxRank], tc[kMaxRank];
+    unravel<R>(gidx, g.d, gc);
+    unravel<R>(tile, g.nt, tc);
+
+    int n[kMaxRank], to[kMaxRank];
+    Box<R> halo;
+#pragma unroll
+    for (int a = 0; a < R; ++a) {
+        n[a] = group_len(g.L[a], g.d[a], gc[a]);
+        to[a] = tc[a] * g.T[a];
+        if (to[a] >= n[a]) return;  // tile beyond this (shorter) group: uniform exit
+        const int last = min(to[a] + g.T[a], n[a]) - 1;
+        halo.lo[a] = win_start(to[a], n[a], g.k[a]);
+        halo.E[a] = win_start(last, n[a], g.k[a]) + g.k[a] - halo.lo[a];
+    }
+    halo.finish();
+
+    const size_t slice = (size_t)bh * g.N * D;
+    const T* kb = kg + slice;
+    const T* vb = vg + slice;
+
+    // ---- this wave's query sub-box: its halo and the keys inside all of its windows ----
+    int wc[kMaxRank], wo[kMaxRank];
+    unravel<R>(wave, g.WGd, wc);
+    bool wave_live = true;
+    WaveRange<R> wr;
+#pragma unroll
+    for (int a = 0; a < R; ++a) {
+        wo[a] = to[a] + wc[a] * g.WT[a];
+        if (wo[a] >= n[a]) wave_live = false;
+        const int f = min(wo[a], n[a] - 1);
+        const int l = min(wo[a] + g.WT[a], n[a]) - 1;
+        const int sf = win_start(f, n[a], g.k[a]), sl = win_start(l, n[a], g.k[a]);
+        wr.lo[a] = sf - halo.lo[a];
+        wr.hi[a] = sl + g.k[a] - halo.lo[a];
+        wr.flo[a] = sl - halo.lo[a];
+        wr.fhi[a] = sf + g.k[a] - halo.lo[a];
+    }
+
+    // ---- per-lane queries: validity, window starts (relative to the halo), Q ----
+    int qs[QM][kMaxRank];
+    bool qvalid[QM];
+    size_t qoff[QM];
+    x8 qf[QM][C::kKS];
+#pragma unroll
+    for (int m = 0; m < QM; ++m) {
+        int c[kMaxRank];
+        unravel<R>(m * 16 + col, g.WT, c);
+        bool ok = wave_live;
+        int tok = 0;
+#pragma unroll
+        for (int a = 0; a < R; ++a) {
+            int p = wo[a] + c[a];
+            if (p >= n[a]) ok = false;
+            p = min(p, n[a] - 1);
+            qs[m][a] = win_start(p, n[a], g.k[a]) - halo.lo[a];
+            tok += (gc[a] + g.d[a] * p) * g.ts[a];
+        }
+        qvalid[m] = ok;
+        qoff[m] = slice + (size_t)tok * D;
+#pragma unroll
+        for (int s = 0; s < C::kKS; ++s)
+            qf[m][s] = ok ? ld_x8<T>(qg + qoff[m] + s * 32 + grp * 8) : zero_x8<T>();
+    }
+
+    // ---- staging of K (row-major) and V (transposed) ----
+    typename C::Stg kst, vst;
+    auto load_stage = [&](int s) {
+        auto tok_of = [&](int row, bool& ok) {
+            return halo.token(g, gc, s * SB + (row >> 4), row & 15, ok);
+        };
+        kst.load(kb, tid, tok_of);
+        vst.load(vb, tid, tok_of);
+    };
+    auto store_stage = [&](int buf) {
+        T* ks = smem + buf * C::kBufElems;
+        kst.store_rows(ks, C::kKRow, tid);
+        vst.store_cols(ks + C::kKElems, C::kVCol, tid);
+    };
+
+    // ---- online-softmax state (per lane: its query column) ----
+    f32x4 oacc[QM][C::kDB];
+    float mrow[QM], lrow[QM];
+#pragma unroll
+    for (int m = 0; m < QM; ++m) {
+        mrow[m] = -INFINITY;
+        lrow[m] = 0.f;
+#pragma unroll
+        for (int db = 0; db < C::kDB; ++db) oacc[m][db] = f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+
+    const int nst = (halo.nb + SB - 1) / SB;
+    load_stage(0);
+    store_stage(0);
+    __syncthreads();
+
+    for (int s = 0; s < nst; ++s) {
+        if (s + 1 < nst) load_stage(s + 1);
+        const T* ks = smem + (s & 1) * C::kBufElems;
+        const T* vt = ks + C::kKElems;
+
+        if (wave_live) {
+#pragma unroll 1
+            for (int tp = 0; tp < SB / 2; ++tp) {
+                bool rel[2], full[2];
+                int boc[2][kMaxRank], bin0[2];
+#pragma unroll
+                for (int bi = 0; bi < 2; ++bi)
+                    wr.test(halo, s * SB + tp * 2 + bi, boc[bi], bin0[bi], rel[bi], full[bi]);
+                if (!rel[0] && !rel[1]) continue;
+
+                // ---- S^T = K Q^T for both blocks ----
+                f32x4 sacc[QM][2];
+#pragma unroll
+                for (int bi = 0; bi < 2; ++bi) {
+#pragma unroll
+                    for (int m = 0; m < QM; ++m) sacc[m][bi] = f32x4{0.f, 0.f, 0.f, 0.f};
+                    if (!rel[bi]) continue;
+                    const T* krow = ks + ((tp * 2 + bi) * 16 + col) * C::kKRow + grp * 8;
+#pragma unroll
+                    for (int st = 0; st < C::kKS; ++st) {
+                        const x8 kf = ld_x8<T>(krow + st * 32);
+#pragma unroll
+                        for (int m = 0; m < QM; ++m)
+                            sacc[m][bi] = Tr<T>::mma(kf, qf[m][st], sacc[m][bi]);
+                    }
+                }
+
+                // ---- mask + online softmax per query block ----
+                x8 pf[QM];
+#pragma unroll
+                for (int m = 0; m < QM; ++m) {
+                    float t[2][4];
+                    float tmax = -INFINITY;
+#pragma unroll
+                    for (int bi = 0; bi < 2; ++bi) {
+                        bool outer_ok = rel[bi];
+#pragma unroll
+                        for (int a = 0; a < R - 1; ++a)
+                            outer_ok = outer_ok && (unsigned)(boc[bi][a] - qs[m][a]) < (unsigned)g.k[a];
+                        const int base = bin0[bi] + grp * 4 - qs[m][R - 1];
+#pragma unroll
+                        for (int r = 0; r < 4; ++r) {
+                            const bool ok = full[bi] ||
+                                            (outer_ok && (unsigned)(base + r) < (unsigned)g.k[R - 1]);
+                            const float x = ok ? sacc[m][bi][r] * scale_log2 : -INFINITY;
+                            t[bi][r] = x;
+                            tmax = fmaxf(tmax, x);
+                        }
+                    }
+                    tmax = wave_max_groups(tmax);
+                    const float mnew = fmaxf(mrow[m], tmax);
+                    const float muse = mnew == -INFINITY ? 0.f : mnew;
+                    const float alpha = fast_exp2(mrow[m] - muse);
+                    mrow[m] = mnew;
+                    float p[2][4];
+                    float psum = 0.f;
+#pragma unroll
+                    for (int bi = 0; bi < 2; ++bi)
+#pragma unroll
+                        for (int r = 0; r < 4; ++r) {
+                            p[bi][r] = fast_exp2(t[bi][r] - muse);
+                            psum += p[bi][r];
+                        }
+                    lrow[m] = lrow[m] * alpha + psum;
+#pragma unroll
+                    for (int db = 0; db < C::kDB; ++db) oacc[m][db] *= alpha;
+                    pf[m] = x8{Tr<T>::cvt(p[0][0]), Tr<T>::cvt(p[0][1]), Tr<T>::cvt(p[0][2]),
+                               Tr<T>::cvt(p[0][3]), Tr<T>::cvt(p[1][0]), Tr<T>::cvt(p[1][1]),
+                               Tr<T>::cvt(p[1][2]), Tr<T>::cvt(p[1][3])};
+                }
+
+                // ---- O^T += V^T P^T ----
+#pragma unroll
+                for (int db = 0; db < C::kDB; ++db) {
+                    const T* vrow = vt + (db * 16 + col) * C::kVCol + tp * 32 + grp * 4;
+                    const x8 vf = cat_x4<T>(ld_x4<T>(vrow), ld_x4<T>(vrow + 16));
+#pragma unroll
+                    for (int m = 0; m < QM; ++m) oacc[m][db] = Tr<T>::mma(vf, pf[m], oacc[m][db]);
+                }
+            }
+        }
+
+        if (s + 1 < nst) store_stage((s + 1) & 1);
+        __syncthreads();
+    }
+
+    // ---- epilogue: normalise, store O (rounded once) and the natural-log LSE ----
+#pragma unroll
+    for (int m = 0; m < QM; ++m) {
+        const float l = wave_sum_groups(lrow[m]);
+        if (!qvalid[m]) continue;
+        const float inv = 1.f / l;
+#pragma unroll
+        for (int db = 0; db < C::kDB; ++db)
+            st_x4<T>(og + qoff[m] + db * 16 + grp * 4, oacc[m][db] * inv);
+        if (grp == 0) lseg[qoff[m] / D] = (mrow[m] + __log2f(l)) * kLn2;
+    }
+}
+
+// ---- host-side launch ----
+template <int R, int D, typename T, int QM, int SB>
+static hipError_t launch_fwd_inst(const Geo& g, const void* q, const void* k, const void* v,
+                                  void* o, float* lse, float scale, hipStream_t stream) {
+    using C = FwdCfg<R, D, T, QM, SB>;
+    auto kern = na_fwd_kernel<R, D, T, QM, SB>;
+    static bool attr_set = false;
+    if (!attr_set) {
+        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                                           hipFuncAttributeMaxDynamicSharedMemorySize,
+                                           (int)C::kLdsBytes);
+        if (e != hipSuccess) return e;
+        attr_set = true;
+    }
+    hipLaunchKernelGGL(kern, dim3(g.nwg), dim3(C::kThreads), C::kLdsBytes, stream, g,
+                       static_cast<const T*>(q), static_cast<const T*>(k),
+                       static_cast<const T*>(v), static_cast<T*>(o), lse, scale * kLog2e);
+    return hipGetLastError();
+}
+
+template <int R, int D, typename T>
+static hipError_t launch_fwd_qm(const Geo& g, int qm, const void* q, const void* k, const void* v,
+                                void* o, float* lse, float scale, hipStream_t stream) {
+    constexpr int SB = sizeof(T) == 4 ? 2 : 4;
+    if (qm == 1) return launch_fwd_inst<R, D, T, 1, SB>(g, q, k, v, o, lse, scale, stream);
+    return launch_fwd_inst<R, D, T, 2, SB>(g, q, k, v, o, lse, scale, stream);
+}
+
+template <int R, typename T>
+static hipError_t launch_fwd_d(const Geo& g, int D, int qm, const void* q, const void* k,
+                               const void* v, void* o, float* lse, float scale, hipStream_t s) {
+    switch (D) {
+        case 32: return launch_fwd_qm<R, 32, T>(g, qm, q, k, v, o, lse, scale, s);
+        case 64: return launch_fwd_qm<R, 64, T>(g, qm, q, k, v, o, lse, scale, s);
+        case 128: return launch_fwd_qm<R, 128, T>(g, qm, q, k, v, o, lse, scale, s);
+    }
+    return hipErrorInvalidValue;
+}
+
+template <typename T>
+static hipError_t launch_fwd_r(const Geo& g, int rank, int D, int qm, const void* q, const void* k,
+                               const void* v, void* o, float* lse, float scale, hipStream_t s) {
+    switch (rank) {
+        case 1: return launch_fwd_d<1, T>(g, D, qm, q, k, v, o, lse, scale, s);
+        case 2: return launch_fwd_d<2, T>(g, D, qm, q, k, v, o, lse, scale, s);
+        case 3: return launch_fwd_d<3, T>(g, D, qm, q, k, v, o, lse, scale, s);
+    }
+    return hipErrorInvalidValue;
+}
+
+hipError_t launch_forward(const Geo& g, int rank, int D, int dtype, int qm, const void* q,
+                          const void* k, const void* v, void* o, float* lse, float scale,
+                          hipStream_t s) {
+    switch (dtype) {
+        case 0: return launch_fwd_r<float>(g, rank, D, qm, q, k, v, o, lse, scale, s);
+        case 1: return launch_fwd_r<_Float16>(g, rank, D, qm, q, k, v, o, lse, scale, s);
+        case 2: return launch_fwd_r<__bf16>(g, rank, D, qm, q, k, v, o, lse, scale, s);
+    }
+    return hipErrorInvalidValue;
+}
+
+}  // namespace na

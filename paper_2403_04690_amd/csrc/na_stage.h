@@ -1,0 +1,161 @@
+// na_stage.h -- global -> register -> LDS staging of token rows, and the
+// halo geometry those rows come from.
+#pragma once
+
+#include "na_common.h"
+
+namespace na {
+
+// A box of tokens in group coordinates, [lo, lo + E) per axis, cut into rows
+// along the innermost axis and each row into 16-token blocks (rows are padded
+// to a multiple of 16; padding tokens are zero-filled and always masked).
+template <int R>
+struct Box {
+    int lo[kMaxRank];
+    int E[kMaxRank];
+    int nbr;  // blocks per row
+    int nb;   // total blocks
+
+    __device__ __forceinline__ void finish() {
+        nbr = (E[R - 1] + 15) >> 4;
+        nb = nbr;
+#pragma unroll
+        for (int a = 0; a < R - 1; ++a) nb *= E[a];
+    }
+
+    // Outer coordinates (relative to lo) and first inner coordinate of block b.
+    __device__ __forceinline__ void block_coords(int b, int* oc, int& inner0) const {
+        int row = b / nbr;
+        inner0 = (b - row * nbr) * 16;
+#pragma unroll
+        for (int a = R - 2; a >= 0; --a) {
+            oc[a] = row % E[a];
+            row /= E[a];
+        }
+    }
+
+    // Token index (within the (batch, head) slice) of token j of block b;
+    // ok is false for padding and for blocks past the end.
+    __device__ __forceinline__ int token(const Geo& g, const int* gc, int b, int j, bool& ok) const {
+        int oc[kMaxRank];
+        int inner0;
+        block_coords(b, oc, inner0);
+        oc[R - 1] = inner0 + j;
+        ok = (b < nb) && (oc[R - 1] < E[R - 1]);
+        int tok = 0;
+#pragma unroll
+        for (int a = 0; a < R; ++a) tok += (gc[a] + g.d[a] * (lo[a] + oc[a])) * g.ts[a];
+        return tok;
+    }
+};
+
+// Per-wave block tests against a box of the other side: a block is relevant
+// when it intersects [lo, hi) on every axis, and full when it lies inside
+// [flo, fhi) on every axis (all its pairs with the wave's tokens are valid).
+template <int R>
+struct WaveRange {
+    int lo[kMaxRank], hi[kMaxRank], flo[kMaxRank], fhi[kMaxRank];
+
+    __device__ __forceinline__ void test(const Box<R>& box, int b, int* oc, int& inner0, bool& rel,
+                                         bool& full) const {
+        box.block_coords(b, oc, inner0);
+        bool r_ = b < box.nb, f_ = b < box.nb;
+#pragma unroll
+        for (int a = 0; a < R - 1; ++a) {
+            r_ = r_ && oc[a] >= lo[a] && oc[a] < hi[a];
+            f_ = f_ && oc[a] >= flo[a] && oc[a] < fhi[a];
+        }
+        r_ = r_ && inner0 < hi[R - 1] && inner0 + 16 > lo[R - 1];
+        f_ = f_ && inner0 >= flo[R - 1] && inner0 + 16 <= fhi[R - 1];
+        rel = r_;
+        full = f_;
+    }
+};
+
+// Stages ROWS token rows of D elements.  Each thread item is 4 consecutive
+// rows x one 16-byte segment, loaded with 16-byte global loads; rows can then
+// be written row-major (dst[row][d]) and/or transposed (dst[d][row]).
+template <typename T, int D, int ROWS, int NT>
+struct Stager {
+    static constexpr int kVec = Tr<T>::kVec;
+    static constexpr int kSegs = D / kVec;
+    static constexpr int kQuads = ROWS / 4;
+    static constexpr int kItems = (kQuads * kSegs + NT - 1) / NT;
+    i32x4 r[kItems][4];
+
+    template <class TokOf>
+    __device__ __forceinline__ void load(const T* base, int tid, TokOf tok_of_row) {
+#pragma unroll
+        for (int it = 0; it < kItems; ++it) {
+            const int i = tid + it * NT;
+#pragma unroll
+            for (int rr = 0; rr < 4; ++rr) r[it][rr] = i32x4{0, 0, 0, 0};
+            if (i < kQuads * kSegs) {
+                const int quad = i / kSegs, seg = i - quad * kSegs;
+#pragma unroll
+                for (int rr = 0; rr < 4; ++rr) {
+                    bool ok;
+                    const int tok = tok_of_row(quad * 4 + rr, ok);
+                    if (ok) r[it][rr] = ld16<i32x4>(base + (size_t)tok * D + seg * kVec);
+                }
+            }
+        }
+    }
+
+    __device__ __forceinline__ void store_rows(T* dst, int row_stride, int tid) const {
+#pragma unroll
+        for (int it = 0; it < kItems; ++it) {
+            const int i = tid + it * NT;
+            if (i < kQuads * kSegs) {
+                const int quad = i / kSegs, seg = i - quad * kSegs;
+#pragma unroll
+                for (int rr = 0; rr < 4; ++rr)
+                    st16<i32x4>(dst + (quad * 4 + rr) * row_stride + seg * kVec, r[it][rr]);
+            }
+        }
+    }
+
+    __device__ __forceinline__ void store_cols(T* dst, int col_stride, int tid) const {
+#pragma unroll
+        for (int it = 0; it < kItems; ++it) {
+            const int i = tid + it * NT;
+            if (i < kQuads * kSegs) {
+                const int quad = i / kSegs, seg = i - quad * kSegs;
+                T* d0 = dst + (seg * kVec) * col_stride + quad * 4;
+                if constexpr (sizeof(T) == 2) {
+                    // 4 rows x 8 elements -> 8 lines of 4 rows (16-bit pair transpose)
+#pragma unroll
+                    for (int w = 0; w < 4; ++w) {
+                        const uint32_t a0 = r[it][0][w], a1 = r[it][1][w];
+                        const uint32_t a2 = r[it][2][w], a3 = r[it][3][w];
+                        const i32x2 lo = {(int)((a0 & 0xffffu) | (a1 << 16)),
+                                          (int)((a2 & 0xffffu) | (a3 << 16))};
+                        const i32x2 hi = {(int)((a0 >> 16) | (a1 & 0xffff0000u)),
+                                          (int)((a2 >> 16) | (a3 & 0xffff0000u))};
+                        *reinterpret_cast<i32x2*>(d0 + (2 * w) * col_stride) = lo;
+                        *reinterpret_cast<i32x2*>(d0 + (2 * w + 1) * col_stride) = hi;
+                    }
+                } else {
+#pragma unroll
+                    for (int w = 0; w < 4; ++w) {
+                        const i32x4 t = {r[it][0][w], r[it][1][w], r[it][2][w], r[it][3][w]};
+                        st16<i32x4>(d0 + w * col_stride, t);
+                    }
+                }
+            }
+        }
+    }
+};
+
+// LDS row strides: row-major rows get a 16-byte pad, transposed lines a
+// 4-element pad (keeps 16-byte alignment for fp32 and 8-byte for 16-bit).
+template <typename T, int D>
+struct RowLayout {
+    static constexpr int kRow = D + Tr<T>::kVec;
+};
+template <int ROWS>
+struct ColLayout {
+    static constexpr int kCol = ROWS + 4;
+};
+
+}  // namespace na

@@ -1,0 +1,135 @@
+"""Host-side checks of the C ABI (no GPU needed, no kernel launched).
+
+  * libna.so loads and exports every function include/na.h declares;
+  * na_validate and the entry points return each documented error status
+    before touching the device (bad rank, extents, window, dilation, head
+    dim, dtype, scale, NULL or misaligned pointers, short workspace);
+  * an empty batch or head count is a no-op that returns NA_OK.
+"""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "na.h")
+
+NA_OK, NA_ERR_NULL, NA_ERR_RANK, NA_ERR_SHAPE = 0, 1, 2, 3
+NA_ERR_KERNEL_SIZE, NA_ERR_DILATION, NA_ERR_WINDOW, NA_ERR_HEAD_DIM = 4, 5, 6, 7
+NA_ERR_DTYPE, NA_ERR_ALIGNMENT, NA_ERR_WORKSPACE, NA_ERR_HIP, NA_ERR_SCALE = 8, 9, 10, 11, 12
+
+
+@pytest.fixture(scope="module")
+def lib():
+    import paper_2403_04690_amd as na
+
+    if not os.path.exists(na.library_path()):
+        pytest.fail("libna.so is not built (run __graft_entry__.build())")
+    return na.load_library()
+
+
+def _declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    names = re.findall(r"\b(na_[a-z_]+)\s*\(", text)
+    return sorted(set(names))
+
+
+def test_header_declares_expected_entry_points():
+    names = _declared_functions()
+    for n in ("na_forward", "na_backward", "na_backward_workspace_bytes", "na_validate",
+              "na_status_string", "na_debug_windows", "na_version"):
+        assert n in names
+
+
+def test_library_exports_every_declared_symbol(lib):
+    for name in _declared_functions():
+        assert hasattr(lib, name), name
+
+
+def _args(rank=2, ext=(10, 12), ks=(3, 5), ds=(2, 1)):
+    e = (ctypes.c_int64 * len(ext))(*ext)
+    k = (ctypes.c_int32 * len(ks))(*ks)
+    d = (ctypes.c_int32 * len(ds))(*ds)
+    return rank, e, k, d
+
+
+def _validate(lib, rank=2, ext=(10, 12), ks=(3, 5), ds=(2, 1), B=2, H=3, D=64, dt=1, scale=0.125):
+    r, e, k, d = _args(rank, ext, ks, ds)
+    return lib.na_validate(r, e, k, d, B, H, D, dt, scale)
+
+
+def test_validate_statuses(lib):
+    assert _validate(lib) == NA_OK
+    assert _validate(lib, rank=0) == NA_ERR_RANK
+    assert _validate(lib, rank=4, ext=(2, 2, 2, 2), ks=(1,) * 4, ds=(1,) * 4) == NA_ERR_RANK
+    assert _validate(lib, ext=(0, 12)) == NA_ERR_SHAPE
+    assert _validate(lib, ks=(0, 5)) == NA_ERR_KERNEL_SIZE
+    assert _validate(lib, ds=(2, 0)) == NA_ERR_DILATION
+    assert _validate(lib, ks=(6, 5)) == NA_ERR_WINDOW  # 6 * 2 > 10
+    assert _validate(lib, ks=(5, 5), ds=(2, 3)) == NA_ERR_WINDOW  # 5 * 3 > 12
+    assert _validate(lib, ks=(5, 12), ds=(2, 1)) == NA_OK  # k * d == extent is legal
+    for D in (16, 48, 96, 256):
+        assert _validate(lib, D=D) == NA_ERR_HEAD_DIM
+    for D in (32, 64, 128):
+        assert _validate(lib, D=D) == NA_OK
+    assert _validate(lib, dt=3) == NA_ERR_DTYPE
+    assert _validate(lib, scale=float("inf")) == NA_ERR_SCALE
+    assert _validate(lib, scale=float("nan")) == NA_ERR_SCALE
+    assert _validate(lib, B=-1) == NA_ERR_SHAPE
+    # token index limit: N * D must stay below 2^31
+    assert _validate(lib, rank=1, ext=(1 << 25,), ks=(3,), ds=(1,), D=64) == NA_ERR_SHAPE
+    assert _validate(lib, rank=1, ext=(1 << 24,), ks=(3,), ds=(1,), D=64) == NA_OK
+
+
+def test_status_strings(lib):
+    for s in range(13):
+        text = lib.na_status_string(s).decode()
+        assert text and text != "unknown status"
+    assert lib.na_status_string(99).decode() == "unknown status"
+    assert lib.na_version() >= 100
+
+
+FAKE = 0x10000  # aligned, never dereferenced: validation fails first
+
+
+def _fwd(lib, ptrs, **kw):
+    r, e, k, d = _args()
+    B, H, D = kw.get("B", 2), kw.get("H", 3), kw.get("D", 64)
+    return lib.na_forward(r, e, k, d, B, H, D, 1, 0.125, *ptrs, None)
+
+
+def test_forward_rejects_before_launch(lib):
+    good = [FAKE] * 5
+    assert _fwd(lib, [None] + good[1:]) == NA_ERR_NULL
+    assert _fwd(lib, good[:4] + [None]) == NA_ERR_NULL
+    assert _fwd(lib, [FAKE + 2] + good[1:]) == NA_ERR_ALIGNMENT
+    assert _fwd(lib, good[:4] + [FAKE + 4]) == NA_ERR_ALIGNMENT
+    assert _fwd(lib, good, D=80) == NA_ERR_HEAD_DIM
+    # empty batch / heads: a no-op, pointers are not even looked at
+    assert _fwd(lib, [None] * 5, B=0) == NA_OK
+    assert _fwd(lib, [None] * 5, H=0) == NA_OK
+
+
+def test_backward_workspace_and_rejections(lib):
+    r, e, k, d = _args()
+    need = lib.na_backward_workspace_bytes(r, e, 2, 3)
+    assert need >= 2 * 3 * 10 * 12 * 4 and need % 256 == 0
+    ptrs = [FAKE] * 9
+    bwd = lambda p, ws, nbytes, B=2: lib.na_backward(r, e, k, d, B, 3, 64, 1, 0.125, *p, ws, nbytes, None)
+    assert bwd(ptrs, None, need) == NA_ERR_WORKSPACE
+    assert bwd(ptrs, FAKE, need - 1) == NA_ERR_WORKSPACE
+    assert bwd(ptrs, FAKE + 8, need) == NA_ERR_ALIGNMENT
+    assert bwd([None] + ptrs[1:], FAKE, need) == NA_ERR_NULL
+    assert bwd(ptrs[:8] + [FAKE + 1], FAKE, need) == NA_ERR_ALIGNMENT
+    assert bwd([None] * 9, None, 0, B=0) == NA_OK
+    bad_rank = lib.na_backward(0, e, k, d, 2, 3, 64, 1, 0.125, *ptrs, FAKE, need, None)
+    assert bad_rank == NA_ERR_RANK
+
+
+def test_debug_windows_rejects_before_launch(lib):
+    r, e, k, d = _args(ks=(6, 5))
+    assert lib.na_debug_windows(r, e, k, d, FAKE, FAKE, FAKE, None) == NA_ERR_WINDOW
+    r, e, k, d = _args()
+    assert lib.na_debug_windows(r, e, k, d, None, FAKE, FAKE, None) == NA_ERR_NULL

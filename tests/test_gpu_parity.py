@@ -1,0 +1,263 @@
+"""GPU parity of the fused NA kernels against the fp64 oracle (needs an MI355X).
+
+All calls go through libna.so's C ABI (paper_2403_04690_amd binding).  The
+bar: neighbour sets bit-exact; outputs, logsumexp and gradients within 2e-2
+max-abs for fp16/bf16 and 1e-4 for fp32 of the oracle evaluated on the same
+(already rounded) inputs.  Small problems are compared element by element
+(they span several tiles and ragged tails); the five full-size workloads are
+compared in full where the oracle is fast and on sampled rows (borders
+included) otherwise.
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import workloads
+from tests import na_bruteforce as bf
+
+pytestmark = pytest.mark.gpu
+
+TOL = {"fp32": 1e-4, "fp16": 2e-2, "bf16": 2e-2}
+TDT = workloads.TORCH_DTYPE
+
+
+@pytest.fixture(scope="module")
+def na():
+    if not torch.cuda.is_available():
+        pytest.fail("no GPU visible")
+    import paper_2403_04690_amd as lib
+
+    lib.load_library()
+    return lib
+
+
+def _inputs(shape, dtype, seed, n=4):
+    gen = torch.Generator().manual_seed(seed)
+    return [torch.randn(shape, generator=gen).to(TDT[dtype]) for _ in range(n)]
+
+
+def _dev(*ts):
+    return [t.cuda() for t in ts]
+
+
+def _f64(t):
+    return t.detach().cpu().double().numpy()
+
+
+def _maxerr(gpu, ref):
+    return float(np.max(np.abs(_f64(gpu) - ref))) if ref.size else 0.0
+
+
+def _log(msg):
+    print(msg, flush=True)
+
+
+# ---------------------------------------------------------------- index math
+@pytest.mark.parametrize("ext,ks,ds", [
+    ((40,), (7,), (1,)), ((37,), (4,), (3,)), ((32768,), (1023,), (4,)),
+    ((56, 56), (7, 7), (1, 1)), ((128, 128), (13, 13), (2, 2)), ((10, 9), (3, 2), (3, 4)),
+    ((16, 64, 64), (7, 7, 7), (1, 2, 2)), ((5, 12, 7), (5, 1, 2), (1, 6, 3)),
+])
+def test_debug_windows_bit_exact(na, ext, ks, ds):
+    start, ilo, ihi = (t.cpu().numpy() for t in na.debug_windows(ext, ks, ds))
+    off = 0
+    for a, L in enumerate(ext):
+        first, lo, hi, _ = oracle.axis_relation(L, ks[a], ds[a])
+        np.testing.assert_array_equal(start[off:off + L], first)
+        np.testing.assert_array_equal(ilo[off:off + L], lo)
+        np.testing.assert_array_equal(ihi[off:off + L], hi)
+        off += L
+
+
+@pytest.mark.parametrize("ext,ks,ds,dtype", [
+    ((150,), (7,), (2,), "fp32"), ((21, 26), (5, 3), (2, 3), "fp16"),
+    ((6, 9, 10), (3, 5, 3), (2, 1, 3), "bf16"), ((70,), (9,), (1,), "fp16"),
+])
+def test_neighbour_support_probe(na, ext, ks, ds, dtype):
+    """Q = 0 makes P uniform on N(i); one-hot V rows then expose N(i) exactly."""
+    D = 32
+    N = int(np.prod(ext))
+    lists = bf.neighbours(ext, ks, ds)
+    ell = int(np.prod(ks))
+    q = torch.zeros((1, 1) + ext + (D,), dtype=TDT[dtype])
+    k = _inputs(q.shape, dtype, 5, 1)[0]
+    for chunk in range((N + D - 1) // D):
+        v = torch.zeros(1, 1, N, D)
+        for c in range(D):
+            t = chunk * D + c
+            if t < N:
+                v[0, 0, t, c] = 1.0
+        v = v.reshape(q.shape).to(TDT[dtype])
+        out, lse = na.forward(*_dev(q, k, v), ks, ds)
+        o = out.float().cpu().reshape(N, D).numpy()
+        for i in range(N):
+            want = set(t - chunk * D for t in lists[i] if chunk * D <= t < (chunk + 1) * D)
+            got = set(np.nonzero(o[i])[0].tolist())
+            assert got == want, (i, chunk)
+        np.testing.assert_allclose(lse.cpu().numpy(), math.log(ell), atol=1e-5)
+
+
+# ---------------------------------------------------------------- forward
+FWD_CASES = [
+    # (extents, kernel, dilation, head_dim, dtype, batch, heads)
+    ((200,), (7,), (1,), 32, "fp32", 1, 2),
+    ((300,), (13,), (3,), 64, "fp16", 2, 2),
+    ((129,), (1,), (2,), 128, "bf16", 1, 3),
+    ((257,), (64,), (4,), 64, "fp16", 1, 2),
+    ((1000,), (255,), (2,), 64, "bf16", 1, 2),
+    ((70,), (70,), (1,), 32, "fp16", 2, 1),
+    ((37, 45), (7, 5), (2, 1), 32, "fp16", 2, 2),
+    ((20, 23), (3, 3), (3, 2), 64, "bf16", 1, 3),
+    ((16, 16), (16, 16), (1, 1), 64, "fp32", 1, 2),
+    ((9, 50), (9, 1), (1, 3), 128, "fp16", 1, 2),
+    ((33, 31), (13, 13), (2, 2), 64, "bf16", 1, 2),
+    ((6, 20, 22), (3, 7, 5), (1, 2, 2), 64, "fp16", 1, 2),
+    ((5, 9, 11), (5, 3, 3), (1, 3, 3), 32, "fp32", 2, 1),
+    ((8, 12, 12), (7, 7, 7), (1, 1, 1), 64, "bf16", 1, 1),
+    ((4, 4, 4), (4, 4, 4), (1, 1, 1), 128, "fp16", 1, 2),
+]
+
+
+@pytest.mark.parametrize("ext,ks,ds,D,dtype,B,H", FWD_CASES)
+def test_forward_small(na, ext, ks, ds, D, dtype, B, H):
+    shape = (B, H) + ext + (D,)
+    q, k, v = _inputs(shape, dtype, 11, 3)
+    out, lse = na.forward(*_dev(q, k, v), ks, ds)
+    ro, rl = oracle.forward(_f64(q), _f64(k), _f64(v), ks, ds, 1.0 / math.sqrt(D))
+    eo, el = _maxerr(out, ro), _maxerr(lse, rl)
+    _log(f"fwd {ext} k={ks} d={ds} D={D} {dtype}: max|dO|={eo:.3g} max|dLSE|={el:.3g}")
+    assert eo <= TOL[dtype] and el <= TOL[dtype]
+
+
+def test_forward_window_one_is_exact_copy(na):
+    for dtype in ("fp16", "bf16", "fp32"):
+        shape = (2, 2, 13, 17, 64)
+        q, k, v = _inputs(shape, dtype, 12, 3)
+        out, lse = na.forward(*_dev(q, k, v), (1, 1), (3, 2))
+        assert torch.equal(out.cpu(), v), dtype
+        ref = (q.double() * k.double()).sum(-1) / 8.0
+        assert float((lse.cpu().double() - ref).abs().max()) <= TOL[dtype]
+
+
+def test_forward_deterministic_and_empty(na):
+    shape = (1, 2, 24, 40, 64)
+    q, k, v = _dev(*_inputs(shape, "fp16", 13, 3))
+    a, la = na.forward(q, k, v, (5, 7), (2, 3))
+    b, lb = na.forward(q, k, v, (5, 7), (2, 3))
+    assert torch.equal(a, b) and torch.equal(la, lb)
+    z = torch.empty((0, 2, 24, 40, 64), dtype=torch.float16, device="cuda")
+    o, l = na.forward(z, z, z, (5, 7), (2, 3))
+    assert o.shape == z.shape
+
+
+# ---------------------------------------------------------------- backward
+BWD_CASES = [
+    ((200,), (7,), (1,), 32, "fp32", 1, 2),
+    ((300,), (13,), (3,), 64, "fp16", 1, 2),
+    ((257,), (64,), (4,), 64, "bf16", 1, 1),
+    ((37, 45), (7, 5), (2, 1), 32, "fp16", 1, 2),
+    ((20, 23), (3, 3), (3, 2), 64, "bf16", 1, 2),
+    ((16, 16), (16, 16), (1, 1), 64, "fp32", 1, 1),
+    ((33, 31), (13, 13), (2, 2), 64, "bf16", 1, 1),
+    ((9, 50), (9, 1), (1, 3), 128, "fp16", 1, 1),
+    ((6, 20, 22), (3, 7, 5), (1, 2, 2), 64, "fp16", 1, 1),
+    ((5, 9, 11), (5, 3, 3), (1, 3, 3), 32, "fp32", 1, 2),
+    ((8, 12, 12), (7, 7, 7), (1, 1, 1), 128, "bf16", 1, 1),
+]
+
+
+@pytest.mark.parametrize("ext,ks,ds,D,dtype,B,H", BWD_CASES)
+def test_backward_small(na, ext, ks, ds, D, dtype, B, H):
+    shape = (B, H) + ext + (D,)
+    q, k, v, g = _inputs(shape, dtype, 21, 4)
+    dq_, dk_, dv_, dg_ = _dev(q, k, v, g)
+    out, lse = na.forward(dq_, dk_, dv_, ks, ds)
+    dq, dk, dv = na.backward(dq_, dk_, dv_, out, lse, dg_, ks, ds)
+    rq, rk, rv = oracle.backward(_f64(q), _f64(k), _f64(v), _f64(g), ks, ds, 1.0 / math.sqrt(D))
+    e = [_maxerr(dq, rq), _maxerr(dk, rk), _maxerr(dv, rv)]
+    _log(f"bwd {ext} k={ks} d={ds} D={D} {dtype}: max err dq/dk/dv = {e}")
+    assert max(e) <= TOL[dtype]
+
+
+def test_backward_deterministic(na):
+    shape = (1, 2, 30, 27, 64)
+    q, k, v, g = _dev(*_inputs(shape, "bf16", 22, 4))
+    out, lse = na.forward(q, k, v, (7, 5), (2, 3))
+    a = na.backward(q, k, v, out, lse, g, (7, 5), (2, 3))
+    b = na.backward(q, k, v, out, lse, g, (7, 5), (2, 3))
+    for x, y in zip(a, b):
+        assert torch.equal(x, y)
+
+
+def test_autograd_function_matches_explicit_calls(na):
+    shape = (1, 2, 19, 64)
+    q, k, v, g = _dev(*_inputs(shape, "fp32", 23, 4))
+    qq, kk, vv = (t.clone().requires_grad_(True) for t in (q, k, v))
+    o = na.na_attention(qq, kk, vv, 5, 2)
+    o.backward(g)
+    out, lse = na.forward(q, k, v, 5, 2)
+    dq, dk, dv = na.backward(q, k, v, out, lse, g, 5, 2)
+    assert torch.equal(o.detach(), out)
+    for a, b in ((qq.grad, dq), (kk.grad, dk), (vv.grad, dv)):
+        assert torch.equal(a, b)
+
+
+# ---------------------------------------------------------------- full-size workloads
+def _border_rows(p, count, seed):
+    """Sampled flat rows of [B*H*N]: random ones plus every token on a corner of the volume."""
+    rows = set(workloads.sample_rows(p.batch * p.heads * p.tokens, count, seed).tolist())
+    corners = []
+    for c in np.ndindex(*([2] * p.rank)):
+        coord = [0 if b == 0 else e - 1 for b, e in zip(c, p.extents)]
+        t = 0
+        for x, e in zip(coord, p.extents):
+            t = t * e + x
+        corners.append(t)
+    for bh in (0, p.batch * p.heads - 1):
+        rows.update(bh * p.tokens + t for t in corners)
+    return np.array(sorted(rows), dtype=np.int64)
+
+
+@pytest.mark.parametrize("name", workloads.CONFIG_ORDER)
+def test_full_workload_forward(na, name):
+    p = workloads.CONFIGS[name]
+    _log(f"[full fwd] {p.describe()}")
+    x = workloads.make_inputs(p, seed=0, with_grad=False)
+    out, lse = na.forward(*_dev(x["q"], x["k"], x["v"]), p.kernel_size, p.dilation,
+                          p.softmax_scale)
+    torch.cuda.synchronize()
+    qd, kd, vd = (_f64(x[n]) for n in ("q", "k", "v"))
+    if p.tokens * p.batch * p.heads * p.window <= 4_000_000:
+        ro, rl = oracle.forward(qd, kd, vd, p.kernel_size, p.dilation, p.softmax_scale)
+        eo, el = _maxerr(out, ro), _maxerr(lse, rl)
+    else:
+        rows = _border_rows(p, 1536, seed=3)
+        ro, rl = oracle.forward_rows(qd, kd, vd, p.kernel_size, p.dilation, p.softmax_scale, rows)
+        eo = float(np.max(np.abs(_f64(out).reshape(-1, p.head_dim)[rows] - ro)))
+        el = float(np.max(np.abs(_f64(lse).reshape(-1)[rows] - rl)))
+    _log(f"[full fwd] {name}: max|dO|={eo:.3g} max|dLSE|={el:.3g}")
+    assert eo <= TOL[p.dtype] and el <= TOL[p.dtype]
+
+
+@pytest.mark.parametrize("name", [n for n in workloads.CONFIG_ORDER if workloads.CONFIGS[n].backward])
+def test_full_workload_backward(na, name):
+    p = workloads.CONFIGS[name]
+    _log(f"[full bwd] {p.describe()}")
+    x = workloads.make_inputs(p, seed=0, with_grad=True)
+    q, k, v, g = _dev(x["q"], x["k"], x["v"], x["dout"])
+    out, lse = na.forward(q, k, v, p.kernel_size, p.dilation, p.softmax_scale)
+    dq, dk, dv = na.backward(q, k, v, out, lse, g, p.kernel_size, p.dilation, p.softmax_scale)
+    torch.cuda.synchronize()
+    qrows = _border_rows(p, 384, seed=4)
+    krows = _border_rows(p, 96, seed=5)
+    rq, rk, rv = oracle.backward_rows(*(_f64(x[n]) for n in ("q", "k", "v", "dout")),
+                                      p.kernel_size, p.dilation, p.softmax_scale, qrows, krows)
+    D = p.head_dim
+    e = [float(np.max(np.abs(_f64(dq).reshape(-1, D)[qrows] - rq))),
+         float(np.max(np.abs(_f64(dk).reshape(-1, D)[krows] - rk))),
+         float(np.max(np.abs(_f64(dv).reshape(-1, D)[krows] - rv)))]
+    _log(f"[full bwd] {name}: max err dq/dk/dv = {e}")
+    assert max(e) <= TOL[p.dtype]
