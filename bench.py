@@ -74,7 +74,7 @@ def cpu_baseline(problem, x, budget_s):
         "unit": "TFLOP/s",
         "cores": oracle.num_threads(),
         "kind": "oracle",
-        "sample": f"full {WORKLOAD} forward (all {problem.batch * problem.heads * problem.tokens}"
+        "sample": f"full {problem.name} forward (all {problem.batch * problem.heads * problem.tokens}"
                   f" queries) x {reps} repetitions in {el:.1f} s, fp64",
     }
 
@@ -86,7 +86,22 @@ def main():
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--workload", default=WORKLOAD, choices=workloads.CONFIG_ORDER,
+                    help="profiling aid: run the same step on another workload (the reported "
+                         "line is defined on the default one)")
+    ap.add_argument("--copy-probe-mib", type=int, default=0,
+                    help="counter calibration: only run 5 device-to-device copies of this many "
+                         "MiB (the HBM traffic of each is known) and exit")
     args = ap.parse_args()
+    if args.copy_probe_mib:
+        n = args.copy_probe_mib << 20
+        src = torch.ones(n, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(5):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_probe_bytes": n, "copies": 5}), flush=True)
+        return
     if args.gpus != 1:
         print(f"bench.py: this build runs on exactly one GPU; --gpus {args.gpus} is not supported",
               file=sys.stderr)
@@ -96,7 +111,7 @@ def main():
 
     na.load_library()
     dev = torch.device("cuda", 0)
-    p = workloads.CONFIGS[WORKLOAD]
+    p = workloads.CONFIGS[args.workload]
     x = workloads.make_inputs(p, seed=0, with_grad=True)
     q, k, v, g = (x[n].to(dev) for n in ("q", "k", "v", "dout"))
     out = torch.empty_like(q)
@@ -119,14 +134,29 @@ def main():
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
+    # host cost of enqueueing one step (no synchronisation inside)
+    t0 = time.perf_counter()
+    for _ in range(max(args.warmup, 5)):
+        step()
+    host_step_s = (time.perf_counter() - t0) / max(args.warmup, 5)
+    torch.cuda.synchronize()
+    # rate of the GPU-side spin used to give the host a head start
+    s0, s1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    s0.record()
+    torch.cuda._sleep(1_000_000)
+    s1.record()
+    torch.cuda.synchronize()
+    spin_s_per_cycle = s0.elapsed_time(s1) * 1e-3 / 1_000_000
 
     K = args.steps
     ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(K)]
     ev_end = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
-    # Give the host a head start (a GPU-side spin before the first step) so the
-    # launches below queue up and the GPU runs the K steps back to back.
-    torch.cuda._sleep(int(2e7))
+    # Head start: a GPU-side spin long enough for the host to enqueue all K
+    # steps, so the GPU then runs them back to back (the spin is outside the
+    # events that time the steps).
+    head_s = min(2.0 * K * host_step_s + 1e-3, 5.0)
+    torch.cuda._sleep(int(head_s / max(spin_s_per_cycle, 1e-12)))
     for i in range(K):
         step(*ev[i])
     ev_end.record()
@@ -152,10 +182,10 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "f16",
+        "dtype": {"fp16": "f16", "bf16": "bf16", "fp32": "f32"}[p.dtype],
         "data": "synthetic: iid N(0,1) q, k, v, dO (torch CPU generator, seed 0), rounded to fp16",
         "config": {
-            "workload": WORKLOAD,
+            "workload": p.name,
             "rank": p.rank, "batch": p.batch, "heads": p.heads, "extents": list(p.extents),
             "head_dim": p.head_dim, "kernel_size": list(p.kernel_size),
             "dilation": list(p.dilation), "step": "na_forward + na_backward",
@@ -163,6 +193,7 @@ def main():
         "fwd_ms": round(fwd_ms, 5),
         "bwd_ms": round(bwd_ms, 5),
         "fwd_bwd_ms": round(step_ms, 5),
+        "host_enqueue_ms_per_step": round(host_step_s * 1e3, 4),
         "mfma_peak_frac": round(fwd_tflops / PEAK_FP16_TFLOPS, 5),
         "roofline": {
             "kernel": "na_fwd_kernel",
