@@ -164,13 +164,15 @@ __global__ __launch_bounds__(256) void na_dq_kernel(Geo g, const T* __restrict__
         dlt[m] = ok ? deltag[qoff[m] / D] : 0.f;
     }
 
+    const int tstep = g.d[R - 1];
     typename C::Stg kst, vst;
+    typename C::Stg::Addr addr;
     auto load_stage = [&](int s) {
-        auto tok_of = [&](int row, bool& ok) {
-            return halo.token(g, gc, s * SB + (row >> 4), row & 15, ok);
-        };
-        kst.load(kb, tid, tok_of);
-        vst.load(vb, tid, tok_of);
+        addr.compute(tid, [&](int quad, int& cnt) {
+            return halo.quad_token(g, gc, s * SB + (quad >> 2), (quad & 3) * 4, cnt);
+        });
+        kst.load(kb, tid, addr, tstep);
+        vst.load(vb, tid, addr, tstep);
     };
     auto store_stage = [&](int buf) {
         T* base = smem + buf * C::kBufElems;
@@ -394,17 +396,21 @@ __global__ __launch_bounds__(256) void na_dkdv_kernel(Geo g, const T* __restrict
         }
     }
 
+    const int tstep = g.d[R - 1];
     typename C::Stg qst, gst;
+    typename C::Stg::Addr addr;
     float lse_reg = 0.f, dlt_reg = 0.f;
     auto load_stage = [&](int s) {
-        auto tok_of = [&](int row, bool& ok) {
-            return ibox.token(g, gc, s * SB + (row >> 4), row & 15, ok);
-        };
-        qst.load(qb, tid, tok_of);
-        gst.load(gb, tid, tok_of);
+        addr.compute(tid, [&](int quad, int& cnt) {
+            return ibox.quad_token(g, gc, s * SB + (quad >> 2), (quad & 3) * 4, cnt);
+        });
+        qst.load(qb, tid, addr, tstep);
+        gst.load(gb, tid, addr, tstep);
         if (tid < C::kRows) {
-            bool ok;
-            const int tok = tok_of(tid, ok);
+            int cnt;
+            const int tok = ibox.quad_token(g, gc, s * SB + (tid >> 4), tid & 12, cnt) +
+                            (tid & 3) * tstep;
+            const bool ok = (tid & 3) < cnt;
             lse_reg = ok ? lb[tok] * kLog2e : 0.f;
             dlt_reg = ok ? db_[tok] : 0.f;
         }

@@ -127,6 +127,26 @@ __device__ __forceinline__ void st_x4(T* p, f32x4 v) {
     }
 }
 
+// Reductions over the four 16-lane groups holding the same column, with the
+// gfx950 lane-swap instructions (VALU, no LDS traffic): permlane16_swap pairs
+// groups (0,1) and (2,3), permlane32_swap pairs (0,2) and (1,3).
+__device__ __forceinline__ float group_max4(float x) {
+    const unsigned u = __float_as_uint(x);
+    const auto a = __builtin_amdgcn_permlane16_swap(u, u, false, false);
+    x = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+    const unsigned v = __float_as_uint(x);
+    const auto b = __builtin_amdgcn_permlane32_swap(v, v, false, false);
+    return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
+}
+__device__ __forceinline__ float group_sum4(float x) {
+    const unsigned u = __float_as_uint(x);
+    const auto a = __builtin_amdgcn_permlane16_swap(u, u, false, false);
+    x = __uint_as_float(a[0]) + __uint_as_float(a[1]);
+    const unsigned v = __float_as_uint(x);
+    const auto b = __builtin_amdgcn_permlane32_swap(v, v, false, false);
+    return __uint_as_float(b[0]) + __uint_as_float(b[1]);
+}
+
 __device__ __forceinline__ float wave_max_groups(float x) {
     // max over the four 16-lane groups holding the same column
     x = fmaxf(x, __shfl_xor(x, 16, kWave));

@@ -11,20 +11,29 @@
 //   * workgroup = 4 waves = one query tile of one (batch, head, dilation
 //     group); each wave owns QM x 16 queries of it (a sub-box);
 //   * the workgroup's key halo is cut into blocks of 16 keys that run along
-//     the innermost axis; stages of SB blocks are staged in LDS,
-//     double-buffered, K row-major and V transposed, by 16-byte loads;
+//     the innermost axis; stages of SB blocks are staged in LDS (double
+//     buffered when there is more than one stage), K row-major and V
+//     transposed, by 16-byte loads whose addresses are computed once per
+//     4 keys and shared by K and V;
 //   * a wave only runs the matrix cores on blocks that intersect its own
 //     sub-box halo, and evaluates the mask only on blocks that are not inside
 //     every one of its windows;
 //   * S^T = K Q^T (16 keys x 16 queries per MFMA) leaves each query's scores
-//     in one lane column, so softmax statistics stay per lane except for a
-//     two-step cross-group max, and P^T feeds O^T = V^T P^T directly as the B
-//     operand;
-//   * scores are kept in base 2 (scale * log2 e folded into one multiply).
+//     in one lane column; the row maximum needs two lane-swap steps, and P^T
+//     feeds O^T = V^T P^T directly as the B operand;
+//   * scores are scaled once into base 2 (so the row maximum maps to exactly
+//     exp2(0) = 1 and a window of one key returns V bit for bit); the running
+//     maximum is only raised (and O rescaled) when a row's maximum grows by
+//     more than kLazy, which keeps every P <= 2^kLazy.
+#include <algorithm>
+#include <cmath>
+
 #include "na_launch.h"
 #include "na_stage.h"
 
 namespace na {
+
+constexpr float kLazy = 8.f;  // base-2 headroom before the running max is raised
 
 template <int R, int D, typename T, int QM, int SB>
 struct FwdCfg {
@@ -35,17 +44,18 @@ struct FwdCfg {
     static constexpr int kKElems = kKeys * kKRow;
     static constexpr int kVElems = D * kVCol;
     static constexpr int kBufElems = kKElems + kVElems;
-    static constexpr size_t kLdsBytes = 2 * kBufElems * sizeof(T);
+    static constexpr size_t kBufBytes = kBufElems * sizeof(T);
     static constexpr int kKS = D / 32;  // contraction steps over D
     static constexpr int kDB = D / 16;  // 16-wide blocks of D
     using Stg = Stager<T, D, kKeys, kThreads>;
 };
 
+// c = scale * log2(e): scores are kept in base 2.
 template <int R, int D, typename T, int QM, int SB>
 __global__ __launch_bounds__(256) void na_fwd_kernel(Geo g, const T* __restrict__ qg,
                                                      const T* __restrict__ kg,
                                                      const T* __restrict__ vg, T* __restrict__ og,
-                                                     float* __restrict__ lseg, float scale_log2) {
+                                                     float* __restrict__ lseg, float c) {
     using C = FwdCfg<R, D, T, QM, SB>;
     using x8 = typename Tr<T>::x8;
     extern __shared__ __align__(16) unsigned char smem_raw[];
@@ -84,6 +94,7 @@ __global__ __launch_bounds__(256) void na_fwd_kernel(Geo g, const T* __restrict_
     const size_t slice = (size_t)bh * g.N * D;
     const T* kb = kg + slice;
     const T* vb = vg + slice;
+    const int tstep = g.d[R - 1];  // token step along the innermost axis
 
     // ---- this wave's query sub-box: its halo and the keys inside all of its windows ----
     int wc[kMaxRank], wo[kMaxRank];
@@ -110,13 +121,13 @@ __global__ __launch_bounds__(256) void na_fwd_kernel(Geo g, const T* __restrict_
     x8 qf[QM][C::kKS];
 #pragma unroll
     for (int m = 0; m < QM; ++m) {
-        int c[kMaxRank];
-        unravel<R>(m * 16 + col, g.WT, c);
+        int cc[kMaxRank];
+        unravel<R>(m * 16 + col, g.WT, cc);
         bool ok = wave_live;
         int tok = 0;
 #pragma unroll
         for (int a = 0; a < R; ++a) {
-            int p = wo[a] + c[a];
+            int p = wo[a] + cc[a];
             if (p >= n[a]) ok = false;
             p = min(p, n[a] - 1);
             qs[m][a] = win_start(p, n[a], g.k[a]) - halo.lo[a];
@@ -129,14 +140,15 @@ __global__ __launch_bounds__(256) void na_fwd_kernel(Geo g, const T* __restrict_
             qf[m][s] = ok ? ld_x8<T>(qg + qoff[m] + s * 32 + grp * 8) : zero_x8<T>();
     }
 
-    // ---- staging of K (row-major) and V (transposed) ----
+    // ---- staging of K (row-major) and V (transposed), one address set for both ----
     typename C::Stg kst, vst;
+    typename C::Stg::Addr addr;
     auto load_stage = [&](int s) {
-        auto tok_of = [&](int row, bool& ok) {
-            return halo.token(g, gc, s * SB + (row >> 4), row & 15, ok);
-        };
-        kst.load(kb, tid, tok_of);
-        vst.load(vb, tid, tok_of);
+        addr.compute(tid, [&](int quad, int& cnt) {
+            return halo.quad_token(g, gc, s * SB + (quad >> 2), (quad & 3) * 4, cnt);
+        });
+        kst.load(kb, tid, addr, tstep);
+        vst.load(vb, tid, addr, tstep);
     };
     auto store_stage = [&](int buf) {
         T* ks = smem + buf * C::kBufElems;
@@ -146,10 +158,10 @@ __global__ __launch_bounds__(256) void na_fwd_kernel(Geo g, const T* __restrict_
 
     // ---- online-softmax state (per lane: its query column) ----
     f32x4 oacc[QM][C::kDB];
-    float mrow[QM], lrow[QM];
+    float mref[QM], lrow[QM];
 #pragma unroll
     for (int m = 0; m < QM; ++m) {
-        mrow[m] = -INFINITY;
+        mref[m] = -INFINITY;
         lrow[m] = 0.f;
 #pragma unroll
         for (int db = 0; db < C::kDB; ++db) oacc[m][db] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -166,7 +178,7 @@ __global__ __launch_bounds__(256) void na_fwd_kernel(Geo g, const T* __restrict_
         const T* vt = ks + C::kKElems;
 
         if (wave_live) {
-#pragma unroll 1
+#pragma unroll
             for (int tp = 0; tp < SB / 2; ++tp) {
                 bool rel[2], full[2];
                 int boc[2][kMaxRank], bin0[2];
@@ -196,41 +208,52 @@ __global__ __launch_bounds__(256) void na_fwd_kernel(Geo g, const T* __restrict_
                 x8 pf[QM];
 #pragma unroll
                 for (int m = 0; m < QM; ++m) {
-                    float t[2][4];
+                    float sv[2][4];
                     float tmax = -INFINITY;
 #pragma unroll
                     for (int bi = 0; bi < 2; ++bi) {
-                        bool outer_ok = rel[bi];
+                        if (full[bi]) {
 #pragma unroll
-                        for (int a = 0; a < R - 1; ++a)
-                            outer_ok = outer_ok && (unsigned)(boc[bi][a] - qs[m][a]) < (unsigned)g.k[a];
-                        const int base = bin0[bi] + grp * 4 - qs[m][R - 1];
+                            for (int r = 0; r < 4; ++r) sv[bi][r] = sacc[m][bi][r] * c;
+                        } else {
+                            bool outer_ok = rel[bi];
 #pragma unroll
-                        for (int r = 0; r < 4; ++r) {
-                            const bool ok = full[bi] ||
-                                            (outer_ok && (unsigned)(base + r) < (unsigned)g.k[R - 1]);
-                            const float x = ok ? sacc[m][bi][r] * scale_log2 : -INFINITY;
-                            t[bi][r] = x;
-                            tmax = fmaxf(tmax, x);
+                            for (int a = 0; a < R - 1; ++a)
+                                outer_ok = outer_ok &&
+                                           (unsigned)(boc[bi][a] - qs[m][a]) < (unsigned)g.k[a];
+                            const int base = bin0[bi] + grp * 4 - qs[m][R - 1];
+#pragma unroll
+                            for (int r = 0; r < 4; ++r) {
+                                const bool ok =
+                                    outer_ok && (unsigned)(base + r) < (unsigned)g.k[R - 1];
+                                sv[bi][r] = ok ? sacc[m][bi][r] * c : -INFINITY;
+                            }
                         }
+#pragma unroll
+                        for (int r = 0; r < 4; ++r) tmax = fmaxf(tmax, sv[bi][r]);
                     }
-                    tmax = wave_max_groups(tmax);
-                    const float mnew = fmaxf(mrow[m], tmax);
-                    const float muse = mnew == -INFINITY ? 0.f : mnew;
-                    const float alpha = fast_exp2(mrow[m] - muse);
-                    mrow[m] = mnew;
+                    // tile maximum of this query, in base-2 units
+                    const float t = group_max4(tmax);
+                    const bool raise = t > mref[m] + kLazy;
+                    if (__builtin_amdgcn_ballot_w64(raise)) {
+                        // lanes that do not raise keep their reference (alpha = 1)
+                        const float alpha = raise ? fast_exp2(mref[m] - t) : 1.f;
+                        mref[m] = raise ? t : mref[m];
+                        lrow[m] *= alpha;
+#pragma unroll
+                        for (int db = 0; db < C::kDB; ++db) oacc[m][db] *= alpha;
+                    }
+                    const float negm = mref[m] == -INFINITY ? 0.f : -mref[m];
                     float p[2][4];
                     float psum = 0.f;
 #pragma unroll
                     for (int bi = 0; bi < 2; ++bi)
 #pragma unroll
                         for (int r = 0; r < 4; ++r) {
-                            p[bi][r] = fast_exp2(t[bi][r] - muse);
+                            p[bi][r] = fast_exp2(sv[bi][r] + negm);
                             psum += p[bi][r];
                         }
-                    lrow[m] = lrow[m] * alpha + psum;
-#pragma unroll
-                    for (int db = 0; db < C::kDB; ++db) oacc[m][db] *= alpha;
+                    lrow[m] += psum;
                     pf[m] = x8{Tr<T>::cvt(p[0][0]), Tr<T>::cvt(p[0][1]), Tr<T>::cvt(p[0][2]),
                                Tr<T>::cvt(p[0][3]), Tr<T>::cvt(p[1][0]), Tr<T>::cvt(p[1][1]),
                                Tr<T>::cvt(p[1][2]), Tr<T>::cvt(p[1][3])};
@@ -254,31 +277,42 @@ __global__ __launch_bounds__(256) void na_fwd_kernel(Geo g, const T* __restrict_
     // ---- epilogue: normalise, store O (rounded once) and the natural-log LSE ----
 #pragma unroll
     for (int m = 0; m < QM; ++m) {
-        const float l = wave_sum_groups(lrow[m]);
+        const float l = group_sum4(lrow[m]);
         if (!qvalid[m]) continue;
         const float inv = 1.f / l;
 #pragma unroll
         for (int db = 0; db < C::kDB; ++db)
             st_x4<T>(og + qoff[m] + db * 16 + grp * 4, oacc[m][db] * inv);
-        if (grp == 0) lseg[qoff[m] / D] = (mrow[m] + __log2f(l)) * kLn2;
+        if (grp == 0) lseg[qoff[m] / D] = (mref[m] + __log2f(l)) * kLn2;
     }
 }
 
 // ---- host-side launch ----
+// Largest number of 16-key blocks in any workgroup's halo (interior tiles).
+static int max_halo_blocks(const Geo& g, int rank) {
+    int nb = 1;
+    for (int a = 0; a < rank; ++a) {
+        const int n0 = group_len(g.L[a], g.d[a], 0);
+        int e = std::min(g.T[a], n0) + g.k[a] - 1;
+        e = std::min(e, n0);
+        nb *= (a == rank - 1) ? (e + 15) / 16 : e;
+    }
+    return nb;
+}
+
 template <int R, int D, typename T, int QM, int SB>
 static hipError_t launch_fwd_inst(const Geo& g, const void* q, const void* k, const void* v,
                                   void* o, float* lse, float scale, hipStream_t stream) {
     using C = FwdCfg<R, D, T, QM, SB>;
     auto kern = na_fwd_kernel<R, D, T, QM, SB>;
-    static bool attr_set = false;
-    if (!attr_set) {
+    const int nst_max = (max_halo_blocks(g, R) + SB - 1) / SB;
+    const size_t lds = (nst_max > 1 ? 2 : 1) * C::kBufBytes;
+    if (lds > 65536) {
         hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
-                                           hipFuncAttributeMaxDynamicSharedMemorySize,
-                                           (int)C::kLdsBytes);
+                                           hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
         if (e != hipSuccess) return e;
-        attr_set = true;
     }
-    hipLaunchKernelGGL(kern, dim3(g.nwg), dim3(C::kThreads), C::kLdsBytes, stream, g,
+    hipLaunchKernelGGL(kern, dim3(g.nwg), dim3(C::kThreads), lds, stream, g,
                        static_cast<const T*>(q), static_cast<const T*>(k),
                        static_cast<const T*>(v), static_cast<T*>(o), lse, scale * kLog2e);
     return hipGetLastError();
@@ -287,9 +321,20 @@ static hipError_t launch_fwd_inst(const Geo& g, const void* q, const void* k, co
 template <int R, int D, typename T>
 static hipError_t launch_fwd_qm(const Geo& g, int qm, const void* q, const void* k, const void* v,
                                 void* o, float* lse, float scale, hipStream_t stream) {
-    constexpr int SB = sizeof(T) == 4 ? 2 : 4;
-    if (qm == 1) return launch_fwd_inst<R, D, T, 1, SB>(g, q, k, v, o, lse, scale, stream);
-    return launch_fwd_inst<R, D, T, 2, SB>(g, q, k, v, o, lse, scale, stream);
+    if constexpr (sizeof(T) == 4) {
+        if (qm == 1) return launch_fwd_inst<R, D, T, 1, 2>(g, q, k, v, o, lse, scale, stream);
+        return launch_fwd_inst<R, D, T, 2, 2>(g, q, k, v, o, lse, scale, stream);
+    } else {
+        // one LDS stage covering the whole halo when it is small and D is 32
+        if constexpr (D == 32) {
+            if (max_halo_blocks(g, R) <= 16) {
+                if (qm == 1) return launch_fwd_inst<R, D, T, 1, 16>(g, q, k, v, o, lse, scale, stream);
+                return launch_fwd_inst<R, D, T, 2, 16>(g, q, k, v, o, lse, scale, stream);
+            }
+        }
+        if (qm == 1) return launch_fwd_inst<R, D, T, 1, 4>(g, q, k, v, o, lse, scale, stream);
+        return launch_fwd_inst<R, D, T, 2, 4>(g, q, k, v, o, lse, scale, stream);
+    }
 }
 
 template <int R, typename T>

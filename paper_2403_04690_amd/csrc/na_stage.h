@@ -6,6 +6,23 @@
 
 namespace na {
 
+// Division by a runtime divisor that stays fixed for a whole workgroup:
+// q = (umulhi(n, mul) + n) >> shr, exact for 0 <= n < 2^31 and d >= 1.
+struct FastDiv {
+    uint32_t mul, shr;
+    int d;
+    __device__ __forceinline__ void init(int d_) {
+        d = d_;
+        uint32_t s = 0;
+        while ((1u << s) < (uint32_t)d_) ++s;
+        shr = s;
+        mul = (uint32_t)((((uint64_t)1 << 32) * (((uint64_t)1 << s) - (uint64_t)d_)) / (uint64_t)d_ + 1);
+    }
+    __device__ __forceinline__ int div(int n) const {
+        return (int)((__umulhi((uint32_t)n, mul) + (uint32_t)n) >> shr);
+    }
+};
+
 // A box of tokens in group coordinates, [lo, lo + E) per axis, cut into rows
 // along the innermost axis and each row into 16-token blocks (rows are padded
 // to a multiple of 16; padding tokens are zero-filled and always masked).
@@ -15,33 +32,43 @@ struct Box {
     int E[kMaxRank];
     int nbr;  // blocks per row
     int nb;   // total blocks
+    FastDiv fd_nbr;
+    FastDiv fd_E[kMaxRank];
 
     __device__ __forceinline__ void finish() {
         nbr = (E[R - 1] + 15) >> 4;
         nb = nbr;
 #pragma unroll
         for (int a = 0; a < R - 1; ++a) nb *= E[a];
+        fd_nbr.init(nbr);
+#pragma unroll
+        for (int a = 1; a < R - 1; ++a) fd_E[a].init(E[a]);
     }
 
     // Outer coordinates (relative to lo) and first inner coordinate of block b.
     __device__ __forceinline__ void block_coords(int b, int* oc, int& inner0) const {
-        int row = b / nbr;
+        int row = fd_nbr.div(b);
         inner0 = (b - row * nbr) * 16;
 #pragma unroll
-        for (int a = R - 2; a >= 0; --a) {
-            oc[a] = row % E[a];
-            row /= E[a];
+        for (int a = R - 2; a >= 1; --a) {
+            const int nx = fd_E[a].div(row);
+            oc[a] = row - nx * E[a];
+            row = nx;
         }
+        if (R >= 2) oc[0] = row;
     }
 
-    // Token index (within the (batch, head) slice) of token j of block b;
-    // ok is false for padding and for blocks past the end.
-    __device__ __forceinline__ int token(const Geo& g, const int* gc, int b, int j, bool& ok) const {
+    // Token (within the (batch, head) slice) of token j0 of block b, and how
+    // many of the tokens j0 .. j0+3 exist (0 for blocks past the end).
+    // Consecutive tokens of a block are g.d[R-1] tokens apart.
+    __device__ __forceinline__ int quad_token(const Geo& g, const int* gc, int b, int j0,
+                                              int& cnt) const {
         int oc[kMaxRank];
         int inner0;
         block_coords(b, oc, inner0);
-        oc[R - 1] = inner0 + j;
-        ok = (b < nb) && (oc[R - 1] < E[R - 1]);
+        oc[R - 1] = inner0 + j0;
+        const int left = E[R - 1] - oc[R - 1];
+        cnt = b < nb ? (left < 0 ? 0 : (left > 4 ? 4 : left)) : 0;
         int tok = 0;
 #pragma unroll
         for (int a = 0; a < R; ++a) tok += (gc[a] + g.d[a] * (lo[a] + oc[a])) * g.ts[a];
@@ -73,31 +100,52 @@ struct WaveRange {
 };
 
 // Stages ROWS token rows of D elements.  Each thread item is 4 consecutive
-// rows x one 16-byte segment, loaded with 16-byte global loads; rows can then
-// be written row-major (dst[row][d]) and/or transposed (dst[d][row]).
+// rows (of one 16-row block) x one 16-byte segment, loaded with 16-byte
+// global loads; rows can then be written row-major (dst[row][d]) and/or
+// transposed (dst[d][row]).  Several stagers of the same shape share one
+// set of item addresses (QuadAddr).
+template <int ROWS, int SEGS, int NT>
+struct QuadAddr {
+    static constexpr int kQuads = ROWS / 4;
+    static constexpr int kItems = (kQuads * SEGS + NT - 1) / NT;
+    int tok[kItems];  // token of the item's first row
+    int cnt[kItems];  // rows of the item that exist (0..4)
+
+    template <class QuadTok>
+    __device__ __forceinline__ void compute(int tid, QuadTok quad_tok) {
+#pragma unroll
+        for (int it = 0; it < kItems; ++it) {
+            const int i = tid + it * NT;
+            cnt[it] = 0;
+            tok[it] = 0;
+            if (i < kQuads * SEGS) {
+                const int quad = i / SEGS;
+                tok[it] = quad_tok(quad, cnt[it]);
+            }
+        }
+    }
+};
+
 template <typename T, int D, int ROWS, int NT>
 struct Stager {
     static constexpr int kVec = Tr<T>::kVec;
     static constexpr int kSegs = D / kVec;
     static constexpr int kQuads = ROWS / 4;
-    static constexpr int kItems = (kQuads * kSegs + NT - 1) / NT;
+    using Addr = QuadAddr<ROWS, kSegs, NT>;
+    static constexpr int kItems = Addr::kItems;
     i32x4 r[kItems][4];
 
-    template <class TokOf>
-    __device__ __forceinline__ void load(const T* base, int tid, TokOf tok_of_row) {
+    // tstep: token distance between consecutive rows of a quad
+    __device__ __forceinline__ void load(const T* base, int tid, const Addr& ad, int tstep) {
 #pragma unroll
         for (int it = 0; it < kItems; ++it) {
             const int i = tid + it * NT;
+            const int seg = i % kSegs;
+            const T* p = base + (size_t)ad.tok[it] * D + seg * kVec;
 #pragma unroll
-            for (int rr = 0; rr < 4; ++rr) r[it][rr] = i32x4{0, 0, 0, 0};
-            if (i < kQuads * kSegs) {
-                const int quad = i / kSegs, seg = i - quad * kSegs;
-#pragma unroll
-                for (int rr = 0; rr < 4; ++rr) {
-                    bool ok;
-                    const int tok = tok_of_row(quad * 4 + rr, ok);
-                    if (ok) r[it][rr] = ld16<i32x4>(base + (size_t)tok * D + seg * kVec);
-                }
+            for (int rr = 0; rr < 4; ++rr) {
+                r[it][rr] = i32x4{0, 0, 0, 0};
+                if (rr < ad.cnt[it]) r[it][rr] = ld16<i32x4>(p + (size_t)(rr * tstep) * D);
             }
         }
     }
