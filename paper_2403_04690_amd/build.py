@@ -16,6 +16,11 @@ ARCH = os.environ.get("NA_OFFLOAD_ARCH", "gfx950")
 # Packed fp32 instructions stay off: the compiler must not form v_pk_*_f32.
 FLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", "-Wall",
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+         # keep matrix-core results in ordinary VGPRs (no AGPR copies around the softmax)
+         "-mllvm", "-amdgpu-mfma-vgpr-form",
+         # no NaN inputs are supported, so max() needs no NaN canonicalisation
+         # (infinities stay honoured: masked scores are -inf)
+         "-fno-honor-nans",
          "-I", INCLUDE, "-I", CSRC]
 
 

@@ -13,6 +13,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 #include "na_index.h"
 
 namespace na {
@@ -145,6 +147,30 @@ __device__ __forceinline__ float group_sum4(float x) {
     const unsigned v = __float_as_uint(x);
     const auto b = __builtin_amdgcn_permlane32_swap(v, v, false, false);
     return __uint_as_float(b[0]) + __uint_as_float(b[1]);
+}
+
+// acc + sum of the 8 probabilities of a P fragment.  16-bit types sum the
+// rounded values the matrix product uses, two at a time (v_dot2 with 1.0);
+// fp32 sums the values themselves.
+template <typename T>
+__device__ __forceinline__ float row_sum8(typename Tr<T>::x8 pf, const float (&p)[2][4],
+                                          float acc) {
+    if constexpr (sizeof(T) == 4) {
+        return acc + ((p[0][0] + p[0][1]) + (p[0][2] + p[0][3])) +
+               ((p[1][0] + p[1][1]) + (p[1][2] + p[1][3]));
+    } else {
+        typedef T t2 __attribute__((ext_vector_type(2)));
+        const t2 one = {(T)1.0f, (T)1.0f};
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const t2 pr = {pf[2 * j], pf[2 * j + 1]};
+            if constexpr (std::is_same<T, _Float16>::value)
+                acc = __builtin_amdgcn_fdot2(pr, one, acc, false);
+            else
+                acc = __builtin_amdgcn_fdot2_f32_bf16(pr, one, acc, false);
+        }
+        return acc;
+    }
 }
 
 __device__ __forceinline__ float wave_max_groups(float x) {

@@ -205,17 +205,21 @@ __global__ __launch_bounds__(256) void na_fwd_kernel(Geo g, const T* __restrict_
                 }
 
                 // ---- mask + online softmax per query block ----
+                // y = scale*log2(e)*s - m (base 2, relative to the running
+                // reference m; masked pairs get -inf through the FMA addend)
                 x8 pf[QM];
 #pragma unroll
                 for (int m = 0; m < QM; ++m) {
-                    float sv[2][4];
-                    float tmax = -INFINITY;
+                    const float negm = mref[m] == -INFINITY ? 0.f : -mref[m];
+                    float y[2][4];
+                    if (full[0] && full[1]) {
 #pragma unroll
-                    for (int bi = 0; bi < 2; ++bi) {
-                        if (full[bi]) {
+                        for (int bi = 0; bi < 2; ++bi)
 #pragma unroll
-                            for (int r = 0; r < 4; ++r) sv[bi][r] = sacc[m][bi][r] * c;
-                        } else {
+                            for (int r = 0; r < 4; ++r) y[bi][r] = fmaf(sacc[m][bi][r], c, negm);
+                    } else {
+#pragma unroll
+                        for (int bi = 0; bi < 2; ++bi) {
                             bool outer_ok = rel[bi];
 #pragma unroll
                             for (int a = 0; a < R - 1; ++a)
@@ -224,39 +228,39 @@ __global__ __launch_bounds__(256) void na_fwd_kernel(Geo g, const T* __restrict_
                             const int base = bin0[bi] + grp * 4 - qs[m][R - 1];
 #pragma unroll
                             for (int r = 0; r < 4; ++r) {
-                                const bool ok =
-                                    outer_ok && (unsigned)(base + r) < (unsigned)g.k[R - 1];
-                                sv[bi][r] = ok ? sacc[m][bi][r] * c : -INFINITY;
+                                const bool ok = full[bi] || (outer_ok && (unsigned)(base + r) <
+                                                                             (unsigned)g.k[R - 1]);
+                                y[bi][r] = fmaf(sacc[m][bi][r], c, ok ? negm : -INFINITY);
                             }
                         }
-#pragma unroll
-                        for (int r = 0; r < 4; ++r) tmax = fmaxf(tmax, sv[bi][r]);
                     }
-                    // tile maximum of this query, in base-2 units
-                    const float t = group_max4(tmax);
-                    const bool raise = t > mref[m] + kLazy;
+                    float ymax = fmaxf(fmaxf(fmaxf(y[0][0], y[0][1]), fmaxf(y[0][2], y[0][3])),
+                                       fmaxf(fmaxf(y[1][0], y[1][1]), fmaxf(y[1][2], y[1][3])));
+                    ymax = group_max4(ymax);
+                    // raise the reference on the first valid key of a row, or when
+                    // the row grows by more than kLazy (rare, wave-uniform branch)
+                    const bool raise = ymax > (mref[m] == -INFINITY ? -INFINITY : kLazy);
                     if (__builtin_amdgcn_ballot_w64(raise)) {
-                        // lanes that do not raise keep their reference (alpha = 1)
-                        const float alpha = raise ? fast_exp2(mref[m] - t) : 1.f;
-                        mref[m] = raise ? t : mref[m];
+                        const float dlt = raise ? ymax : 0.f;
+                        const float alpha = fast_exp2(-dlt);
+                        mref[m] = raise ? dlt - negm : mref[m];
                         lrow[m] *= alpha;
 #pragma unroll
                         for (int db = 0; db < C::kDB; ++db) oacc[m][db] *= alpha;
+#pragma unroll
+                        for (int bi = 0; bi < 2; ++bi)
+#pragma unroll
+                            for (int r = 0; r < 4; ++r) y[bi][r] -= dlt;
                     }
-                    const float negm = mref[m] == -INFINITY ? 0.f : -mref[m];
                     float p[2][4];
-                    float psum = 0.f;
 #pragma unroll
                     for (int bi = 0; bi < 2; ++bi)
 #pragma unroll
-                        for (int r = 0; r < 4; ++r) {
-                            p[bi][r] = fast_exp2(sv[bi][r] + negm);
-                            psum += p[bi][r];
-                        }
-                    lrow[m] += psum;
+                        for (int r = 0; r < 4; ++r) p[bi][r] = fast_exp2(y[bi][r]);
                     pf[m] = x8{Tr<T>::cvt(p[0][0]), Tr<T>::cvt(p[0][1]), Tr<T>::cvt(p[0][2]),
                                Tr<T>::cvt(p[0][3]), Tr<T>::cvt(p[1][0]), Tr<T>::cvt(p[1][1]),
                                Tr<T>::cvt(p[1][2]), Tr<T>::cvt(p[1][3])};
+                    lrow[m] = row_sum8<T>(pf[m], p, lrow[m]);
                 }
 
                 // ---- O^T += V^T P^T ----

@@ -120,7 +120,8 @@ struct QuadAddr {
             tok[it] = 0;
             if (i < kQuads * SEGS) {
                 const int quad = i / SEGS;
-                tok[it] = quad_tok(quad, cnt[it]);
+                const int t = quad_tok(quad, cnt[it]);
+                tok[it] = cnt[it] > 0 ? t : 0;  // token 0 is a safe dummy address
             }
         }
     }
@@ -142,10 +143,12 @@ struct Stager {
             const int i = tid + it * NT;
             const int seg = i % kSegs;
             const T* p = base + (size_t)ad.tok[it] * D + seg * kVec;
+            // branch-free: absent rows re-read the first row and are zeroed
 #pragma unroll
             for (int rr = 0; rr < 4; ++rr) {
-                r[it][rr] = i32x4{0, 0, 0, 0};
-                if (rr < ad.cnt[it]) r[it][rr] = ld16<i32x4>(p + (size_t)(rr * tstep) * D);
+                const bool ok = rr < ad.cnt[it];
+                const i32x4 v = ld16<i32x4>(p + (ok ? (size_t)(rr * tstep) * D : 0));
+                r[it][rr] = ok ? v : i32x4{0, 0, 0, 0};
             }
         }
     }
