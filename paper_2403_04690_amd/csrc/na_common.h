@@ -173,18 +173,6 @@ __device__ __forceinline__ float row_sum8(typename Tr<T>::x8 pf, const float (&p
     }
 }
 
-__device__ __forceinline__ float wave_max_groups(float x) {
-    // max over the four 16-lane groups holding the same column
-    x = fmaxf(x, __shfl_xor(x, 16, kWave));
-    x = fmaxf(x, __shfl_xor(x, 32, kWave));
-    return x;
-}
-__device__ __forceinline__ float wave_sum_groups(float x) {
-    x += __shfl_xor(x, 16, kWave);
-    x += __shfl_xor(x, 32, kWave);
-    return x;
-}
-
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
 // Problem geometry shared by all kernels (filled on the host).  Axes beyond
