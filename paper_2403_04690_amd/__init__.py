@@ -20,7 +20,9 @@ __all__ = ["NAError", "forward", "backward", "na_attention", "debug_windows", "v
            "workspace_bytes", "library_path", "load_library", "DTYPES"]
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
-_LIB_PATH = os.path.join(_PKG, "libna.so")
+# NA_LIBRARY may point at another build of the same library (A/B comparisons
+# of kernel variants); by default the in-tree build is used.
+_LIB_PATH = os.environ.get("NA_LIBRARY") or os.path.join(_PKG, "libna.so")
 _lib = None
 
 DTYPES = {torch.float32: 0, torch.float16: 1, torch.bfloat16: 2}
