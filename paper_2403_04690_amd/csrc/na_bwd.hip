@@ -156,12 +156,14 @@ __global__ __launch_bounds__(256) void na_dq_kernel(Geo g, const T* __restrict__
         qvalid[m] = ok;
         qoff[m] = slice + (size_t)tok * D;
 #pragma unroll
+        // unconditional: qoff points at a real (clamped) query even for absent
+        // slots, whose results are discarded
         for (int s = 0; s < C::kKS; ++s) {
-            qf[m][s] = ok ? ld_x8<T>(qg + qoff[m] + s * 32 + grp * 8) : zero_x8<T>();
-            gf[m][s] = ok ? ld_x8<T>(dog + qoff[m] + s * 32 + grp * 8) : zero_x8<T>();
+            qf[m][s] = ld_x8<T>(qg + qoff[m] + s * 32 + grp * 8);
+            gf[m][s] = ld_x8<T>(dog + qoff[m] + s * 32 + grp * 8);
         }
-        lse2[m] = ok ? lseg[qoff[m] / D] * kLog2e : 0.f;
-        dlt[m] = ok ? deltag[qoff[m] / D] : 0.f;
+        lse2[m] = lseg[qoff[m] / D] * kLog2e;
+        dlt[m] = deltag[qoff[m] / D];
     }
 
     const int tstep = g.d[R - 1];
@@ -390,9 +392,11 @@ __global__ __launch_bounds__(256) void na_dkdv_kernel(Geo g, const T* __restrict
         kvalid[m] = ok;
         koff[m] = slice + (size_t)tok * D;
 #pragma unroll
+        // unconditional: koff points at a real (clamped) key even for absent
+        // slots, whose results are discarded
         for (int s = 0; s < C::kKS; ++s) {
-            kf[m][s] = ok ? ld_x8<T>(kg + koff[m] + s * 32 + grp * 8) : zero_x8<T>();
-            vf[m][s] = ok ? ld_x8<T>(vg + koff[m] + s * 32 + grp * 8) : zero_x8<T>();
+            kf[m][s] = ld_x8<T>(kg + koff[m] + s * 32 + grp * 8);
+            vf[m][s] = ld_x8<T>(vg + koff[m] + s * 32 + grp * 8);
         }
     }
 
@@ -411,8 +415,10 @@ __global__ __launch_bounds__(256) void na_dkdv_kernel(Geo g, const T* __restrict
             const int tok = ibox.quad_token(g, gc, s * SB + (tid >> 4), tid & 12, cnt) +
                             (tid & 3) * tstep;
             const bool ok = (tid & 3) < cnt;
-            lse_reg = ok ? lb[tok] * kLog2e : 0.f;
-            dlt_reg = ok ? db_[tok] : 0.f;
+            const int tk = ok ? tok : 0;  // token 0 is a safe dummy address
+            const float lv = lb[tk], dv_ = db_[tk];
+            lse_reg = ok ? lv * kLog2e : 0.f;
+            dlt_reg = ok ? dv_ : 0.f;
         }
     };
     auto buf_base = [&](int buf) { return smem_raw + buf * C::kBufBytes; };

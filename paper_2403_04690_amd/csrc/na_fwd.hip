@@ -136,8 +136,9 @@ __global__ __launch_bounds__(256) void na_fwd_kernel(Geo g, const T* __restrict_
         qvalid[m] = ok;
         qoff[m] = slice + (size_t)tok * D;
 #pragma unroll
-        for (int s = 0; s < C::kKS; ++s)
-            qf[m][s] = ok ? ld_x8<T>(qg + qoff[m] + s * 32 + grp * 8) : zero_x8<T>();
+        // unconditional: qoff points at a real (clamped) query even for absent
+        // slots, whose results are discarded; no wait before the K/V loads
+        for (int s = 0; s < C::kKS; ++s) qf[m][s] = ld_x8<T>(qg + qoff[m] + s * 32 + grp * 8);
     }
 
     // ---- staging of K (row-major) and V (transposed), one address set for both ----
@@ -157,14 +158,41 @@ __global__ __launch_bounds__(256) void na_fwd_kernel(Geo g, const T* __restrict_
     };
 
     // ---- online-softmax state (per lane: its query column) ----
+    // mref: running reference (base 2, -inf until the row sees a key);
+    // negm = -mref (0 while mref = -inf) is the scores' FMA addend and thr the
+    // score above which the reference must be raised.
     f32x4 oacc[QM][C::kDB];
-    float mref[QM], lrow[QM];
+    float mref[QM], negm[QM], thr[QM], lrow[QM];
 #pragma unroll
     for (int m = 0; m < QM; ++m) {
         mref[m] = -INFINITY;
+        negm[m] = 0.f;
+        thr[m] = -INFINITY;
         lrow[m] = 0.f;
 #pragma unroll
         for (int db = 0; db < C::kDB; ++db) oacc[m][db] = f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+    // Halo rows of at most two 16-key blocks (the usual 2-D / 3-D case): the
+    // inner-axis test of this lane's 4 key slots is fixed for the whole
+    // kernel, so it is folded into per-slot FMA addends (negm where valid,
+    // -inf where not), refreshed only when the reference moves.  Block bi of
+    // a tile has inner block index bi when rows hold two blocks, else 0.
+    const bool short_rows = R > 1 && halo.nbr <= 2;
+    float ain[QM][2][4];
+    auto refresh_addends = [&](int m) {
+#pragma unroll
+        for (int bi = 0; bi < 2; ++bi)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int ib = halo.nbr == 2 ? bi : 0;
+                const bool v =
+                    (unsigned)(ib * 16 + grp * 4 + r - qs[m][R - 1]) < (unsigned)g.k[R - 1];
+                ain[m][bi][r] = v ? negm[m] : -INFINITY;
+            }
+    };
+    if (R > 1) {
+#pragma unroll
+        for (int m = 0; m < QM; ++m) refresh_addends(m);
     }
 
     const int nst = (halo.nb + SB - 1) / SB;
@@ -210,13 +238,25 @@ __global__ __launch_bounds__(256) void na_fwd_kernel(Geo g, const T* __restrict_
                 x8 pf[QM];
 #pragma unroll
                 for (int m = 0; m < QM; ++m) {
-                    const float negm = mref[m] == -INFINITY ? 0.f : -mref[m];
                     float y[2][4];
                     if (full[0] && full[1]) {
 #pragma unroll
                         for (int bi = 0; bi < 2; ++bi)
 #pragma unroll
-                            for (int r = 0; r < 4; ++r) y[bi][r] = fmaf(sacc[m][bi][r], c, negm);
+                            for (int r = 0; r < 4; ++r) y[bi][r] = fmaf(sacc[m][bi][r], c, negm[m]);
+                    } else if (R > 1 && short_rows) {
+#pragma unroll
+                        for (int bi = 0; bi < 2; ++bi) {
+                            bool outer_ok = rel[bi];
+#pragma unroll
+                            for (int a = 0; a < R - 1; ++a)
+                                outer_ok = outer_ok &&
+                                           (unsigned)(boc[bi][a] - qs[m][a]) < (unsigned)g.k[a];
+#pragma unroll
+                            for (int r = 0; r < 4; ++r)
+                                y[bi][r] = fmaf(sacc[m][bi][r], c,
+                                                outer_ok ? ain[m][bi][r] : -INFINITY);
+                        }
                     } else {
 #pragma unroll
                         for (int bi = 0; bi < 2; ++bi) {
@@ -230,7 +270,7 @@ __global__ __launch_bounds__(256) void na_fwd_kernel(Geo g, const T* __restrict_
                             for (int r = 0; r < 4; ++r) {
                                 const bool ok = full[bi] || (outer_ok && (unsigned)(base + r) <
                                                                              (unsigned)g.k[R - 1]);
-                                y[bi][r] = fmaf(sacc[m][bi][r], c, ok ? negm : -INFINITY);
+                                y[bi][r] = fmaf(sacc[m][bi][r], c, ok ? negm[m] : -INFINITY);
                             }
                         }
                     }
@@ -239,11 +279,15 @@ __global__ __launch_bounds__(256) void na_fwd_kernel(Geo g, const T* __restrict_
                     ymax = group_max4(ymax);
                     // raise the reference on the first valid key of a row, or when
                     // the row grows by more than kLazy (rare, wave-uniform branch)
-                    const bool raise = ymax > (mref[m] == -INFINITY ? -INFINITY : kLazy);
+                    const bool raise = ymax > thr[m];
                     if (__builtin_amdgcn_ballot_w64(raise)) {
                         const float dlt = raise ? ymax : 0.f;
                         const float alpha = fast_exp2(-dlt);
-                        mref[m] = raise ? dlt - negm : mref[m];
+                        mref[m] = raise ? dlt - negm[m] : mref[m];
+                        const bool seen = mref[m] != -INFINITY;
+                        negm[m] = seen ? -mref[m] : 0.f;
+                        thr[m] = seen ? kLazy : -INFINITY;
+                        if (R > 1) refresh_addends(m);
                         lrow[m] *= alpha;
 #pragma unroll
                         for (int db = 0; db < C::kDB; ++db) oacc[m][db] *= alpha;
