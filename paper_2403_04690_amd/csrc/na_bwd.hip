@@ -188,6 +188,22 @@ __global__ __launch_bounds__(256) void na_dq_kernel(Geo g, const T* __restrict__
     for (int m = 0; m < QM; ++m)
 #pragma unroll
         for (int db = 0; db < C::kDB; ++db) dqacc[m][db] = f32x4{0.f, 0.f, 0.f, 0.f};
+    // Halo rows of at most two 16-key blocks: the inner-axis test of this
+    // lane's 4 key slots is fixed, folded with -lse2 into per-slot addends.
+    const bool short_rows = R > 1 && halo.nbr <= 2;
+    float ain[QM][2][4];
+#pragma unroll
+    for (int m = 0; m < QM; ++m)
+#pragma unroll
+        for (int bi = 0; bi < 2; ++bi)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int ib = halo.nbr == 2 ? bi : 0;
+                ain[m][bi][r] =
+                    (unsigned)(ib * 16 + grp * 4 + r - qs[m][R - 1]) < (unsigned)g.k[R - 1]
+                        ? -lse2[m]
+                        : -INFINITY;
+            }
 
     const int nst = (halo.nb + SB - 1) / SB;
     load_stage(0);
@@ -214,26 +230,29 @@ __global__ __launch_bounds__(256) void na_dq_kernel(Geo g, const T* __restrict__
                 f32x4 sacc[QM][2], pacc[QM][2];
 #pragma unroll
                 for (int bi = 0; bi < 2; ++bi) {
+                    if (rel[bi]) {
+                        const int row = (tp * 2 + bi) * 16 + col;
 #pragma unroll
-                    for (int m = 0; m < QM; ++m) {
-                        sacc[m][bi] = f32x4{0.f, 0.f, 0.f, 0.f};
-                        pacc[m][bi] = f32x4{0.f, 0.f, 0.f, 0.f};
-                    }
-                    if (!rel[bi]) continue;
-                    const int row = (tp * 2 + bi) * 16 + col;
+                        for (int st = 0; st < C::kKS; ++st) {
+                            const x8 kf = ld_x8<T>(ks + row * C::kRow + st * 32 + grp * 8);
+                            const x8 vf = ld_x8<T>(vs + row * C::kRow + st * 32 + grp * 8);
 #pragma unroll
-                    for (int st = 0; st < C::kKS; ++st) {
-                        const x8 kf = ld_x8<T>(ks + row * C::kRow + st * 32 + grp * 8);
-                        const x8 vf = ld_x8<T>(vs + row * C::kRow + st * 32 + grp * 8);
+                            for (int m = 0; m < QM; ++m) {
+                                const f32x4 z = f32x4{0.f, 0.f, 0.f, 0.f};
+                                sacc[m][bi] = Tr<T>::mma(kf, qf[m][st], st == 0 ? z : sacc[m][bi]);
+                                pacc[m][bi] = Tr<T>::mma(vf, gf[m][st], st == 0 ? z : pacc[m][bi]);
+                            }
+                        }
+                    } else {
 #pragma unroll
                         for (int m = 0; m < QM; ++m) {
-                            sacc[m][bi] = Tr<T>::mma(kf, qf[m][st], sacc[m][bi]);
-                            pacc[m][bi] = Tr<T>::mma(vf, gf[m][st], pacc[m][bi]);
+                            sacc[m][bi] = f32x4{0.f, 0.f, 0.f, 0.f};
+                            pacc[m][bi] = f32x4{0.f, 0.f, 0.f, 0.f};
                         }
                     }
                 }
 
-                // dA^T = P^T (dP^T - Delta), P recomputed from the logsumexp
+                // dA^T = P^T (dP^T - Delta), P = exp2(scale*log2(e)*s - lse2) on valid pairs
                 x8 dsf[QM];
 #pragma unroll
                 for (int m = 0; m < QM; ++m) {
@@ -247,9 +266,17 @@ __global__ __launch_bounds__(256) void na_dq_kernel(Geo g, const T* __restrict__
                         const int base = bin0[bi] + grp * 4 - qs[m][R - 1];
 #pragma unroll
                         for (int r = 0; r < 4; ++r) {
-                            const bool ok = full[bi] ||
-                                            (outer_ok && (unsigned)(base + r) < (unsigned)g.k[R - 1]);
-                            const float p = ok ? fast_exp2(sacc[m][bi][r] * scale_log2 - lse2[m]) : 0.f;
+                            float add;
+                            if (full[bi]) {
+                                add = -lse2[m];
+                            } else if (short_rows) {
+                                add = outer_ok ? ain[m][bi][r] : -INFINITY;
+                            } else {
+                                const bool ok =
+                                    outer_ok && (unsigned)(base + r) < (unsigned)g.k[R - 1];
+                                add = ok ? -lse2[m] : -INFINITY;
+                            }
+                            const float p = fast_exp2(fmaf(sacc[m][bi][r], scale_log2, add));
                             ds[bi][r] = p * (pacc[m][bi][r] - dlt[m]);
                         }
                     }
@@ -400,6 +427,34 @@ __global__ __launch_bounds__(256) void na_dkdv_kernel(Geo g, const T* __restrict
         }
     }
 
+    // A query q attends to this lane's key j exactly when q lies in j's
+    // inverse range [inv_lo(j), inv_hi(j)] on every axis (contiguous, since
+    // window starts are non-decreasing): per lane, relative to the query box.
+    int ilo[KM][kMaxRank], ispan[KM][kMaxRank];
+#pragma unroll
+    for (int m = 0; m < KM; ++m)
+#pragma unroll
+        for (int a = 0; a < R; ++a) {
+            ilo[m][a] = inv_lo(kc[m][a], n[a], g.k[a]) - ibox.lo[a];
+            ispan[m][a] = inv_hi(kc[m][a], n[a], g.k[a]) - inv_lo(kc[m][a], n[a], g.k[a]);
+        }
+    // Query-box rows of at most two 16-query blocks: the inner-axis test of
+    // this lane's 4 query slots is fixed, folded into 0 / -inf addends.
+    const bool short_rows = R > 1 && ibox.nbr <= 2;
+    float ain[KM][2][4];
+#pragma unroll
+    for (int m = 0; m < KM; ++m)
+#pragma unroll
+        for (int bi = 0; bi < 2; ++bi)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int ib = ibox.nbr == 2 ? bi : 0;
+                ain[m][bi][r] = (unsigned)(ib * 16 + grp * 4 + r - ilo[m][R - 1]) <=
+                                        (unsigned)ispan[m][R - 1]
+                                    ? 0.f
+                                    : -INFINITY;
+            }
+
     const int tstep = g.d[R - 1];
     typename C::Stg qst, gst;
     typename C::Stg::Addr addr;
@@ -472,43 +527,42 @@ __global__ __launch_bounds__(256) void na_dkdv_kernel(Geo g, const T* __restrict
                 f32x4 sacc[KM][2], pacc[KM][2];
 #pragma unroll
                 for (int bi = 0; bi < 2; ++bi) {
+                    if (rel[bi]) {
+                        const int row = (tp * 2 + bi) * 16 + col;
 #pragma unroll
-                    for (int m = 0; m < KM; ++m) {
-                        sacc[m][bi] = f32x4{0.f, 0.f, 0.f, 0.f};
-                        pacc[m][bi] = f32x4{0.f, 0.f, 0.f, 0.f};
-                    }
-                    if (!rel[bi]) continue;
-                    const int row = (tp * 2 + bi) * 16 + col;
+                        for (int st = 0; st < C::kKS; ++st) {
+                            const x8 qa = ld_x8<T>(qs + row * C::kRow + st * 32 + grp * 8);
+                            const x8 ga = ld_x8<T>(gs + row * C::kRow + st * 32 + grp * 8);
 #pragma unroll
-                    for (int st = 0; st < C::kKS; ++st) {
-                        const x8 qa = ld_x8<T>(qs + row * C::kRow + st * 32 + grp * 8);
-                        const x8 ga = ld_x8<T>(gs + row * C::kRow + st * 32 + grp * 8);
+                            for (int m = 0; m < KM; ++m) {
+                                const f32x4 z = f32x4{0.f, 0.f, 0.f, 0.f};
+                                sacc[m][bi] = Tr<T>::mma(qa, kf[m][st], st == 0 ? z : sacc[m][bi]);
+                                pacc[m][bi] = Tr<T>::mma(ga, vf[m][st], st == 0 ? z : pacc[m][bi]);
+                            }
+                        }
+                    } else {
 #pragma unroll
                         for (int m = 0; m < KM; ++m) {
-                            sacc[m][bi] = Tr<T>::mma(qa, kf[m][st], sacc[m][bi]);
-                            pacc[m][bi] = Tr<T>::mma(ga, vf[m][st], pacc[m][bi]);
+                            sacc[m][bi] = f32x4{0.f, 0.f, 0.f, 0.f};
+                            pacc[m][bi] = f32x4{0.f, 0.f, 0.f, 0.f};
                         }
                     }
                 }
 
-                // per-query window starts of the 2 x 4 queries this lane holds
-                int qwin[2][4];
-                bool qin[2][4];
-                int owin[2][kMaxRank];
+                // -LSE and Delta of the 2 x 4 queries this lane holds
+                float nlse[2][4], dlv[2][4];
 #pragma unroll
                 for (int bi = 0; bi < 2; ++bi) {
-#pragma unroll
-                    for (int a = 0; a < R - 1; ++a)
-                        owin[bi][a] = win_start(ibox.lo[a] + boc[bi][a], n[a], g.k[a]);
+                    const int srow = (tp * 2 + bi) * 16 + grp * 4;
+                    const f32x4 lv = ld16<f32x4>(ls + srow), dv4 = ld16<f32x4>(dls + srow);
 #pragma unroll
                     for (int r = 0; r < 4; ++r) {
-                        const int qi = bin0[bi] + grp * 4 + r;
-                        qin[bi][r] = qi < ibox.E[R - 1];
-                        qwin[bi][r] = win_start(min(ibox.lo[R - 1] + qi, n[R - 1] - 1), n[R - 1],
-                                                g.k[R - 1]);
+                        nlse[bi][r] = -lv[r];
+                        dlv[bi][r] = dv4[r];
                     }
                 }
 
+                // P = exp2(scale*log2(e)*s - lse2) on valid pairs, dA = P (dP - Delta)
                 x8 pf[KM], dsf[KM];
 #pragma unroll
                 for (int m = 0; m < KM; ++m) {
@@ -518,17 +572,24 @@ __global__ __launch_bounds__(256) void na_dkdv_kernel(Geo g, const T* __restrict
                         bool outer_ok = rel[bi];
 #pragma unroll
                         for (int a = 0; a < R - 1; ++a)
-                            outer_ok = outer_ok && (unsigned)(kc[m][a] - owin[bi][a]) < (unsigned)g.k[a];
-                        const int srow = (tp * 2 + bi) * 16 + grp * 4;
+                            outer_ok = outer_ok &&
+                                       (unsigned)(boc[bi][a] - ilo[m][a]) <= (unsigned)ispan[m][a];
+                        const int base = bin0[bi] + grp * 4 - ilo[m][R - 1];
 #pragma unroll
                         for (int r = 0; r < 4; ++r) {
-                            const bool ok =
-                                full[bi] || (outer_ok && qin[bi][r] &&
-                                             (unsigned)(kc[m][R - 1] - qwin[bi][r]) < (unsigned)g.k[R - 1]);
-                            const float pv =
-                                ok ? fast_exp2(sacc[m][bi][r] * scale_log2 - ls[srow + r]) : 0.f;
+                            float add;
+                            if (full[bi]) {
+                                add = nlse[bi][r];
+                            } else if (short_rows) {
+                                add = outer_ok ? nlse[bi][r] + ain[m][bi][r] : -INFINITY;
+                            } else {
+                                const bool ok =
+                                    outer_ok && (unsigned)(base + r) <= (unsigned)ispan[m][R - 1];
+                                add = ok ? nlse[bi][r] : -INFINITY;
+                            }
+                            const float pv = fast_exp2(fmaf(sacc[m][bi][r], scale_log2, add));
                             p[bi][r] = pv;
-                            ds[bi][r] = pv * (pacc[m][bi][r] - dls[srow + r]);
+                            ds[bi][r] = pv * (pacc[m][bi][r] - dlv[bi][r]);
                         }
                     }
                     pf[m] = x8{Tr<T>::cvt(p[0][0]), Tr<T>::cvt(p[0][1]), Tr<T>::cvt(p[0][2]),
