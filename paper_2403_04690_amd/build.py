@@ -15,6 +15,7 @@ SOURCES = ["na_fwd.hip", "na_bwd.hip", "na_debug.hip", "na_api.cpp"]
 ARCH = os.environ.get("NA_OFFLOAD_ARCH", "gfx950")
 # Packed fp32 instructions stay off: the compiler must not form v_pk_*_f32.
 FLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", "-Wall",
+         "-Werror=uninitialized", "-Werror=sometimes-uninitialized",
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
          # keep matrix-core results in ordinary VGPRs (no AGPR copies around the softmax)
          "-mllvm", "-amdgpu-mfma-vgpr-form",

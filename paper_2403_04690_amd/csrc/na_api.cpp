@@ -18,6 +18,12 @@ constexpr int kVersion = 100;  // 0.1.0
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
+int ilog2(int x) {  // x is a power of two
+    int l = 0;
+    while ((1 << l) < x) ++l;
+    return l;
+}
+
 int pow2ceil(int x) {
     int p = 1;
     while (p < x) p <<= 1;
@@ -110,6 +116,14 @@ bool make_geo(int rank, const int64_t* extents, const int32_t* ks, const int32_t
     if (nwg >= (int64_t(1) << 31)) return false;
     g.ntiles = (int)ntiles;
     g.nwg = (int)nwg;
+    for (int a = 0; a < 3; ++a) {
+        g.lgWT[a] = ilog2(g.WT[a]);
+        g.lgWGd[a] = ilog2(g.WGd[a]);
+        g.fd_d[a].init(g.d[a]);
+        g.fd_nt[a].init(g.nt[a]);
+    }
+    g.fd_ntiles.init(g.ntiles);
+    g.fd_ngroups.init(g.ngroups);
     return true;
 }
 

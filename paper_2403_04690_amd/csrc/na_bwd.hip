@@ -91,20 +91,12 @@ __global__ __launch_bounds__(256) void na_dq_kernel(Geo g, const T* __restrict__
     const int grp = lane >> 4;
 
     const int bid = xcd_remap(blockIdx.x, g.nwg);
-    const int tile = bid % g.ntiles;
-    const int rest = bid / g.ntiles;
-    const int gidx = rest % g.ngroups;
-    const int bh = rest / g.ngroups;
+    int bh, gc[kMaxRank], tc[kMaxRank], n[kMaxRank], to[kMaxRank];
+    decode_workgroup<R>(g, bid, bh, gc, tc, n);
 
-    int gc[kMaxRank], tc[kMaxRank];
-    unravel<R>(gidx, g.d, gc);
-    unravel<R>(tile, g.nt, tc);
-
-    int n[kMaxRank], to[kMaxRank];
     Box<R> halo;
 #pragma unroll
     for (int a = 0; a < R; ++a) {
-        n[a] = group_len(g.L[a], g.d[a], gc[a]);
         to[a] = tc[a] * g.T[a];
         if (to[a] >= n[a]) return;
         const int last = min(to[a] + g.T[a], n[a]) - 1;
@@ -118,7 +110,7 @@ __global__ __launch_bounds__(256) void na_dq_kernel(Geo g, const T* __restrict__
     const T* vb = vg + slice;
 
     int wc[kMaxRank], wo[kMaxRank];
-    unravel<R>(wave, g.WGd, wc);
+    unravel_pow2<R>(wave, g.lgWGd, wc);
     bool wave_live = true;
     WaveRange<R> wr;
 #pragma unroll
@@ -142,7 +134,7 @@ __global__ __launch_bounds__(256) void na_dq_kernel(Geo g, const T* __restrict__
 #pragma unroll
     for (int m = 0; m < QM; ++m) {
         int c[kMaxRank];
-        unravel<R>(m * 16 + col, g.WT, c);
+        unravel_pow2<R>(m * 16 + col, g.lgWT, c);
         bool ok = wave_live;
         int tok = 0;
 #pragma unroll
@@ -351,21 +343,13 @@ __global__ __launch_bounds__(256) void na_dkdv_kernel(Geo g, const T* __restrict
     const int grp = lane >> 4;
 
     const int bid = xcd_remap(blockIdx.x, g.nwg);
-    const int tile = bid % g.ntiles;
-    const int rest = bid / g.ntiles;
-    const int gidx = rest % g.ngroups;
-    const int bh = rest / g.ngroups;
-
-    int gc[kMaxRank], tc[kMaxRank];
-    unravel<R>(gidx, g.d, gc);
-    unravel<R>(tile, g.nt, tc);
+    int bh, gc[kMaxRank], tc[kMaxRank], n[kMaxRank], to[kMaxRank];
+    decode_workgroup<R>(g, bid, bh, gc, tc, n);
 
     // key tile [to, last] and the box of queries attending to it
-    int n[kMaxRank], to[kMaxRank];
     Box<R> ibox;
 #pragma unroll
     for (int a = 0; a < R; ++a) {
-        n[a] = group_len(g.L[a], g.d[a], gc[a]);
         to[a] = tc[a] * g.T[a];
         if (to[a] >= n[a]) return;
         const int last = min(to[a] + g.T[a], n[a]) - 1;
@@ -382,7 +366,7 @@ __global__ __launch_bounds__(256) void na_dkdv_kernel(Geo g, const T* __restrict
 
     // this wave's key sub-box: the queries that attend to any / all of its keys
     int wc[kMaxRank], wo[kMaxRank];
-    unravel<R>(wave, g.WGd, wc);
+    unravel_pow2<R>(wave, g.lgWGd, wc);
     bool wave_live = true;
     WaveRange<R> wr;
 #pragma unroll
@@ -405,7 +389,7 @@ __global__ __launch_bounds__(256) void na_dkdv_kernel(Geo g, const T* __restrict
 #pragma unroll
     for (int m = 0; m < KM; ++m) {
         int c[kMaxRank];
-        unravel<R>(m * 16 + col, g.WT, c);
+        unravel_pow2<R>(m * 16 + col, g.lgWT, c);
         bool ok = wave_live;
         int tok = 0;
 #pragma unroll

@@ -175,6 +175,36 @@ __device__ __forceinline__ float row_sum8(typename Tr<T>::x8 pf, const float (&p
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
+// Division by a divisor that stays fixed for a whole launch or workgroup:
+// q = (umulhi(n, mul) + n) >> shr, exact for 0 <= n < 2^31 and d >= 1.
+// The multiplier is floor(2^32 (2^s - d) / d) + 1 with s = ceil(log2 d); on
+// the device it is formed with one double division (exact for d < 2^20,
+// since 2^32 (2^s - d) < 2^52 and the quotient's fractional part exceeds the
+// rounding error), on the host in 64-bit integers.
+struct FastDiv {
+    uint32_t mul, shr;
+    NA_HD void init(int d) {
+        uint32_t s = 0;
+        while ((1u << s) < (uint32_t)d) ++s;
+        shr = s;
+        const uint64_t a = ((uint64_t)1 << s) - (uint64_t)d;
+#if defined(__HIP_DEVICE_COMPILE__)
+        if (d < (1 << 20)) {
+            mul = (uint32_t)((uint64_t)__builtin_floor((double)a * 4294967296.0 / (double)d) + 1);
+            return;
+        }
+#endif
+        mul = (uint32_t)((a << 32) / (uint64_t)d + 1);
+    }
+    NA_HD int div(int n) const {
+#if defined(__HIP_DEVICE_COMPILE__)
+        return (int)((__umulhi((uint32_t)n, mul) + (uint32_t)n) >> shr);
+#else
+        return (int)((((uint64_t)(uint32_t)n * mul >> 32) + (uint32_t)n) >> shr);
+#endif
+    }
+};
+
 // Problem geometry shared by all kernels (filled on the host).  Axes beyond
 // the problem's rank are inert (extent 1, window 1, dilation 1).
 struct Geo {
@@ -189,7 +219,41 @@ struct Geo {
     int nt[kMaxRank];    // tiles per axis (sized for the longest group)
     int ntiles;          // prod nt
     int nwg;             // workgroups in the grid
+    int lgWT[kMaxRank];  // log2 WT (wave tiles are powers of two)
+    int lgWGd[kMaxRank]; // log2 WGd
+    FastDiv fd_ntiles, fd_ngroups, fd_d[kMaxRank], fd_nt[kMaxRank];
 };
+
+// Workgroup -> (batch*head, dilation group coordinates, tile coordinates) and
+// the length of this group along every axis.
+template <int R>
+__device__ __forceinline__ void decode_workgroup(const Geo& g, int bid, int& bh, int* gc, int* tc,
+                                                 int* n) {
+    const int rest = g.fd_ntiles.div(bid);
+    int tile = bid - rest * g.ntiles;
+    bh = g.fd_ngroups.div(rest);
+    int gidx = rest - bh * g.ngroups;
+#pragma unroll
+    for (int a = R - 1; a >= 0; --a) {
+        const int gq = g.fd_d[a].div(gidx);
+        gc[a] = gidx - gq * g.d[a];
+        gidx = gq;
+        const int tq = g.fd_nt[a].div(tile);
+        tc[a] = tile - tq * g.nt[a];
+        tile = tq;
+        n[a] = g.fd_d[a].div(g.L[a] - gc[a] + g.d[a] - 1);
+    }
+}
+
+// Row-major unravel of idx over power-of-two extents 2^lg[a].
+template <int R>
+__device__ __forceinline__ void unravel_pow2(int idx, const int* lg, int* c) {
+#pragma unroll
+    for (int a = R - 1; a >= 0; --a) {
+        c[a] = idx & ((1 << lg[a]) - 1);
+        idx >>= lg[a];
+    }
+}
 
 // Workgroups are dispatched round-robin over the 8 XCDs; renumber them so
 // that each XCD receives a contiguous run of logical tiles (neighbouring tiles

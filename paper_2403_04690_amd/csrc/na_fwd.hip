@@ -50,8 +50,10 @@ struct FwdCfg {
     using Stg = Stager<T, D, kKeys, kThreads>;
 };
 
-// c = scale * log2(e): scores are kept in base 2.
-template <int R, int D, typename T, int QM, int SB>
+// c = scale * log2(e): scores are kept in base 2.  SHORT = 1: every halo row
+// holds at most two 16-key blocks (rank >= 2), so the inner-axis mask is a
+// per-lane constant; SHORT = 0: general masking with mask-free full blocks.
+template <int R, int D, typename T, int QM, int SB, int SHORT>
 __global__ __launch_bounds__(256) void na_fwd_kernel(Geo g, const T* __restrict__ qg,
                                                      const T* __restrict__ kg,
                                                      const T* __restrict__ vg, T* __restrict__ og,
@@ -69,20 +71,12 @@ __global__ __launch_bounds__(256) void na_fwd_kernel(Geo g, const T* __restrict_
 
     // ---- workgroup -> (bh, dilation group, tile) ----
     const int bid = xcd_remap(blockIdx.x, g.nwg);
-    const int tile = bid % g.ntiles;
-    const int rest = bid / g.ntiles;
-    const int gidx = rest % g.ngroups;
-    const int bh = rest / g.ngroups;
+    int bh, gc[kMaxRank], tc[kMaxRank], n[kMaxRank], to[kMaxRank];
+    decode_workgroup<R>(g, bid, bh, gc, tc, n);
 
-    int gc[kMaxRank], tc[kMaxRank];
-    unravel<R>(gidx, g.d, gc);
-    unravel<R>(tile, g.nt, tc);
-
-    int n[kMaxRank], to[kMaxRank];
     Box<R> halo;
 #pragma unroll
     for (int a = 0; a < R; ++a) {
-        n[a] = group_len(g.L[a], g.d[a], gc[a]);
         to[a] = tc[a] * g.T[a];
         if (to[a] >= n[a]) return;  // tile beyond this (shorter) group: uniform exit
         const int last = min(to[a] + g.T[a], n[a]) - 1;
@@ -98,7 +92,7 @@ __global__ __launch_bounds__(256) void na_fwd_kernel(Geo g, const T* __restrict_
 
     // ---- this wave's query sub-box: its halo and the keys inside all of its windows ----
     int wc[kMaxRank], wo[kMaxRank];
-    unravel<R>(wave, g.WGd, wc);
+    unravel_pow2<R>(wave, g.lgWGd, wc);
     bool wave_live = true;
     WaveRange<R> wr;
 #pragma unroll
@@ -122,7 +116,7 @@ __global__ __launch_bounds__(256) void na_fwd_kernel(Geo g, const T* __restrict_
 #pragma unroll
     for (int m = 0; m < QM; ++m) {
         int cc[kMaxRank];
-        unravel<R>(m * 16 + col, g.WT, cc);
+        unravel_pow2<R>(m * 16 + col, g.lgWT, cc);
         bool ok = wave_live;
         int tok = 0;
 #pragma unroll
@@ -177,7 +171,7 @@ __global__ __launch_bounds__(256) void na_fwd_kernel(Geo g, const T* __restrict_
     // kernel, so it is folded into per-slot FMA addends (negm where valid,
     // -inf where not), refreshed only when the reference moves.  Block bi of
     // a tile has inner block index bi when rows hold two blocks, else 0.
-    const bool short_rows = R > 1 && halo.nbr <= 2;
+    constexpr bool short_rows = SHORT != 0 && R > 1;
     float ain[QM][2][4];
     auto refresh_addends = [&](int m) {
 #pragma unroll
@@ -239,12 +233,12 @@ __global__ __launch_bounds__(256) void na_fwd_kernel(Geo g, const T* __restrict_
 #pragma unroll
                 for (int m = 0; m < QM; ++m) {
                     float y[2][4];
-                    if (full[0] && full[1]) {
+                    if (!short_rows && full[0] && full[1]) {
 #pragma unroll
                         for (int bi = 0; bi < 2; ++bi)
 #pragma unroll
                             for (int r = 0; r < 4; ++r) y[bi][r] = fmaf(sacc[m][bi][r], c, negm[m]);
-                    } else if (R > 1 && short_rows) {
+                    } else if (short_rows) {
 #pragma unroll
                         for (int bi = 0; bi < 2; ++bi) {
                             bool outer_ok = rel[bi];
@@ -348,11 +342,20 @@ static int max_halo_blocks(const Geo& g, int rank) {
     return nb;
 }
 
+// Largest number of 16-key blocks in one halo row (interior tiles).
+static int max_row_blocks(const Geo& g, int rank) {
+    const int a = rank - 1;
+    const int n0 = group_len(g.L[a], g.d[a], 0);
+    const int e = std::min(std::min(g.T[a], n0) + g.k[a] - 1, n0);
+    return (e + 15) / 16;
+}
+
 template <int R, int D, typename T, int QM, int SB>
 static hipError_t launch_fwd_inst(const Geo& g, const void* q, const void* k, const void* v,
                                   void* o, float* lse, float scale, hipStream_t stream) {
     using C = FwdCfg<R, D, T, QM, SB>;
-    auto kern = na_fwd_kernel<R, D, T, QM, SB>;
+    const bool short_rows = R > 1 && max_row_blocks(g, R) <= 2;
+    auto kern = short_rows ? na_fwd_kernel<R, D, T, QM, SB, 1> : na_fwd_kernel<R, D, T, QM, SB, 0>;
     const int nst_max = (max_halo_blocks(g, R) + SB - 1) / SB;
     const size_t lds = (nst_max > 1 ? 2 : 1) * C::kBufBytes;
     if (lds > 65536) {

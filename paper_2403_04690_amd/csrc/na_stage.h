@@ -6,23 +6,6 @@
 
 namespace na {
 
-// Division by a runtime divisor that stays fixed for a whole workgroup:
-// q = (umulhi(n, mul) + n) >> shr, exact for 0 <= n < 2^31 and d >= 1.
-struct FastDiv {
-    uint32_t mul, shr;
-    int d;
-    __device__ __forceinline__ void init(int d_) {
-        d = d_;
-        uint32_t s = 0;
-        while ((1u << s) < (uint32_t)d_) ++s;
-        shr = s;
-        mul = (uint32_t)((((uint64_t)1 << 32) * (((uint64_t)1 << s) - (uint64_t)d_)) / (uint64_t)d_ + 1);
-    }
-    __device__ __forceinline__ int div(int n) const {
-        return (int)((__umulhi((uint32_t)n, mul) + (uint32_t)n) >> shr);
-    }
-};
-
 // A box of tokens in group coordinates, [lo, lo + E) per axis, cut into rows
 // along the innermost axis and each row into 16-token blocks (rows are padded
 // to a multiple of 16; padding tokens are zero-filled and always masked).
