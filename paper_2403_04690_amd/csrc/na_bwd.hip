@@ -15,6 +15,8 @@
 //                    k + floor(k/2) queries per axis)
 //   na_dq_kernel     one workgroup per query tile over its key halo, like the
 //                    forward pass
+#include <algorithm>
+
 #include "na_launch.h"
 #include "na_stage.h"
 
@@ -70,7 +72,9 @@ struct DqCfg {
     using Stg = Stager<T, D, kKeys, kThreads>;
 };
 
-template <int R, int D, typename T, int QM, int SB>
+// SHORT = 1: every halo row holds at most two 16-key blocks (rank >= 2), so
+// the inner-axis mask is a per-lane constant (chosen on the host).
+template <int R, int D, typename T, int QM, int SB, int SHORT>
 __global__ __launch_bounds__(256) void na_dq_kernel(Geo g, const T* __restrict__ qg,
                                                     const T* __restrict__ kg,
                                                     const T* __restrict__ vg,
@@ -182,7 +186,7 @@ __global__ __launch_bounds__(256) void na_dq_kernel(Geo g, const T* __restrict__
         for (int db = 0; db < C::kDB; ++db) dqacc[m][db] = f32x4{0.f, 0.f, 0.f, 0.f};
     // Halo rows of at most two 16-key blocks: the inner-axis test of this
     // lane's 4 key slots is fixed, folded with -lse2 into per-slot addends.
-    const bool short_rows = R > 1 && halo.nbr <= 2;
+    constexpr bool short_rows = SHORT != 0 && R > 1;
     float ain[QM][2][4];
 #pragma unroll
     for (int m = 0; m < QM; ++m)
@@ -259,7 +263,7 @@ __global__ __launch_bounds__(256) void na_dq_kernel(Geo g, const T* __restrict__
 #pragma unroll
                         for (int r = 0; r < 4; ++r) {
                             float add;
-                            if (full[bi]) {
+                            if (!short_rows && full[bi]) {
                                 add = -lse2[m];
                             } else if (short_rows) {
                                 add = outer_ok ? ain[m][bi][r] : -INFINITY;
@@ -323,7 +327,8 @@ struct DkvCfg {
     using Stg = Stager<T, D, kRows, kThreads>;
 };
 
-template <int R, int D, typename T, int KM, int SB>
+// SHORT = 1: every query-box row holds at most two 16-query blocks (rank >= 2).
+template <int R, int D, typename T, int KM, int SB, int SHORT>
 __global__ __launch_bounds__(256) void na_dkdv_kernel(Geo g, const T* __restrict__ qg,
                                                       const T* __restrict__ kg,
                                                       const T* __restrict__ vg,
@@ -424,7 +429,7 @@ __global__ __launch_bounds__(256) void na_dkdv_kernel(Geo g, const T* __restrict
         }
     // Query-box rows of at most two 16-query blocks: the inner-axis test of
     // this lane's 4 query slots is fixed, folded into 0 / -inf addends.
-    const bool short_rows = R > 1 && ibox.nbr <= 2;
+    constexpr bool short_rows = SHORT != 0 && R > 1;
     float ain[KM][2][4];
 #pragma unroll
     for (int m = 0; m < KM; ++m)
@@ -562,7 +567,7 @@ __global__ __launch_bounds__(256) void na_dkdv_kernel(Geo g, const T* __restrict
 #pragma unroll
                         for (int r = 0; r < 4; ++r) {
                             float add;
-                            if (full[bi]) {
+                            if (!short_rows && full[bi]) {
                                 add = nlse[bi][r];
                             } else if (short_rows) {
                                 add = outer_ok ? nlse[bi][r] + ain[m][bi][r] : -INFINITY;
@@ -631,6 +636,16 @@ static hipError_t launch_bwd_inst(const Geo& gq, const Geo& gk, const void* q, c
                                   hipStream_t stream) {
     constexpr int SBQ = sizeof(T) == 4 ? 2 : 4;
     constexpr int SBK = (sizeof(T) == 4 || D == 128) ? 2 : 4;
+    // rows of the halo (dQ) and of the query box (dK/dV) hold at most
+    // 2 blocks: interior extent min(T, n) + k - 1 along the innermost axis
+    bool short_rows = false;
+    if (R > 1) {
+        const int a = R - 1;
+        const int n0 = group_len(gq.L[a], gq.d[a], 0);
+        const int eq = std::min(std::min(gq.T[a], n0) + gq.k[a] - 1, n0);
+        const int ek = std::min(std::min(gk.T[a], n0) + gk.k[a] - 1, n0);
+        short_rows = (eq + 15) / 16 <= 2 && (ek + 15) / 16 <= 2;
+    }
     const T* tq = static_cast<const T*>(q);
     const T* tk = static_cast<const T*>(k);
     const T* tv = static_cast<const T*>(v);
@@ -650,7 +665,8 @@ static hipError_t launch_bwd_inst(const Geo& gq, const Geo& gk, const void* q, c
     // dK, dV
     {
         using C = DkvCfg<R, D, T, KM, SBK>;
-        auto kern = na_dkdv_kernel<R, D, T, KM, SBK>;
+        auto kern = short_rows ? na_dkdv_kernel<R, D, T, KM, SBK, 1>
+                               : na_dkdv_kernel<R, D, T, KM, SBK, 0>;
         hipError_t e = set_lds(kern, C::kLdsBytes);
         if (e != hipSuccess) return e;
         hipLaunchKernelGGL(kern, dim3(gk.nwg), dim3(C::kThreads), C::kLdsBytes, stream, gk, tq,
@@ -662,7 +678,8 @@ static hipError_t launch_bwd_inst(const Geo& gq, const Geo& gk, const void* q, c
     // dQ
     {
         using C = DqCfg<R, D, T, QM, SBQ>;
-        auto kern = na_dq_kernel<R, D, T, QM, SBQ>;
+        auto kern = short_rows ? na_dq_kernel<R, D, T, QM, SBQ, 1>
+                               : na_dq_kernel<R, D, T, QM, SBQ, 0>;
         hipError_t e = set_lds(kern, C::kLdsBytes);
         if (e != hipSuccess) return e;
         hipLaunchKernelGGL(kern, dim3(gq.nwg), dim3(C::kThreads), C::kLdsBytes, stream, gq, tq,
