@@ -48,6 +48,7 @@ struct FwdCfg {
     static constexpr int kKS = D / 32;  // contraction steps over D
     static constexpr int kDB = D / 16;  // 16-wide blocks of D
     using Stg = Stager<T, D, kKeys, kThreads>;
+    static_assert(SB % 2 == 0 && SB <= 32, "stage blocks are tested by one lane each");
 };
 
 // c = scale * log2(e): scores are kept in base 2.  SHORT = 1: every halo row
@@ -200,14 +201,29 @@ __global__ __launch_bounds__(256) void na_fwd_kernel(Geo g, const T* __restrict_
         const T* vt = ks + C::kKElems;
 
         if (wave_live) {
-#pragma unroll
-            for (int tp = 0; tp < SB / 2; ++tp) {
+            // lane j < SB tests block s*SB + j of the halo against this wave's
+            // queries; the wave then visits only the tiles (block pairs) with
+            // a relevant block, reading their coordinates back from the lanes
+            int loc[kMaxRank], lin0;
+            bool lrel, lfull;
+            wr.test(halo, s * SB + (lane < SB ? lane : 0), loc, lin0, lrel, lfull);
+            const uint64_t relm = __builtin_amdgcn_ballot_w64(lane < SB && lrel);
+            const uint64_t fullm = __builtin_amdgcn_ballot_w64(lane < SB && lfull);
+            uint64_t tiles = (relm | (relm >> 1)) & 0x5555555555555555ull;
+            while (tiles) {
+                const int tp = __builtin_ctzll(tiles) >> 1;
+                tiles &= tiles - 1;
                 bool rel[2], full[2];
                 int boc[2][kMaxRank], bin0[2];
 #pragma unroll
-                for (int bi = 0; bi < 2; ++bi)
-                    wr.test(halo, s * SB + tp * 2 + bi, boc[bi], bin0[bi], rel[bi], full[bi]);
-                if (!rel[0] && !rel[1]) continue;
+                for (int bi = 0; bi < 2; ++bi) {
+                    const int j = tp * 2 + bi;
+                    rel[bi] = (relm >> j) & 1;
+                    full[bi] = (fullm >> j) & 1;
+                    bin0[bi] = __builtin_amdgcn_readlane(lin0, j);
+#pragma unroll
+                    for (int a = 0; a < R - 1; ++a) boc[bi][a] = __builtin_amdgcn_readlane(loc[a], j);
+                }
 
                 // ---- S^T = K Q^T for both blocks ----
                 f32x4 sacc[QM][2];
