@@ -213,14 +213,28 @@ __global__ __launch_bounds__(256) void na_dq_kernel(Geo g, const T* __restrict__
         const T* kt = vs + C::kVElems;
 
         if (wave_live) {
-#pragma unroll 1
-            for (int tp = 0; tp < SB / 2; ++tp) {
+            // lane j < SB tests block s*SB + j; only tiles with a relevant
+            // block are visited, their coordinates read back from the lanes
+            int loc[kMaxRank], lin0;
+            bool lrel, lfull;
+            wr.test(halo, s * SB + (lane < SB ? lane : 0), loc, lin0, lrel, lfull);
+            const uint64_t relm = __builtin_amdgcn_ballot_w64(lane < SB && lrel);
+            const uint64_t fullm = __builtin_amdgcn_ballot_w64(lane < SB && lfull);
+            uint64_t tiles = (relm | (relm >> 1)) & 0x5555555555555555ull;
+            while (tiles) {
+                const int tp = __builtin_ctzll(tiles) >> 1;
+                tiles &= tiles - 1;
                 bool rel[2], full[2];
                 int boc[2][kMaxRank], bin0[2];
 #pragma unroll
-                for (int bi = 0; bi < 2; ++bi)
-                    wr.test(halo, s * SB + tp * 2 + bi, boc[bi], bin0[bi], rel[bi], full[bi]);
-                if (!rel[0] && !rel[1]) continue;
+                for (int bi = 0; bi < 2; ++bi) {
+                    const int j = tp * 2 + bi;
+                    rel[bi] = (relm >> j) & 1;
+                    full[bi] = (fullm >> j) & 1;
+                    bin0[bi] = __builtin_amdgcn_readlane(lin0, j);
+#pragma unroll
+                    for (int a = 0; a < R - 1; ++a) boc[bi][a] = __builtin_amdgcn_readlane(loc[a], j);
+                }
 
                 // S^T = K Q^T and dP^T = V dO^T
                 f32x4 sacc[QM][2], pacc[QM][2];
@@ -503,14 +517,28 @@ __global__ __launch_bounds__(256) void na_dkdv_kernel(Geo g, const T* __restrict
         const float* dls = ls + C::kRows;
 
         if (wave_live) {
-#pragma unroll 1
-            for (int tp = 0; tp < SB / 2; ++tp) {
+            // lane j < SB tests block s*SB + j; only tiles with a relevant
+            // block are visited, their coordinates read back from the lanes
+            int loc[kMaxRank], lin0;
+            bool lrel, lfull;
+            wr.test(ibox, s * SB + (lane < SB ? lane : 0), loc, lin0, lrel, lfull);
+            const uint64_t relm = __builtin_amdgcn_ballot_w64(lane < SB && lrel);
+            const uint64_t fullm = __builtin_amdgcn_ballot_w64(lane < SB && lfull);
+            uint64_t tiles = (relm | (relm >> 1)) & 0x5555555555555555ull;
+            while (tiles) {
+                const int tp = __builtin_ctzll(tiles) >> 1;
+                tiles &= tiles - 1;
                 bool rel[2], full[2];
                 int boc[2][kMaxRank], bin0[2];
 #pragma unroll
-                for (int bi = 0; bi < 2; ++bi)
-                    wr.test(ibox, s * SB + tp * 2 + bi, boc[bi], bin0[bi], rel[bi], full[bi]);
-                if (!rel[0] && !rel[1]) continue;
+                for (int bi = 0; bi < 2; ++bi) {
+                    const int j = tp * 2 + bi;
+                    rel[bi] = (relm >> j) & 1;
+                    full[bi] = (fullm >> j) & 1;
+                    bin0[bi] = __builtin_amdgcn_readlane(lin0, j);
+#pragma unroll
+                    for (int a = 0; a < R - 1; ++a) boc[bi][a] = __builtin_amdgcn_readlane(loc[a], j);
+                }
 
                 // S = Q K^T and dP = dO V^T (rows: queries, columns: this wave's keys)
                 f32x4 sacc[KM][2], pacc[KM][2];
