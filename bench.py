@@ -117,8 +117,6 @@ def main():
     out = torch.empty_like(q)
     lse = torch.empty(q.shape[:-1], dtype=torch.float32, device=dev)
     dq, dk, dv = torch.empty_like(q), torch.empty_like(k), torch.empty_like(v)
-    ws = torch.empty(na.workspace_bytes(p.extents, p.batch, p.heads), dtype=torch.uint8,
-                     device=dev)
     ks, ds, sc = p.kernel_size, p.dilation, p.softmax_scale
 
     def step(e0=None, e1=None, e2=None):
@@ -127,7 +125,7 @@ def main():
         na.forward(q, k, v, ks, ds, sc, out=out, lse=lse)
         if e1 is not None:
             e1.record()
-        na.backward(q, k, v, out, lse, g, ks, ds, sc, workspace=ws, dq=dq, dk=dk, dv=dv)
+        na.backward(q, k, v, out, lse, g, ks, ds, sc, dq=dq, dk=dk, dv=dv)
         if e2 is not None:
             e2.record()
 

@@ -21,9 +21,9 @@
  *   - logsumexp: contiguous [B, H, X_1 .. X_r] fp32 in device memory, natural
  *     log, scale included: lse = log sum_j exp(scale * q.k_j).
  *   - Every device pointer must be 16-byte aligned.
- *   - The caller owns all memory (including the backward workspace); the
- *     library never allocates or frees device memory, keeps no global state
- *     and is re-entrant.
+ *   - The caller owns all memory; the library never allocates or frees
+ *     device memory, needs no workspace, keeps no global state and is
+ *     re-entrant.
  *   - Calls are asynchronous and stream-ordered on `stream` (a hipStream_t;
  *     NULL means the legacy default stream).  Problem validation is
  *     synchronous and happens before any launch: a non-NA_OK status means
@@ -60,7 +60,7 @@ typedef enum {
     NA_ERR_HEAD_DIM = 7,              /* head_dim not in {32, 64, 128} */
     NA_ERR_DTYPE = 8,                 /* dtype not an na_dtype value */
     NA_ERR_ALIGNMENT = 9,             /* a device pointer is not 16-byte aligned */
-    NA_ERR_WORKSPACE = 10,            /* backward workspace missing or too small */
+    /* 10 is not used */
     NA_ERR_HIP = 11,                  /* a HIP launch or query failed */
     NA_ERR_SCALE = 12                 /* scale is not finite */
 } na_status;
@@ -92,26 +92,21 @@ na_status na_forward(int rank, const int64_t* extents, const int32_t* kernel_siz
                      na_dtype dtype, float scale, const void* q, const void* k, const void* v,
                      void* out, float* logsumexp, na_stream_t stream);
 
-/* Bytes of device workspace na_backward needs (the per-query Delta = dO.O, fp32). */
-size_t na_backward_workspace_bytes(int rank, const int64_t* extents, int64_t batch, int64_t heads);
-
 /*
  * Fused NA backward: gradients of out with respect to q, k and v given
  * dout, from the saved out and logsumexp of na_forward on the same inputs.
  * Built from the operators of Sec. 3.1: dP = PN(dO, V), dA = P * (dP - Delta),
  * dQ = scale * NN(dA, K) over each query's neighbourhood, and dK = scale *
  * IN(dA, Q), dV = IN(P, dO) over each key's inverse neighbourhood.
- *   dq, dk, dv are fully overwritten.  workspace: device memory of at least
- *   na_backward_workspace_bytes(...) bytes, 16-byte aligned, owned by the
- *   caller; its contents on entry do not matter.  Deterministic: the same
- *   inputs give bit-identical gradients.
+ *   Delta = rowsum(dO * O) is formed inside the kernels, so no workspace is
+ *   needed.  dq, dk, dv are fully overwritten and must not alias the inputs.
+ *   Deterministic: the same inputs give bit-identical gradients.
  */
 na_status na_backward(int rank, const int64_t* extents, const int32_t* kernel_size,
                       const int32_t* dilation, int64_t batch, int64_t heads, int64_t head_dim,
                       na_dtype dtype, float scale, const void* q, const void* k, const void* v,
                       const void* out, const float* logsumexp, const void* dout, void* dq,
-                      void* dk, void* dv, void* workspace, size_t workspace_bytes,
-                      na_stream_t stream);
+                      void* dk, void* dv, na_stream_t stream);
 
 /*
  * Test hook: evaluates on the device, with the same index functions the

@@ -17,7 +17,7 @@ import os
 import torch
 
 __all__ = ["NAError", "forward", "backward", "na_attention", "debug_windows", "validate",
-           "workspace_bytes", "library_path", "load_library", "DTYPES"]
+           "library_path", "load_library", "DTYPES"]
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
 # NA_LIBRARY may point at another build of the same library (A/B comparisons
@@ -63,9 +63,7 @@ def load_library():
     lib.na_validate.restype = ctypes.c_int
     lib.na_forward.argtypes = prob + [_vp] * 6
     lib.na_forward.restype = ctypes.c_int
-    lib.na_backward_workspace_bytes.argtypes = [ctypes.c_int, _i64p, ctypes.c_int64, ctypes.c_int64]
-    lib.na_backward_workspace_bytes.restype = ctypes.c_size_t
-    lib.na_backward.argtypes = prob + [_vp] * 10 + [ctypes.c_size_t, _vp]
+    lib.na_backward.argtypes = prob + [_vp] * 10
     lib.na_backward.restype = ctypes.c_int
     lib.na_debug_windows.argtypes = [ctypes.c_int, _i64p, _i32p, _i32p, _vp, _vp, _vp, _vp]
     lib.na_debug_windows.restype = ctypes.c_int
@@ -120,13 +118,6 @@ def validate(extents, kernel_size, dilation, batch, heads, head_dim, dtype, scal
     _check(lib.na_validate(rank, ext, ks, ds, batch, heads, head_dim, DTYPES[dtype], scale))
 
 
-def workspace_bytes(extents, batch, heads):
-    lib = load_library()
-    rank = len(extents)
-    ext = (ctypes.c_int64 * rank)(*[int(e) for e in extents])
-    return int(lib.na_backward_workspace_bytes(rank, ext, batch, heads))
-
-
 def forward(q, k, v, kernel_size, dilation=1, scale=None, out=None, lse=None):
     """Fused NA forward.  Returns (out, logsumexp); logsumexp is fp32 [B, H, X..]."""
     lib = load_library()
@@ -149,8 +140,8 @@ def forward(q, k, v, kernel_size, dilation=1, scale=None, out=None, lse=None):
     return out, lse
 
 
-def backward(q, k, v, out, lse, dout, kernel_size, dilation=1, scale=None, workspace=None,
-             dq=None, dk=None, dv=None):
+def backward(q, k, v, out, lse, dout, kernel_size, dilation=1, scale=None, dq=None, dk=None,
+             dv=None):
     """Fused NA backward.  Returns (dq, dk, dv)."""
     lib = load_library()
     _check_tensors(q, k, v, out, dout)
@@ -165,14 +156,10 @@ def backward(q, k, v, out, lse, dout, kernel_size, dilation=1, scale=None, works
     dk = torch.empty_like(k) if dk is None else dk
     dv = torch.empty_like(v) if dv is None else dv
     _check_tensors(q, dq, dk, dv)
-    need = int(lib.na_backward_workspace_bytes(rank, ext, B, H))
-    if workspace is None:
-        workspace = torch.empty(max(need, 16), dtype=torch.uint8, device=q.device)
     _check(lib.na_backward(rank, ext, ks, ds, B, H, D, DTYPES[q.dtype], float(scale),
                            q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(),
                            lse.data_ptr(), dout.data_ptr(), dq.data_ptr(), dk.data_ptr(),
-                           dv.data_ptr(), workspace.data_ptr(), workspace.numel(),
-                           _stream(q.device)))
+                           dv.data_ptr(), _stream(q.device)))
     return dq, dk, dv
 
 

@@ -180,7 +180,6 @@ const char* na_status_string(na_status status) {
         case NA_ERR_HEAD_DIM: return "head_dim must be 32, 64 or 128";
         case NA_ERR_DTYPE: return "unknown dtype";
         case NA_ERR_ALIGNMENT: return "device pointers must be 16-byte aligned";
-        case NA_ERR_WORKSPACE: return "backward workspace missing or too small";
         case NA_ERR_HIP: return "HIP launch failed";
         case NA_ERR_SCALE: return "scale must be finite";
     }
@@ -217,21 +216,11 @@ na_status na_forward(int rank, const int64_t* extents, const int32_t* kernel_siz
     return e == hipSuccess ? NA_OK : NA_ERR_HIP;
 }
 
-size_t na_backward_workspace_bytes(int rank, const int64_t* extents, int64_t batch,
-                                   int64_t heads) {
-    if (rank < 1 || rank > 3 || !extents || batch < 0 || heads < 0) return 0;
-    const int64_t N = token_count(rank, extents);
-    if (N < 0) return 0;
-    const size_t bytes = (size_t)(batch * heads * N) * sizeof(float);
-    return (bytes + 255) & ~size_t(255);
-}
-
 na_status na_backward(int rank, const int64_t* extents, const int32_t* kernel_size,
                       const int32_t* dilation, int64_t batch, int64_t heads, int64_t head_dim,
                       na_dtype dtype, float scale, const void* q, const void* k, const void* v,
                       const void* out, const float* logsumexp, const void* dout, void* dq,
-                      void* dk, void* dv, void* workspace, size_t workspace_bytes,
-                      na_stream_t stream) {
+                      void* dk, void* dv, na_stream_t stream) {
     na_status st = check_problem(rank, extents, kernel_size, dilation, batch, heads, head_dim,
                                  dtype, scale);
     if (st != NA_OK) return st;
@@ -240,17 +229,12 @@ na_status na_backward(int rank, const int64_t* extents, const int32_t* kernel_si
     const void* ptrs[] = {q, k, v, out, logsumexp, dout, dq, dk, dv};
     for (const void* p : ptrs)
         if (!aligned16(p)) return NA_ERR_ALIGNMENT;
-    if (!workspace || workspace_bytes < na_backward_workspace_bytes(rank, extents, batch, heads))
-        return NA_ERR_WORKSPACE;
-    if (!aligned16(workspace)) return NA_ERR_ALIGNMENT;
     const int64_t BH = batch * heads;
     const int m = choose_m(rank, extents, kernel_size, dilation, BH);
-    na::Geo gq, gk;
-    if (!make_geo(rank, extents, kernel_size, dilation, BH, m, gq)) return NA_ERR_SHAPE;
-    if (!make_geo(rank, extents, kernel_size, dilation, BH, m, gk)) return NA_ERR_SHAPE;
-    hipError_t e = na::launch_backward(gq, gk, rank, (int)head_dim, (int)dtype, m, m, q, k, v, out,
-                                       logsumexp, dout, dq, dk, dv,
-                                       static_cast<float*>(workspace), scale,
+    na::Geo g;
+    if (!make_geo(rank, extents, kernel_size, dilation, BH, m, g)) return NA_ERR_SHAPE;
+    hipError_t e = na::launch_backward(g, rank, (int)head_dim, (int)dtype, m, q, k, v, out,
+                                       logsumexp, dout, dq, dk, dv, scale,
                                        reinterpret_cast<hipStream_t>(stream));
     return e == hipSuccess ? NA_OK : NA_ERR_HIP;
 }

@@ -6,52 +6,23 @@
 //   NN  dQ = scale dA K    over each query's neighbourhood
 //   IN  dK = scale dA^T Q, dV = P^T dO  over each key's inverse neighbourhood
 // with dA = P * (dP - Delta), Delta = rowsum(dO * O), and P recomputed from
-// the logsumexp saved by the forward pass.  Three launches, no atomics, so the
-// result is deterministic:
-//   na_delta_kernel  Delta per query (bandwidth pass)
-//   na_dkdv_kernel   one workgroup per key tile; its queries are the union of
-//                    the tile's inverse neighbourhoods (Sec. 3.1: the relation
-//                    is not symmetric and a key may be attended by up to
-//                    k + floor(k/2) queries per axis)
-//   na_dq_kernel     one workgroup per query tile over its key halo, like the
-//                    forward pass
+// the logsumexp saved by the forward pass.  One launch, two workgroup roles,
+// no atomics and no workspace, so the result is deterministic:
+//   dK/dV role  one workgroup per key tile; its queries are the union of the
+//               tile's inverse neighbourhoods (Sec. 3.1: the relation is not
+//               symmetric and a key may be attended by up to k + floor(k/2)
+//               queries per axis); Delta of every staged query is formed
+//               while staging, from the O and dO rows
+//   dQ role     one workgroup per query tile over its key halo, like the
+//               forward pass; Delta of its own queries from their fragments
+// The roles are independent, so they share the GPU instead of running as
+// consecutive launches.
 #include <algorithm>
 
 #include "na_launch.h"
 #include "na_stage.h"
 
 namespace na {
-
-// ---------------------------------------------------------------------------
-// Delta = sum_c dO[c] * O[c] per query row, fp32.
-// ---------------------------------------------------------------------------
-template <int D, typename T>
-__global__ __launch_bounds__(256) void na_delta_kernel(const T* __restrict__ o,
-                                                       const T* __restrict__ dout,
-                                                       float* __restrict__ delta, int64_t rows) {
-    constexpr int kVec = Tr<T>::kVec;
-    constexpr int kLanes = D / kVec;  // lanes per row
-    constexpr int kRowsPerBlock = 256 / kLanes;
-    const int sub = threadIdx.x % kLanes;
-    const int64_t row = (int64_t)blockIdx.x * kRowsPerBlock + threadIdx.x / kLanes;
-    float acc = 0.f;
-    if (row < rows) {
-        const T* po = o + row * D + sub * kVec;
-        const T* pg = dout + row * D + sub * kVec;
-        if constexpr (sizeof(T) == 2) {
-            const typename Tr<T>::x8 a = ld_x8<T>(po), b = ld_x8<T>(pg);
-#pragma unroll
-            for (int j = 0; j < 8; ++j) acc += (float)a[j] * (float)b[j];
-        } else {
-            const f32x4 a = ld16<f32x4>(po), b = ld16<f32x4>(pg);
-#pragma unroll
-            for (int j = 0; j < 4; ++j) acc += a[j] * b[j];
-        }
-    }
-#pragma unroll
-    for (int w = 1; w < kLanes; w <<= 1) acc += __shfl_xor(acc, w, kWave);
-    if (row < rows && sub == 0) delta[row] = acc;
-}
 
 // ---------------------------------------------------------------------------
 // dQ: query-major, over each query tile's key halo.
@@ -74,18 +45,15 @@ struct DqCfg {
 
 // SHORT = 1: every halo row holds at most two 16-key blocks (rank >= 2), so
 // the inner-axis mask is a per-lane constant (chosen on the host).
+// braw: the workgroup's index among the dQ-role workgroups.
 template <int R, int D, typename T, int QM, int SB, int SHORT>
-__global__ __launch_bounds__(256) void na_dq_kernel(Geo g, const T* __restrict__ qg,
-                                                    const T* __restrict__ kg,
-                                                    const T* __restrict__ vg,
-                                                    const T* __restrict__ dog,
-                                                    const float* __restrict__ lseg,
-                                                    const float* __restrict__ deltag,
-                                                    T* __restrict__ dqg, float scale_log2,
-                                                    float scale) {
+__device__ __forceinline__ void dq_role(const Geo& g, int braw, unsigned char* smem_raw,
+                                        const T* __restrict__ qg, const T* __restrict__ kg,
+                                        const T* __restrict__ vg, const T* __restrict__ og,
+                                        const T* __restrict__ dog, const float* __restrict__ lseg,
+                                        T* __restrict__ dqg, float scale_log2, float scale) {
     using C = DqCfg<R, D, T, QM, SB>;
     using x8 = typename Tr<T>::x8;
-    extern __shared__ __align__(16) unsigned char smem_raw[];
     T* smem = reinterpret_cast<T*>(smem_raw);
 
     const int tid = threadIdx.x;
@@ -94,7 +62,7 @@ __global__ __launch_bounds__(256) void na_dq_kernel(Geo g, const T* __restrict__
     const int col = lane & 15;
     const int grp = lane >> 4;
 
-    const int bid = xcd_remap(blockIdx.x, g.nwg);
+    const int bid = xcd_remap(braw, g.nwg);
     int bh, gc[kMaxRank], tc[kMaxRank], n[kMaxRank], to[kMaxRank];
     decode_workgroup<R>(g, bid, bh, gc, tc, n);
 
@@ -133,7 +101,7 @@ __global__ __launch_bounds__(256) void na_dq_kernel(Geo g, const T* __restrict__
     int qs[QM][kMaxRank];
     bool qvalid[QM];
     size_t qoff[QM];
-    x8 qf[QM][C::kKS], gf[QM][C::kKS];
+    x8 qf[QM][C::kKS], gf[QM][C::kKS], of[QM][C::kKS];
     float lse2[QM], dlt[QM];
 #pragma unroll
     for (int m = 0; m < QM; ++m) {
@@ -157,9 +125,9 @@ __global__ __launch_bounds__(256) void na_dq_kernel(Geo g, const T* __restrict__
         for (int s = 0; s < C::kKS; ++s) {
             qf[m][s] = ld_x8<T>(qg + qoff[m] + s * 32 + grp * 8);
             gf[m][s] = ld_x8<T>(dog + qoff[m] + s * 32 + grp * 8);
+            of[m][s] = ld_x8<T>(og + qoff[m] + s * 32 + grp * 8);
         }
         lse2[m] = lseg[qoff[m] / D] * kLog2e;
-        dlt[m] = deltag[qoff[m] / D];
     }
 
     const int tstep = g.d[R - 1];
@@ -203,6 +171,14 @@ __global__ __launch_bounds__(256) void na_dq_kernel(Geo g, const T* __restrict__
 
     const int nst = (halo.nb + SB - 1) / SB;
     load_stage(0);
+    // Delta = dO . O of this lane's queries: 4 lanes hold a query's D slots
+#pragma unroll
+    for (int m = 0; m < QM; ++m) {
+        float part = 0.f;
+#pragma unroll
+        for (int s = 0; s < C::kKS; ++s) part = dot8<T>(of[m][s], gf[m][s], part);
+        dlt[m] = group_sum4(part);
+    }
     store_stage(0);
     __syncthreads();
 
@@ -342,18 +318,17 @@ struct DkvCfg {
 };
 
 // SHORT = 1: every query-box row holds at most two 16-query blocks (rank >= 2).
+// braw: the workgroup's index among the nwk dK/dV-role workgroups (nwk is
+// g.nwg rounded up to a multiple of the 8 XCDs; the surplus ones exit).
 template <int R, int D, typename T, int KM, int SB, int SHORT>
-__global__ __launch_bounds__(256) void na_dkdv_kernel(Geo g, const T* __restrict__ qg,
-                                                      const T* __restrict__ kg,
-                                                      const T* __restrict__ vg,
-                                                      const T* __restrict__ dog,
-                                                      const float* __restrict__ lseg,
-                                                      const float* __restrict__ deltag,
-                                                      T* __restrict__ dkg, T* __restrict__ dvg,
-                                                      float scale_log2, float scale) {
+__device__ __forceinline__ void dkdv_role(const Geo& g, int braw, int nwk,
+                                          unsigned char* smem_raw, const T* __restrict__ qg,
+                                          const T* __restrict__ kg, const T* __restrict__ vg,
+                                          const T* __restrict__ og, const T* __restrict__ dog,
+                                          const float* __restrict__ lseg, T* __restrict__ dkg,
+                                          T* __restrict__ dvg, float scale_log2, float scale) {
     using C = DkvCfg<R, D, T, KM, SB>;
     using x8 = typename Tr<T>::x8;
-    extern __shared__ __align__(16) unsigned char smem_raw[];
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -361,7 +336,8 @@ __global__ __launch_bounds__(256) void na_dkdv_kernel(Geo g, const T* __restrict
     const int col = lane & 15;  // key column of this lane
     const int grp = lane >> 4;
 
-    const int bid = xcd_remap(blockIdx.x, g.nwg);
+    const int bid = xcd_remap(braw, nwk);
+    if (bid >= g.nwg) return;
     int bh, gc[kMaxRank], tc[kMaxRank], n[kMaxRank], to[kMaxRank];
     decode_workgroup<R>(g, bid, bh, gc, tc, n);
 
@@ -380,8 +356,8 @@ __global__ __launch_bounds__(256) void na_dkdv_kernel(Geo g, const T* __restrict
     const size_t slice = (size_t)bh * g.N * D;
     const T* qb = qg + slice;
     const T* gb = dog + slice;
+    const T* ob = og + slice;
     const float* lb = lseg + (size_t)bh * g.N;
-    const float* db_ = deltag + (size_t)bh * g.N;
 
     // this wave's key sub-box: the queries that attend to any / all of its keys
     int wc[kMaxRank], wo[kMaxRank];
@@ -459,24 +435,24 @@ __global__ __launch_bounds__(256) void na_dkdv_kernel(Geo g, const T* __restrict
             }
 
     const int tstep = g.d[R - 1];
-    typename C::Stg qst, gst;
+    typename C::Stg qst, gst, ost;
     typename C::Stg::Addr addr;
-    float lse_reg = 0.f, dlt_reg = 0.f;
+    float lse_reg = 0.f;
     auto load_stage = [&](int s) {
         addr.compute(tid, [&](int quad, int& cnt) {
             return ibox.quad_token(g, gc, s * SB + (quad >> 2), (quad & 3) * 4, cnt);
         });
         qst.load(qb, tid, addr, tstep);
         gst.load(gb, tid, addr, tstep);
+        ost.load(ob, tid, addr, tstep);
         if (tid < C::kRows) {
             int cnt;
             const int tok = ibox.quad_token(g, gc, s * SB + (tid >> 4), tid & 12, cnt) +
                             (tid & 3) * tstep;
             const bool ok = (tid & 3) < cnt;
             const int tk = ok ? tok : 0;  // token 0 is a safe dummy address
-            const float lv = lb[tk], dv_ = db_[tk];
+            const float lv = lb[tk];
             lse_reg = ok ? lv * kLog2e : 0.f;
-            dlt_reg = ok ? dv_ : 0.f;
         }
     };
     auto buf_base = [&](int buf) { return smem_raw + buf * C::kBufBytes; };
@@ -487,10 +463,8 @@ __global__ __launch_bounds__(256) void na_dkdv_kernel(Geo g, const T* __restrict
         qst.store_cols(base + C::kQElems + C::kGElems, C::kCol, tid);
         gst.store_cols(base + C::kQElems + C::kGElems + C::kQtElems, C::kCol, tid);
         float* fl = reinterpret_cast<float*>(base + C::kTElems);
-        if (tid < C::kRows) {
-            fl[tid] = lse_reg;
-            fl[C::kRows + tid] = dlt_reg;
-        }
+        if (tid < C::kRows) fl[tid] = lse_reg;
+        store_row_dots(ost, gst, fl + C::kRows, tid);  // Delta of the staged queries
     };
 
     f32x4 dkacc[KM][C::kDB], dvacc[KM][C::kDB];
@@ -648,122 +622,110 @@ __global__ __launch_bounds__(256) void na_dkdv_kernel(Geo g, const T* __restrict
 }
 
 // ---------------------------------------------------------------------------
-// host-side launches
+// the kernel: workgroups [0, nwk) take the dK/dV role, the next g.nwg the dQ
+// role (dK/dV first: its workgroups carry more work and start earlier)
 // ---------------------------------------------------------------------------
-template <class K>
-static hipError_t set_lds(K kern, size_t bytes) {
-    if (bytes <= 65536) return hipSuccess;
-    return hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
-                               hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
+// 16-bit types with D <= 64 are held to 2 waves per SIMD (<= 256 registers).
+template <int D, typename T>
+constexpr int bwd_min_waves() {
+    return sizeof(T) == 2 && D <= 64 ? 2 : 1;
 }
 
+template <int R, int D, typename T, int QM, int KM, int SBQ, int SBK, int SHORT>
+__global__ __launch_bounds__(256, (bwd_min_waves<D, T>())) void na_bwd_kernel(Geo g, int nwk, const T* __restrict__ q,
+                                                     const T* __restrict__ k,
+                                                     const T* __restrict__ v,
+                                                     const T* __restrict__ o,
+                                                     const T* __restrict__ dout,
+                                                     const float* __restrict__ lse,
+                                                     T* __restrict__ dq, T* __restrict__ dk,
+                                                     T* __restrict__ dv, float scale_log2,
+                                                     float scale) {
+    extern __shared__ __align__(16) unsigned char smem_raw[];
+    const int b = blockIdx.x;
+    if (b < nwk)
+        dkdv_role<R, D, T, KM, SBK, SHORT>(g, b, nwk, smem_raw, q, k, v, o, dout, lse, dk, dv,
+                                           scale_log2, scale);
+    else
+        dq_role<R, D, T, QM, SBQ, SHORT>(g, b - nwk, smem_raw, q, k, v, o, dout, lse, dq,
+                                         scale_log2, scale);
+}
+
+// ---------------------------------------------------------------------------
+// host-side launch
+// ---------------------------------------------------------------------------
 template <int R, int D, typename T, int QM, int KM>
-static hipError_t launch_bwd_inst(const Geo& gq, const Geo& gk, const void* q, const void* k,
-                                  const void* v, const void* o, const float* lse, const void* dout,
-                                  void* dq, void* dk, void* dv, float* delta, float scale,
-                                  hipStream_t stream) {
+static hipError_t launch_bwd_inst(const Geo& g, const void* q, const void* k, const void* v,
+                                  const void* o, const float* lse, const void* dout, void* dq,
+                                  void* dk, void* dv, float scale, hipStream_t stream) {
     constexpr int SBQ = sizeof(T) == 4 ? 2 : 4;
     constexpr int SBK = (sizeof(T) == 4 || D == 128) ? 2 : 4;
-    // rows of the halo (dQ) and of the query box (dK/dV) hold at most
-    // 2 blocks: interior extent min(T, n) + k - 1 along the innermost axis
+    // rows of the halo (dQ) and of the query box (dK/dV) hold at most 2
+    // blocks: interior extent min(T, n) + k - 1 along the innermost axis
     bool short_rows = false;
     if (R > 1) {
         const int a = R - 1;
-        const int n0 = group_len(gq.L[a], gq.d[a], 0);
-        const int eq = std::min(std::min(gq.T[a], n0) + gq.k[a] - 1, n0);
-        const int ek = std::min(std::min(gk.T[a], n0) + gk.k[a] - 1, n0);
-        short_rows = (eq + 15) / 16 <= 2 && (ek + 15) / 16 <= 2;
+        const int n0 = group_len(g.L[a], g.d[a], 0);
+        short_rows = (std::min(std::min(g.T[a], n0) + g.k[a] - 1, n0) + 15) / 16 <= 2;
     }
-    const T* tq = static_cast<const T*>(q);
-    const T* tk = static_cast<const T*>(k);
-    const T* tv = static_cast<const T*>(v);
-    const T* tg = static_cast<const T*>(dout);
-
-    // Delta
-    {
-        constexpr int kLanes = D / Tr<T>::kVec;
-        constexpr int kRowsPerBlock = 256 / kLanes;
-        const int64_t rows = (int64_t)gq.BH * gq.N;
-        const int64_t blocks = (rows + kRowsPerBlock - 1) / kRowsPerBlock;
-        hipLaunchKernelGGL((na_delta_kernel<D, T>), dim3((unsigned)blocks), dim3(256), 0, stream,
-                           static_cast<const T*>(o), tg, delta, rows);
-        hipError_t e = hipGetLastError();
+    auto kern = short_rows ? na_bwd_kernel<R, D, T, QM, KM, SBQ, SBK, 1>
+                           : na_bwd_kernel<R, D, T, QM, KM, SBQ, SBK, 0>;
+    const size_t lds = std::max(DqCfg<R, D, T, QM, SBQ>::kLdsBytes,
+                                DkvCfg<R, D, T, KM, SBK>::kLdsBytes);
+    if (lds > 65536) {
+        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                                           hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
         if (e != hipSuccess) return e;
     }
-    // dK, dV
-    {
-        using C = DkvCfg<R, D, T, KM, SBK>;
-        auto kern = short_rows ? na_dkdv_kernel<R, D, T, KM, SBK, 1>
-                               : na_dkdv_kernel<R, D, T, KM, SBK, 0>;
-        hipError_t e = set_lds(kern, C::kLdsBytes);
-        if (e != hipSuccess) return e;
-        hipLaunchKernelGGL(kern, dim3(gk.nwg), dim3(C::kThreads), C::kLdsBytes, stream, gk, tq,
-                           tk, tv, tg, lse, delta, static_cast<T*>(dk), static_cast<T*>(dv),
-                           scale * kLog2e, scale);
-        e = hipGetLastError();
-        if (e != hipSuccess) return e;
-    }
-    // dQ
-    {
-        using C = DqCfg<R, D, T, QM, SBQ>;
-        auto kern = short_rows ? na_dq_kernel<R, D, T, QM, SBQ, 1>
-                               : na_dq_kernel<R, D, T, QM, SBQ, 0>;
-        hipError_t e = set_lds(kern, C::kLdsBytes);
-        if (e != hipSuccess) return e;
-        hipLaunchKernelGGL(kern, dim3(gq.nwg), dim3(C::kThreads), C::kLdsBytes, stream, gq, tq,
-                           tk, tv, tg, lse, delta, static_cast<T*>(dq), scale * kLog2e, scale);
-        return hipGetLastError();
-    }
+    const int nwk = (g.nwg + 7) & ~7;
+    hipLaunchKernelGGL(kern, dim3((unsigned)(nwk + g.nwg)), dim3(4 * kWave), lds, stream, g, nwk,
+                       static_cast<const T*>(q), static_cast<const T*>(k),
+                       static_cast<const T*>(v), static_cast<const T*>(o),
+                       static_cast<const T*>(dout), lse, static_cast<T*>(dq), static_cast<T*>(dk),
+                       static_cast<T*>(dv), scale * kLog2e, scale);
+    return hipGetLastError();
 }
 
 template <int R, int D, typename T>
-static hipError_t launch_bwd_m(const Geo& gq, const Geo& gk, int qm, int km, const void* q,
-                               const void* k, const void* v, const void* o, const float* lse,
-                               const void* dout, void* dq, void* dk, void* dv, float* delta,
-                               float scale, hipStream_t s) {
-    if (qm == 1 && km == 1)
-        return launch_bwd_inst<R, D, T, 1, 1>(gq, gk, q, k, v, o, lse, dout, dq, dk, dv, delta, scale, s);
-    if (qm == 1)
-        return launch_bwd_inst<R, D, T, 1, 2>(gq, gk, q, k, v, o, lse, dout, dq, dk, dv, delta, scale, s);
-    if (km == 1)
-        return launch_bwd_inst<R, D, T, 2, 1>(gq, gk, q, k, v, o, lse, dout, dq, dk, dv, delta, scale, s);
-    return launch_bwd_inst<R, D, T, 2, 2>(gq, gk, q, k, v, o, lse, dout, dq, dk, dv, delta, scale, s);
+static hipError_t launch_bwd_m(const Geo& g, int m, const void* q, const void* k, const void* v,
+                               const void* o, const float* lse, const void* dout, void* dq,
+                               void* dk, void* dv, float scale, hipStream_t s) {
+    if (m == 1) return launch_bwd_inst<R, D, T, 1, 1>(g, q, k, v, o, lse, dout, dq, dk, dv, scale, s);
+    return launch_bwd_inst<R, D, T, 2, 2>(g, q, k, v, o, lse, dout, dq, dk, dv, scale, s);
 }
 
 template <int R, typename T>
-static hipError_t launch_bwd_d(const Geo& gq, const Geo& gk, int D, int qm, int km, const void* q,
-                               const void* k, const void* v, const void* o, const float* lse,
-                               const void* dout, void* dq, void* dk, void* dv, float* delta,
-                               float scale, hipStream_t s) {
+static hipError_t launch_bwd_d(const Geo& g, int D, int m, const void* q, const void* k,
+                               const void* v, const void* o, const float* lse, const void* dout,
+                               void* dq, void* dk, void* dv, float scale, hipStream_t s) {
     switch (D) {
-        case 32: return launch_bwd_m<R, 32, T>(gq, gk, qm, km, q, k, v, o, lse, dout, dq, dk, dv, delta, scale, s);
-        case 64: return launch_bwd_m<R, 64, T>(gq, gk, qm, km, q, k, v, o, lse, dout, dq, dk, dv, delta, scale, s);
-        case 128: return launch_bwd_m<R, 128, T>(gq, gk, qm, km, q, k, v, o, lse, dout, dq, dk, dv, delta, scale, s);
+        case 32: return launch_bwd_m<R, 32, T>(g, m, q, k, v, o, lse, dout, dq, dk, dv, scale, s);
+        case 64: return launch_bwd_m<R, 64, T>(g, m, q, k, v, o, lse, dout, dq, dk, dv, scale, s);
+        case 128: return launch_bwd_m<R, 128, T>(g, m, q, k, v, o, lse, dout, dq, dk, dv, scale, s);
     }
     return hipErrorInvalidValue;
 }
 
 template <typename T>
-static hipError_t launch_bwd_r(const Geo& gq, const Geo& gk, int rank, int D, int qm, int km,
-                               const void* q, const void* k, const void* v, const void* o,
-                               const float* lse, const void* dout, void* dq, void* dk, void* dv,
-                               float* delta, float scale, hipStream_t s) {
+static hipError_t launch_bwd_r(const Geo& g, int rank, int D, int m, const void* q, const void* k,
+                               const void* v, const void* o, const float* lse, const void* dout,
+                               void* dq, void* dk, void* dv, float scale, hipStream_t s) {
     switch (rank) {
-        case 1: return launch_bwd_d<1, T>(gq, gk, D, qm, km, q, k, v, o, lse, dout, dq, dk, dv, delta, scale, s);
-        case 2: return launch_bwd_d<2, T>(gq, gk, D, qm, km, q, k, v, o, lse, dout, dq, dk, dv, delta, scale, s);
-        case 3: return launch_bwd_d<3, T>(gq, gk, D, qm, km, q, k, v, o, lse, dout, dq, dk, dv, delta, scale, s);
+        case 1: return launch_bwd_d<1, T>(g, D, m, q, k, v, o, lse, dout, dq, dk, dv, scale, s);
+        case 2: return launch_bwd_d<2, T>(g, D, m, q, k, v, o, lse, dout, dq, dk, dv, scale, s);
+        case 3: return launch_bwd_d<3, T>(g, D, m, q, k, v, o, lse, dout, dq, dk, dv, scale, s);
     }
     return hipErrorInvalidValue;
 }
 
-hipError_t launch_backward(const Geo& gq, const Geo& gk, int rank, int D, int dtype, int qm,
-                           int km, const void* q, const void* k, const void* v, const void* o,
-                           const float* lse, const void* dout, void* dq, void* dk, void* dv,
-                           float* delta, float scale, hipStream_t s) {
+hipError_t launch_backward(const Geo& g, int rank, int D, int dtype, int m, const void* q,
+                           const void* k, const void* v, const void* o, const float* lse,
+                           const void* dout, void* dq, void* dk, void* dv, float scale,
+                           hipStream_t s) {
     switch (dtype) {
-        case 0: return launch_bwd_r<float>(gq, gk, rank, D, qm, km, q, k, v, o, lse, dout, dq, dk, dv, delta, scale, s);
-        case 1: return launch_bwd_r<_Float16>(gq, gk, rank, D, qm, km, q, k, v, o, lse, dout, dq, dk, dv, delta, scale, s);
-        case 2: return launch_bwd_r<__bf16>(gq, gk, rank, D, qm, km, q, k, v, o, lse, dout, dq, dk, dv, delta, scale, s);
+        case 0: return launch_bwd_r<float>(g, rank, D, m, q, k, v, o, lse, dout, dq, dk, dv, scale, s);
+        case 1: return launch_bwd_r<_Float16>(g, rank, D, m, q, k, v, o, lse, dout, dq, dk, dv, scale, s);
+        case 2: return launch_bwd_r<__bf16>(g, rank, D, m, q, k, v, o, lse, dout, dq, dk, dv, scale, s);
     }
     return hipErrorInvalidValue;
 }

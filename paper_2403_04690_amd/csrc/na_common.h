@@ -173,6 +173,28 @@ __device__ __forceinline__ float row_sum8(typename Tr<T>::x8 pf, const float (&p
     }
 }
 
+// acc + sum_j a[j] * b[j] over one 8-slot fragment, accumulated in fp32
+// (16-bit types: four v_dot2 steps, the products are exact in fp32).
+template <typename T>
+__device__ __forceinline__ float dot8(typename Tr<T>::x8 a, typename Tr<T>::x8 b, float acc) {
+    if constexpr (sizeof(T) == 4) {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) acc = fmaf(a[j], b[j], acc);
+        return acc;
+    } else {
+        typedef T t2 __attribute__((ext_vector_type(2)));
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const t2 x = {a[2 * j], a[2 * j + 1]}, y = {b[2 * j], b[2 * j + 1]};
+            if constexpr (std::is_same<T, _Float16>::value)
+                acc = __builtin_amdgcn_fdot2(x, y, acc, false);
+            else
+                acc = __builtin_amdgcn_fdot2_f32_bf16(x, y, acc, false);
+        }
+        return acc;
+    }
+}
+
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
 // Division by a divisor that stays fixed for a whole launch or workgroup:
@@ -223,6 +245,28 @@ struct Geo {
     int lgWGd[kMaxRank]; // log2 WGd
     FastDiv fd_ntiles, fd_ngroups, fd_d[kMaxRank], fd_nt[kMaxRank];
 };
+
+// Brings the Geo fields of the problem's R axes into scalar registers in one
+// batch of loads: without it the compiler issues the kernel-argument loads
+// lazily, behind the early-exit branches, and the prologue pays one memory
+// round trip per group of fields.  The empty asm statement only consumes the
+// values (one statement: each volatile asm is a scheduling boundary).
+template <int R>
+__device__ __forceinline__ void fetch_geo(const Geo& g) {
+    constexpr int r1 = R > 1 ? 1 : 0, r2 = R > 2 ? 2 : 0;
+    asm volatile("" ::"s"(g.N), "s"(g.ngroups), "s"(g.ntiles), "s"(g.nwg),
+                 "s"(g.fd_ntiles.mul), "s"(g.fd_ntiles.shr), "s"(g.fd_ngroups.mul),
+                 "s"(g.fd_ngroups.shr),
+                 "s"(g.L[0]), "s"(g.k[0]), "s"(g.d[0]), "s"(g.ts[0]), "s"(g.T[0]), "s"(g.nt[0]),
+                 "s"(g.lgWT[0]), "s"(g.lgWGd[0]), "s"(g.fd_d[0].mul), "s"(g.fd_d[0].shr),
+                 "s"(g.fd_nt[0].mul), "s"(g.fd_nt[0].shr),
+                 "s"(g.L[r1]), "s"(g.k[r1]), "s"(g.d[r1]), "s"(g.ts[r1]), "s"(g.T[r1]),
+                 "s"(g.nt[r1]), "s"(g.lgWT[r1]), "s"(g.lgWGd[r1]), "s"(g.fd_d[r1].mul),
+                 "s"(g.fd_d[r1].shr), "s"(g.fd_nt[r1].mul), "s"(g.fd_nt[r1].shr),
+                 "s"(g.L[r2]), "s"(g.k[r2]), "s"(g.d[r2]), "s"(g.ts[r2]), "s"(g.T[r2]),
+                 "s"(g.nt[r2]), "s"(g.lgWT[r2]), "s"(g.lgWGd[r2]), "s"(g.fd_d[r2].mul),
+                 "s"(g.fd_d[r2].shr), "s"(g.fd_nt[r2].mul), "s"(g.fd_nt[r2].shr));
+}
 
 // Workgroup -> (batch*head, dilation group coordinates, tile coordinates) and
 // the length of this group along every axis.

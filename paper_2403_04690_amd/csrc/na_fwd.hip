@@ -71,6 +71,8 @@ __global__ __launch_bounds__(256) void na_fwd_kernel(Geo g, const T* __restrict_
     const int grp = lane >> 4;  // 16-lane group
 
     // ---- workgroup -> (bh, dilation group, tile) ----
+    fetch_geo<R>(g);
+    asm volatile("" ::"s"(qg), "s"(kg), "s"(vg), "s"(og), "s"(lseg), "s"(c));
     const int bid = xcd_remap(blockIdx.x, g.nwg);
     int bh, gc[kMaxRank], tc[kMaxRank], n[kMaxRank], to[kMaxRank];
     decode_workgroup<R>(g, bid, bh, gc, tc, n);
@@ -226,21 +228,38 @@ __global__ __launch_bounds__(256) void na_fwd_kernel(Geo g, const T* __restrict_
                 }
 
                 // ---- S^T = K Q^T for both blocks ----
+                // Both blocks are read and multiplied without a branch: a block
+                // outside this wave's halo is masked below, and every row of
+                // the stage buffer holds finite data (absent rows are zero).
+                // The V fragments of the tile are read here too (D = 32), so
+                // one LDS round trip serves the whole tile.
+                x8 kf[2][C::kKS];
+#pragma unroll
+                for (int bi = 0; bi < 2; ++bi)
+#pragma unroll
+                    for (int st = 0; st < C::kKS; ++st)
+                        kf[bi][st] = ld_x8<T>(ks + ((tp * 2 + bi) * 16 + col) * C::kKRow +
+                                              st * 32 + grp * 8);
+                constexpr bool kEarlyV = D == 32;
+                x8 vf[C::kDB];
+                auto read_v = [&]() {
+#pragma unroll
+                    for (int db = 0; db < C::kDB; ++db) {
+                        const T* vrow = vt + (db * 16 + col) * C::kVCol + tp * 32 + grp * 4;
+                        vf[db] = cat_x4<T>(ld_x4<T>(vrow), ld_x4<T>(vrow + 16));
+                    }
+                };
+                if (kEarlyV) read_v();
                 f32x4 sacc[QM][2];
 #pragma unroll
-                for (int bi = 0; bi < 2; ++bi) {
+                for (int bi = 0; bi < 2; ++bi)
 #pragma unroll
-                    for (int m = 0; m < QM; ++m) sacc[m][bi] = f32x4{0.f, 0.f, 0.f, 0.f};
-                    if (!rel[bi]) continue;
-                    const T* krow = ks + ((tp * 2 + bi) * 16 + col) * C::kKRow + grp * 8;
+                    for (int m = 0; m < QM; ++m) {
+                        sacc[m][bi] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-                    for (int st = 0; st < C::kKS; ++st) {
-                        const x8 kf = ld_x8<T>(krow + st * 32);
-#pragma unroll
-                        for (int m = 0; m < QM; ++m)
-                            sacc[m][bi] = Tr<T>::mma(kf, qf[m][st], sacc[m][bi]);
+                        for (int st = 0; st < C::kKS; ++st)
+                            sacc[m][bi] = Tr<T>::mma(kf[bi][st], qf[m][st], sacc[m][bi]);
                     }
-                }
 
                 // ---- mask + online softmax per query block ----
                 // y = scale*log2(e)*s - m (base 2, relative to the running
@@ -318,13 +337,11 @@ __global__ __launch_bounds__(256) void na_fwd_kernel(Geo g, const T* __restrict_
                 }
 
                 // ---- O^T += V^T P^T ----
+                if (!kEarlyV) read_v();
 #pragma unroll
-                for (int db = 0; db < C::kDB; ++db) {
-                    const T* vrow = vt + (db * 16 + col) * C::kVCol + tp * 32 + grp * 4;
-                    const x8 vf = cat_x4<T>(ld_x4<T>(vrow), ld_x4<T>(vrow + 16));
+                for (int db = 0; db < C::kDB; ++db)
 #pragma unroll
-                    for (int m = 0; m < QM; ++m) oacc[m][db] = Tr<T>::mma(vf, pf[m], oacc[m][db]);
-                }
+                    for (int m = 0; m < QM; ++m) oacc[m][db] = Tr<T>::mma(vf[db], pf[m], oacc[m][db]);
             }
         }
 

@@ -12,11 +12,11 @@ hipError_t launch_forward(const Geo& g, int rank, int D, int dtype, int qm, cons
                           const void* k, const void* v, void* o, float* lse, float scale,
                           hipStream_t s);
 
-// Backward: Delta pre-pass, then dK/dV (inverse neighbourhoods) and dQ.
-hipError_t launch_backward(const Geo& gq, const Geo& gk, int rank, int D, int dtype, int qm,
-                           int km, const void* q, const void* k, const void* v, const void* o,
-                           const float* lse, const void* dout, void* dq, void* dk, void* dv,
-                           float* delta, float scale, hipStream_t s);
+// Backward: one launch of dK/dV-role and dQ-role workgroups (Delta in-kernel).
+hipError_t launch_backward(const Geo& g, int rank, int D, int dtype, int m, const void* q,
+                           const void* k, const void* v, const void* o, const float* lse,
+                           const void* dout, void* dq, void* dk, void* dv, float scale,
+                           hipStream_t s);
 
 // Per-axis window starts and inverse ranges (absolute coordinates), int32.
 hipError_t launch_debug_windows(int rank, const int* L, const int* k, const int* d, int* start,

@@ -181,6 +181,42 @@ struct Stager {
     }
 };
 
+// Row-wise dot products of two stagers loaded from the same addresses, in
+// fp32: the kSegs lanes that hold one quad's segments reduce their partial
+// sums with lane shuffles (a fixed order, so the result is deterministic)
+// and the lane of segment 0 writes the quad's 4 sums to dst[4 * quad ...].
+// Absent rows were zero-filled by load() and give 0.
+template <typename T, int D, int ROWS, int NT>
+__device__ __forceinline__ void store_row_dots(const Stager<T, D, ROWS, NT>& a,
+                                               const Stager<T, D, ROWS, NT>& b, float* dst,
+                                               int tid) {
+    using S = Stager<T, D, ROWS, NT>;
+    using x8 = typename Tr<T>::x8;
+    static_assert(kWave % S::kSegs == 0 && NT % S::kSegs == 0, "a quad's segments share a wave");
+#pragma unroll
+    for (int it = 0; it < S::kItems; ++it) {
+        const int i = tid + it * NT;
+        float s[4];
+#pragma unroll
+        for (int rr = 0; rr < 4; ++rr) {
+            if constexpr (sizeof(T) == 2) {
+                s[rr] = dot8<T>(__builtin_bit_cast(x8, a.r[it][rr]),
+                                __builtin_bit_cast(x8, b.r[it][rr]), 0.f);
+            } else {
+                const f32x4 x = __builtin_bit_cast(f32x4, a.r[it][rr]);
+                const f32x4 y = __builtin_bit_cast(f32x4, b.r[it][rr]);
+                s[rr] = fmaf(x[3], y[3], fmaf(x[2], y[2], fmaf(x[1], y[1], x[0] * y[0])));
+            }
+        }
+#pragma unroll
+        for (int w = 1; w < S::kSegs; w <<= 1)
+#pragma unroll
+            for (int rr = 0; rr < 4; ++rr) s[rr] += __shfl_xor(s[rr], w, kWave);
+        if (i < S::kQuads * S::kSegs && i % S::kSegs == 0)
+            st16<f32x4>(dst + (i / S::kSegs) * 4, f32x4{s[0], s[1], s[2], s[3]});
+    }
+}
+
 // LDS row strides: row-major rows get a 16-byte pad, transposed lines a
 // 4-element pad (keeps 16-byte alignment for fp32 and 8-byte for 16-bit).
 template <typename T, int D>
