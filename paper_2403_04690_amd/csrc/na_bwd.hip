@@ -31,16 +31,12 @@ template <int R, int D, typename T, int QM, int SB>
 struct DqCfg {
     static constexpr int kThreads = 4 * kWave;
     static constexpr int kKeys = SB * 16;
-    static constexpr int kRow = RowLayout<T, D>::kRow;
-    static constexpr int kCol = ColLayout<kKeys>::kCol;
-    static constexpr int kKElems = kKeys * kRow;    // K rows
-    static constexpr int kVElems = kKeys * kRow;    // V rows
-    static constexpr int kKtElems = D * kCol;       // K transposed
-    static constexpr int kBufElems = kKElems + kVElems + kKtElems;
-    static constexpr size_t kLdsBytes = 2 * kBufElems * sizeof(T);
+    static constexpr int kTileBytes = kKeys * Rows<T, D>::kRowBytes;
+    static constexpr size_t kBufBytes = 2 * kTileBytes;  // K rows, then V rows
+    static constexpr size_t kLdsBytes = 2 * kBufBytes;
     static constexpr int kKS = D / 32;
     static constexpr int kDB = D / 16;
-    using Stg = Stager<T, D, kKeys, kThreads>;
+    using Ld = DirectRows<T, D, kKeys>;
 };
 
 // SHORT = 1: every halo row holds at most two 16-key blocks (rank >= 2), so
@@ -54,7 +50,7 @@ __device__ __forceinline__ void dq_role(const Geo& g, int braw, unsigned char* s
                                         T* __restrict__ dqg, float scale_log2, float scale) {
     using C = DqCfg<R, D, T, QM, SB>;
     using x8 = typename Tr<T>::x8;
-    T* smem = reinterpret_cast<T*>(smem_raw);
+    constexpr int kRowB = Rows<T, D>::kRowBytes;
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -131,21 +127,17 @@ __device__ __forceinline__ void dq_role(const Geo& g, int braw, unsigned char* s
     }
 
     const int tstep = g.d[R - 1];
-    typename C::Stg kst, vst;
-    typename C::Stg::Addr addr;
-    auto load_stage = [&](int s) {
-        addr.compute(tid, [&](int quad, int& cnt) {
-            return halo.quad_token(g, gc, s * SB + (quad >> 2), (quad & 3) * 4, cnt);
-        });
-        kst.load(kb, tid, addr, tstep);
-        vst.load(vb, tid, addr, tstep);
+    typename C::Ld ld;
+    auto issue_stage = [&](int s, int buf) {
+        ld.compute(halo, g, gc, s * SB, tstep, wave, lane);
+        unsigned char* tile = smem_raw + buf * C::kBufBytes;
+        ld.issue(kb, tile, wave);
+        ld.issue(vb, tile + C::kTileBytes, wave);
     };
-    auto store_stage = [&](int buf) {
-        T* base = smem + buf * C::kBufElems;
-        kst.store_rows(base, C::kRow, tid);
-        vst.store_rows(base + C::kKElems, C::kRow, tid);
-        kst.store_cols(base + C::kKElems + C::kVElems, C::kCol, tid);
-    };
+    RowFrag<T, D> rfr;
+    ColFrag<T, D> cfr;
+    rfr.init(lane);
+    cfr.init(lane);
 
     f32x4 dqacc[QM][C::kDB];
 #pragma unroll
@@ -170,7 +162,7 @@ __device__ __forceinline__ void dq_role(const Geo& g, int braw, unsigned char* s
             }
 
     const int nst = (halo.nb + SB - 1) / SB;
-    load_stage(0);
+    issue_stage(0, 0);
     // Delta = dO . O of this lane's queries: 4 lanes hold a query's D slots
 #pragma unroll
     for (int m = 0; m < QM; ++m) {
@@ -179,14 +171,13 @@ __device__ __forceinline__ void dq_role(const Geo& g, int braw, unsigned char* s
         for (int s = 0; s < C::kKS; ++s) part = dot8<T>(of[m][s], gf[m][s], part);
         dlt[m] = group_sum4(part);
     }
-    store_stage(0);
+    wait_vmem();
     __syncthreads();
 
     for (int s = 0; s < nst; ++s) {
-        if (s + 1 < nst) load_stage(s + 1);
-        const T* ks = smem + (s & 1) * C::kBufElems;
-        const T* vs = ks + C::kKElems;
-        const T* kt = vs + C::kVElems;
+        if (s + 1 < nst) issue_stage(s + 1, (s + 1) & 1);
+        const unsigned char* ks = smem_raw + (s & 1) * C::kBufBytes;
+        const unsigned char* vs = ks + C::kTileBytes;
 
         if (wave_live) {
             // lane j < SB tests block s*SB + j; only tiles with a relevant
@@ -217,11 +208,11 @@ __device__ __forceinline__ void dq_role(const Geo& g, int braw, unsigned char* s
 #pragma unroll
                 for (int bi = 0; bi < 2; ++bi) {
                     if (rel[bi]) {
-                        const int row = (tp * 2 + bi) * 16 + col;
+                        const int boff = (tp * 2 + bi) * 16 * kRowB;
 #pragma unroll
                         for (int st = 0; st < C::kKS; ++st) {
-                            const x8 kf = ld_x8<T>(ks + row * C::kRow + st * 32 + grp * 8);
-                            const x8 vf = ld_x8<T>(vs + row * C::kRow + st * 32 + grp * 8);
+                            const x8 kf = rfr.read(ks + boff, st);
+                            const x8 vf = rfr.read(vs + boff, st);
 #pragma unroll
                             for (int m = 0; m < QM; ++m) {
                                 const f32x4 z = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -271,18 +262,17 @@ __device__ __forceinline__ void dq_role(const Geo& g, int braw, unsigned char* s
                                 Tr<T>::cvt(ds[1][2]), Tr<T>::cvt(ds[1][3])};
                 }
 
-                // dQ^T += K^T dA^T
+                // dQ^T += K^T dA^T (K^T read transposed from the K rows)
 #pragma unroll
                 for (int db = 0; db < C::kDB; ++db) {
-                    const T* krow = kt + (db * 16 + col) * C::kCol + tp * 32 + grp * 4;
-                    const x8 kf = cat_x4<T>(ld_x4<T>(krow), ld_x4<T>(krow + 16));
+                    const x8 kf = cfr.read(ks + tp * 32 * kRowB, db, lane);
 #pragma unroll
                     for (int m = 0; m < QM; ++m) dqacc[m][db] = Tr<T>::mma(kf, dsf[m], dqacc[m][db]);
                 }
             }
         }
 
-        if (s + 1 < nst) store_stage((s + 1) & 1);
+        if (s + 1 < nst) wait_vmem();
         __syncthreads();
     }
 
@@ -302,19 +292,13 @@ template <int R, int D, typename T, int KM, int SB>
 struct DkvCfg {
     static constexpr int kThreads = 4 * kWave;
     static constexpr int kRows = SB * 16;  // queries per stage
-    static constexpr int kRow = RowLayout<T, D>::kRow;
-    static constexpr int kCol = ColLayout<kRows>::kCol;
-    static constexpr int kQElems = kRows * kRow;   // Q rows
-    static constexpr int kGElems = kRows * kRow;   // dO rows
-    static constexpr int kQtElems = D * kCol;      // Q transposed
-    static constexpr int kGtElems = D * kCol;      // dO transposed
-    static constexpr int kTElems = kQElems + kGElems + kQtElems + kGtElems;
-    // fp32 lse (base 2) and Delta per staged query follow the element tiles
-    static constexpr size_t kBufBytes = kTElems * sizeof(T) + 2 * kRows * sizeof(float);
+    static constexpr int kTileBytes = kRows * Rows<T, D>::kRowBytes;
+    // Q rows, dO rows, O rows, then fp32 lse (base 2) and Delta per query
+    static constexpr size_t kBufBytes = 3 * kTileBytes + 2 * kRows * sizeof(float);
     static constexpr size_t kLdsBytes = 2 * kBufBytes;
     static constexpr int kKS = D / 32;
     static constexpr int kDB = D / 16;
-    using Stg = Stager<T, D, kRows, kThreads>;
+    using Ld = DirectRows<T, D, kRows>;
 };
 
 // SHORT = 1: every query-box row holds at most two 16-query blocks (rank >= 2).
@@ -435,37 +419,59 @@ __device__ __forceinline__ void dkdv_role(const Geo& g, int braw, int nwk,
             }
 
     const int tstep = g.d[R - 1];
-    typename C::Stg qst, gst, ost;
-    typename C::Stg::Addr addr;
+    typename C::Ld ld;
     float lse_reg = 0.f;
-    auto load_stage = [&](int s) {
-        addr.compute(tid, [&](int quad, int& cnt) {
-            return ibox.quad_token(g, gc, s * SB + (quad >> 2), (quad & 3) * 4, cnt);
-        });
-        qst.load(qb, tid, addr, tstep);
-        gst.load(gb, tid, addr, tstep);
-        ost.load(ob, tid, addr, tstep);
+    auto issue_stage = [&](int s, int buf) {
+        ld.compute(ibox, g, gc, s * SB, tstep, wave, lane);
+        unsigned char* tile = smem_raw + buf * C::kBufBytes;
+        ld.issue(qb, tile, wave);
+        ld.issue(gb, tile + C::kTileBytes, wave);
+        ld.issue(ob, tile + 2 * C::kTileBytes, wave);
         if (tid < C::kRows) {
-            int cnt;
-            const int tok = ibox.quad_token(g, gc, s * SB + (tid >> 4), tid & 12, cnt) +
-                            (tid & 3) * tstep;
-            const bool ok = (tid & 3) < cnt;
-            const int tk = ok ? tok : 0;  // token 0 is a safe dummy address
-            const float lv = lb[tk];
+            int valid;
+            const int tok0 = ibox.block_token(g, gc, s * SB + (tid >> 4), valid);
+            const bool ok = (tid & 15) < valid;
+            const float lv = lb[ok ? tok0 + (tid & 15) * tstep : 0];  // token 0: safe stand-in
             lse_reg = ok ? lv * kLog2e : 0.f;
         }
     };
-    auto buf_base = [&](int buf) { return smem_raw + buf * C::kBufBytes; };
-    auto store_stage = [&](int buf) {
-        T* base = reinterpret_cast<T*>(buf_base(buf));
-        qst.store_rows(base, C::kRow, tid);
-        gst.store_rows(base + C::kQElems, C::kRow, tid);
-        qst.store_cols(base + C::kQElems + C::kGElems, C::kCol, tid);
-        gst.store_cols(base + C::kQElems + C::kGElems + C::kQtElems, C::kCol, tid);
-        float* fl = reinterpret_cast<float*>(base + C::kTElems);
-        if (tid < C::kRows) fl[tid] = lse_reg;
-        store_row_dots(ost, gst, fl + C::kRows, tid);  // Delta of the staged queries
+    auto floats = [&](int buf) {
+        return reinterpret_cast<float*>(smem_raw + buf * C::kBufBytes + 3 * C::kTileBytes);
     };
+    // Delta = dO . O of the stage's staged queries, from their LDS rows
+    // (kThreads / kRows lanes per query, reduced with lane shuffles)
+    auto delta_pass = [&](int buf) {
+        using L = Rows<T, D>;
+        constexpr int kP = C::kThreads / C::kRows;
+        constexpr int kSpt = (L::kSegs + kP - 1) / kP;
+        const unsigned char* gt = smem_raw + buf * C::kBufBytes + C::kTileBytes;
+        const unsigned char* ot = gt + C::kTileBytes;
+        const int row = tid / kP, part = tid % kP;
+        float acc = 0.f;
+#pragma unroll
+        for (int i = 0; i < kSpt; ++i) {
+            const int seg = part * kSpt + i;
+            if (seg < L::kSegs) {
+                const int o = L::off(row, seg);
+                if constexpr (sizeof(T) == 2) {
+                    acc = dot8<T>(__builtin_bit_cast(x8, lds16(gt + o)),
+                                  __builtin_bit_cast(x8, lds16(ot + o)), acc);
+                } else {
+                    const f32x4 a = __builtin_bit_cast(f32x4, lds16(gt + o));
+                    const f32x4 b = __builtin_bit_cast(f32x4, lds16(ot + o));
+                    acc = fmaf(a[3], b[3], fmaf(a[2], b[2], fmaf(a[1], b[1], fmaf(a[0], b[0], acc))));
+                }
+            }
+        }
+#pragma unroll
+        for (int w = 1; w < kP; w <<= 1) acc += __shfl_xor(acc, w, kWave);
+        if (part == 0) floats(buf)[C::kRows + row] = acc;
+    };
+    RowFrag<T, D> rfr;
+    ColFrag<T, D> cfr;
+    rfr.init(lane);
+    cfr.init(lane);
+    constexpr int kRowB = Rows<T, D>::kRowBytes;
 
     f32x4 dkacc[KM][C::kDB], dvacc[KM][C::kDB];
 #pragma unroll
@@ -477,17 +483,18 @@ __device__ __forceinline__ void dkdv_role(const Geo& g, int braw, int nwk,
         }
 
     const int nst = (ibox.nb + SB - 1) / SB;
-    load_stage(0);
-    store_stage(0);
+    issue_stage(0, 0);
+    if (tid < C::kRows) floats(0)[tid] = lse_reg;
+    wait_vmem();
+    __syncthreads();
+    delta_pass(0);
     __syncthreads();
 
     for (int s = 0; s < nst; ++s) {
-        if (s + 1 < nst) load_stage(s + 1);
-        const T* qs = reinterpret_cast<const T*>(buf_base(s & 1));
-        const T* gs = qs + C::kQElems;
-        const T* qt = gs + C::kGElems;
-        const T* gt = qt + C::kQtElems;
-        const float* ls = reinterpret_cast<const float*>(qs + C::kTElems);
+        if (s + 1 < nst) issue_stage(s + 1, (s + 1) & 1);
+        const unsigned char* qs = smem_raw + (s & 1) * C::kBufBytes;
+        const unsigned char* gs = qs + C::kTileBytes;
+        const float* ls = floats(s & 1);
         const float* dls = ls + C::kRows;
 
         if (wave_live) {
@@ -519,11 +526,11 @@ __device__ __forceinline__ void dkdv_role(const Geo& g, int braw, int nwk,
 #pragma unroll
                 for (int bi = 0; bi < 2; ++bi) {
                     if (rel[bi]) {
-                        const int row = (tp * 2 + bi) * 16 + col;
+                        const int boff = (tp * 2 + bi) * 16 * kRowB;
 #pragma unroll
                         for (int st = 0; st < C::kKS; ++st) {
-                            const x8 qa = ld_x8<T>(qs + row * C::kRow + st * 32 + grp * 8);
-                            const x8 ga = ld_x8<T>(gs + row * C::kRow + st * 32 + grp * 8);
+                            const x8 qa = rfr.read(qs + boff, st);
+                            const x8 ga = rfr.read(gs + boff, st);
 #pragma unroll
                             for (int m = 0; m < KM; ++m) {
                                 const f32x4 z = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -591,12 +598,11 @@ __device__ __forceinline__ void dkdv_role(const Geo& g, int braw, int nwk,
                                 Tr<T>::cvt(ds[1][2]), Tr<T>::cvt(ds[1][3])};
                 }
 
-                // dV^T += dO^T P and dK^T += Q^T dA
+                // dV^T += dO^T P and dK^T += Q^T dA (transposed reads of the rows)
 #pragma unroll
                 for (int d = 0; d < C::kDB; ++d) {
-                    const int line = (d * 16 + col) * C::kCol + tp * 32 + grp * 4;
-                    const x8 ga = cat_x4<T>(ld_x4<T>(gt + line), ld_x4<T>(gt + line + 16));
-                    const x8 qa = cat_x4<T>(ld_x4<T>(qt + line), ld_x4<T>(qt + line + 16));
+                    const x8 ga = cfr.read(gs + tp * 32 * kRowB, d, lane);
+                    const x8 qa = cfr.read(qs + tp * 32 * kRowB, d, lane);
 #pragma unroll
                     for (int m = 0; m < KM; ++m) {
                         dvacc[m][d] = Tr<T>::mma(ga, pf[m], dvacc[m][d]);
@@ -606,8 +612,15 @@ __device__ __forceinline__ void dkdv_role(const Geo& g, int braw, int nwk,
             }
         }
 
-        if (s + 1 < nst) store_stage((s + 1) & 1);
+        if (s + 1 < nst) {
+            if (tid < C::kRows) floats((s + 1) & 1)[tid] = lse_reg;
+            wait_vmem();
+        }
         __syncthreads();
+        if (s + 1 < nst) {
+            delta_pass((s + 1) & 1);
+            __syncthreads();
+        }
     }
 
 #pragma unroll

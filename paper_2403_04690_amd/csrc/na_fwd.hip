@@ -11,10 +11,10 @@
 //   * workgroup = 4 waves = one query tile of one (batch, head, dilation
 //     group); each wave owns QM x 16 queries of it (a sub-box);
 //   * the workgroup's key halo is cut into blocks of 16 keys that run along
-//     the innermost axis; stages of SB blocks are staged in LDS (double
-//     buffered when there is more than one stage), K row-major and V
-//     transposed, by 16-byte loads whose addresses are computed once per
-//     4 keys and shared by K and V;
+//     the innermost axis; stages of SB blocks go straight from HBM to LDS
+//     (16-byte direct-to-LDS loads, double buffered when there is more than
+//     one stage), K and V both as swizzled unpadded rows; V^T fragments are
+//     gathered with the transposed LDS read, so no transposed copy exists;
 //   * a wave only runs the matrix cores on blocks that intersect its own
 //     sub-box halo, and evaluates the mask only on blocks that are not inside
 //     every one of its windows;
@@ -39,15 +39,11 @@ template <int R, int D, typename T, int QM, int SB>
 struct FwdCfg {
     static constexpr int kThreads = 4 * kWave;
     static constexpr int kKeys = SB * 16;  // keys per stage
-    static constexpr int kKRow = RowLayout<T, D>::kRow;
-    static constexpr int kVCol = ColLayout<kKeys>::kCol;
-    static constexpr int kKElems = kKeys * kKRow;
-    static constexpr int kVElems = D * kVCol;
-    static constexpr int kBufElems = kKElems + kVElems;
-    static constexpr size_t kBufBytes = kBufElems * sizeof(T);
+    static constexpr int kTileBytes = kKeys * Rows<T, D>::kRowBytes;
+    static constexpr size_t kBufBytes = 2 * kTileBytes;  // K rows, then V rows
     static constexpr int kKS = D / 32;  // contraction steps over D
     static constexpr int kDB = D / 16;  // 16-wide blocks of D
-    using Stg = Stager<T, D, kKeys, kThreads>;
+    using Ld = DirectRows<T, D, kKeys>;
     static_assert(SB % 2 == 0 && SB <= 32, "stage blocks are tested by one lane each");
 };
 
@@ -62,7 +58,6 @@ __global__ __launch_bounds__(256) void na_fwd_kernel(Geo g, const T* __restrict_
     using C = FwdCfg<R, D, T, QM, SB>;
     using x8 = typename Tr<T>::x8;
     extern __shared__ __align__(16) unsigned char smem_raw[];
-    T* smem = reinterpret_cast<T*>(smem_raw);
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -138,21 +133,18 @@ __global__ __launch_bounds__(256) void na_fwd_kernel(Geo g, const T* __restrict_
         for (int s = 0; s < C::kKS; ++s) qf[m][s] = ld_x8<T>(qg + qoff[m] + s * 32 + grp * 8);
     }
 
-    // ---- staging of K (row-major) and V (transposed), one address set for both ----
-    typename C::Stg kst, vst;
-    typename C::Stg::Addr addr;
-    auto load_stage = [&](int s) {
-        addr.compute(tid, [&](int quad, int& cnt) {
-            return halo.quad_token(g, gc, s * SB + (quad >> 2), (quad & 3) * 4, cnt);
-        });
-        kst.load(kb, tid, addr, tstep);
-        vst.load(vb, tid, addr, tstep);
+    // ---- staging: K and V rows straight to LDS, one address set for both ----
+    typename C::Ld ld;
+    auto issue_stage = [&](int s, int buf) {
+        ld.compute(halo, g, gc, s * SB, tstep, wave, lane);
+        unsigned char* tile = smem_raw + buf * C::kBufBytes;
+        ld.issue(kb, tile, wave);
+        ld.issue(vb, tile + C::kTileBytes, wave);
     };
-    auto store_stage = [&](int buf) {
-        T* ks = smem + buf * C::kBufElems;
-        kst.store_rows(ks, C::kKRow, tid);
-        vst.store_cols(ks + C::kKElems, C::kVCol, tid);
-    };
+    RowFrag<T, D> kfr;
+    ColFrag<T, D> vfr;
+    kfr.init(lane);
+    vfr.init(lane);
 
     // ---- online-softmax state (per lane: its query column) ----
     // mref: running reference (base 2, -inf until the row sees a key);
@@ -193,14 +185,14 @@ __global__ __launch_bounds__(256) void na_fwd_kernel(Geo g, const T* __restrict_
     }
 
     const int nst = (halo.nb + SB - 1) / SB;
-    load_stage(0);
-    store_stage(0);
+    issue_stage(0, 0);
+    wait_vmem();
     __syncthreads();
 
     for (int s = 0; s < nst; ++s) {
-        if (s + 1 < nst) load_stage(s + 1);
-        const T* ks = smem + (s & 1) * C::kBufElems;
-        const T* vt = ks + C::kKElems;
+        if (s + 1 < nst) issue_stage(s + 1, (s + 1) & 1);
+        const unsigned char* ks = smem_raw + (s & 1) * C::kBufBytes;
+        const unsigned char* vs = ks + C::kTileBytes;
 
         if (wave_live) {
             // lane j < SB tests block s*SB + j of the halo against this wave's
@@ -230,24 +222,22 @@ __global__ __launch_bounds__(256) void na_fwd_kernel(Geo g, const T* __restrict_
                 // ---- S^T = K Q^T for both blocks ----
                 // Both blocks are read and multiplied without a branch: a block
                 // outside this wave's halo is masked below, and every row of
-                // the stage buffer holds finite data (absent rows are zero).
-                // The V fragments of the tile are read here too (D = 32), so
-                // one LDS round trip serves the whole tile.
+                // the stage buffer holds finite data (missing keys are
+                // stand-in rows).  The V fragments of the tile are read here
+                // too (D = 32), so one LDS round trip serves the whole tile.
+                constexpr int kRowB = Rows<T, D>::kRowBytes;
                 x8 kf[2][C::kKS];
 #pragma unroll
                 for (int bi = 0; bi < 2; ++bi)
 #pragma unroll
                     for (int st = 0; st < C::kKS; ++st)
-                        kf[bi][st] = ld_x8<T>(ks + ((tp * 2 + bi) * 16 + col) * C::kKRow +
-                                              st * 32 + grp * 8);
+                        kf[bi][st] = kfr.read(ks + (tp * 2 + bi) * 16 * kRowB, st);
                 constexpr bool kEarlyV = D == 32;
                 x8 vf[C::kDB];
                 auto read_v = [&]() {
 #pragma unroll
-                    for (int db = 0; db < C::kDB; ++db) {
-                        const T* vrow = vt + (db * 16 + col) * C::kVCol + tp * 32 + grp * 4;
-                        vf[db] = cat_x4<T>(ld_x4<T>(vrow), ld_x4<T>(vrow + 16));
-                    }
+                    for (int db = 0; db < C::kDB; ++db)
+                        vf[db] = vfr.read(vs + tp * 32 * kRowB, db, lane);
                 };
                 if (kEarlyV) read_v();
                 f32x4 sacc[QM][2];
@@ -345,7 +335,7 @@ __global__ __launch_bounds__(256) void na_fwd_kernel(Geo g, const T* __restrict_
             }
         }
 
-        if (s + 1 < nst) store_stage((s + 1) & 1);
+        if (s + 1 < nst) wait_vmem();
         __syncthreads();
     }
 

@@ -1,5 +1,6 @@
-// na_stage.h -- global -> register -> LDS staging of token rows, and the
-// halo geometry those rows come from.
+// na_stage.h -- direct global -> LDS staging of token rows, the swizzled LDS
+// row layout the matrix-core fragments are read from, and the halo geometry
+// those rows come from.
 #pragma once
 
 #include "na_common.h"
@@ -8,7 +9,8 @@ namespace na {
 
 // A box of tokens in group coordinates, [lo, lo + E) per axis, cut into rows
 // along the innermost axis and each row into 16-token blocks (rows are padded
-// to a multiple of 16; padding tokens are zero-filled and always masked).
+// to a multiple of 16; padding slots hold a stand-in token and are always
+// masked).
 template <int R>
 struct Box {
     int lo[kMaxRank];
@@ -41,17 +43,17 @@ struct Box {
         if (R >= 2) oc[0] = row;
     }
 
-    // Token (within the (batch, head) slice) of token j0 of block b, and how
-    // many of the tokens j0 .. j0+3 exist (0 for blocks past the end).
-    // Consecutive tokens of a block are g.d[R-1] tokens apart.
-    __device__ __forceinline__ int quad_token(const Geo& g, const int* gc, int b, int j0,
-                                              int& cnt) const {
+    // Token (within the (batch, head) slice) of slot 0 of block b, and how many
+    // slots of the block hold a token of the box (0 for blocks past the end).
+    // Slot j of the block is token + j * g.d[R-1].
+    __device__ __forceinline__ int block_token(const Geo& g, const int* gc, int b,
+                                               int& valid) const {
         int oc[kMaxRank];
         int inner0;
         block_coords(b, oc, inner0);
-        oc[R - 1] = inner0 + j0;
-        const int left = E[R - 1] - oc[R - 1];
-        cnt = b < nb ? (left < 0 ? 0 : (left > 4 ? 4 : left)) : 0;
+        oc[R - 1] = inner0;
+        const int left = E[R - 1] - inner0;
+        valid = b < nb ? (left > 16 ? 16 : left) : 0;
         int tok = 0;
 #pragma unroll
         for (int a = 0; a < R; ++a) tok += (gc[a] + g.d[a] * (lo[a] + oc[a])) * g.ts[a];
@@ -82,150 +84,176 @@ struct WaveRange {
     }
 };
 
-// Stages ROWS token rows of D elements.  Each thread item is 4 consecutive
-// rows (of one 16-row block) x one 16-byte segment, loaded with 16-byte
-// global loads; rows can then be written row-major (dst[row][d]) and/or
-// transposed (dst[d][row]).  Several stagers of the same shape share one
-// set of item addresses (QuadAddr).
-template <int ROWS, int SEGS, int NT>
-struct QuadAddr {
-    static constexpr int kQuads = ROWS / 4;
-    static constexpr int kItems = (kQuads * SEGS + NT - 1) / NT;
-    int tok[kItems];  // token of the item's first row
-    int cnt[kItems];  // rows of the item that exist (0..4)
+// ---------------------------------------------------------------------------
+// LDS rows: D elements of T per token, row-major and unpadded, cut into
+// 16-byte segments; segment s of row r is stored at position s ^ swz(r).
+// The swizzle is linear in the low four row bits and was chosen (by an
+// exhaustive search over such functions) so that both fragment reads below
+// are free of bank conflicts whether the LDS serves 128 or 256 bytes a cycle:
+//   * 16-byte reads of one segment down 16 consecutive rows (MFMA operands
+//     whose contraction runs along D);
+//   * transposed 8-byte reads of 4 consecutive rows x 2 adjacent segments per
+//     16 lanes (operands whose contraction runs along the tokens).
+// ---------------------------------------------------------------------------
+template <typename T, int D>
+struct Rows {
+    static constexpr int kSegs = D * (int)sizeof(T) / 16;  // segments per row
+    static constexpr int kRowBytes = D * (int)sizeof(T);
+    static constexpr int kVec = 16 / (int)sizeof(T);  // elements per segment
+    static_assert(kSegs == 4 || kSegs == 8 || kSegs == 16 || kSegs == 32, "segments per row");
 
-    template <class QuadTok>
-    __device__ __forceinline__ void compute(int tid, QuadTok quad_tok) {
+    __device__ __forceinline__ static int swz(int r) {
+        constexpr int c0 = kSegs == 4 ? 0 : kSegs == 32 ? 1 : 2;
+        constexpr int c1 = kSegs == 4 ? 2 : kSegs == 32 ? 2 : 4;
+        constexpr int c2 = kSegs == 4 ? 3 : kSegs == 8 ? 3 : kSegs == 16 ? 9 : 4;
+        constexpr int c3 = kSegs == 32 ? 8 : 1;
+        return (-(r & 1) & c0) ^ (-((r >> 1) & 1) & c1) ^ (-((r >> 2) & 1) & c2) ^
+               (-((r >> 3) & 1) & c3);
+    }
+    // byte offset of logical segment s of row r
+    __device__ __forceinline__ static int off(int r, int s) {
+        return r * kRowBytes + ((s ^ swz(r)) << 4);
+    }
+};
+
+// Waits until this wave's outstanding vector memory operations (including
+// direct-to-LDS loads) have completed.
+__device__ __forceinline__ void wait_vmem() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+
+typedef __attribute__((address_space(3))) void lds_void;
+
+// Stages ROWS token rows into an LDS tile with 16-byte direct-to-LDS loads
+// (no register round trip): wave instruction t writes the tile's 16-byte
+// positions [64 t, 64 t + 64), i.e. 64 / kSegs rows of one 16-row block, and
+// lane l loads the segment that the swizzle puts at position 64 t + l.
+// Tokens missing from the box are replaced by token 0 of the slice (finite
+// data that the masks exclude).  Several tensors with the same rows share one
+// set of per-lane source offsets.
+template <typename T, int D, int ROWS>
+struct DirectRows {
+    using L = Rows<T, D>;
+    static constexpr int kRowsPerInstr = 64 / L::kSegs;
+    static constexpr int kInstr = ROWS * L::kSegs / 64;  // wave instructions per tensor
+    static constexpr int kPerWave = (kInstr + 3) / 4;
+    static_assert(ROWS % 16 == 0 && kInstr >= 1, "whole blocks per stage");
+    int src[kPerWave];  // element offset (within the slice) of this lane's segment
+
+    // Rows of stage-local blocks b0, b0 + 1, ... of the box; tstep is the token
+    // distance between consecutive slots of a block.
+    template <int R>
+    __device__ __forceinline__ void compute(const Box<R>& box, const Geo& g, const int* gc, int b0,
+                                            int tstep, int wave, int lane) {
 #pragma unroll
-        for (int it = 0; it < kItems; ++it) {
-            const int i = tid + it * NT;
-            cnt[it] = 0;
-            tok[it] = 0;
-            if (i < kQuads * SEGS) {
-                const int quad = i / SEGS;
-                const int t = quad_tok(quad, cnt[it]);
-                tok[it] = cnt[it] > 0 ? t : 0;  // token 0 is a safe dummy address
+        for (int u = 0; u < kPerWave; ++u) {
+            const int t = wave + 4 * u;
+            src[u] = 0;
+            if (t < kInstr) {
+                const int row0 = t * kRowsPerInstr;  // first stage-local row (uniform)
+                int valid;
+                const int tok0 = box.block_token(g, gc, b0 + (row0 >> 4), valid);
+                const int j = (row0 & 15) + lane / L::kSegs;
+                const int seg = (lane % L::kSegs) ^ L::swz(j);
+                const int tok = j < valid ? tok0 + j * tstep : 0;
+                src[u] = tok * D + seg * L::kVec;
             }
+        }
+    }
+
+    __device__ __forceinline__ void issue(const T* base, unsigned char* tile, int wave) const {
+#pragma unroll
+        for (int u = 0; u < kPerWave; ++u) {
+            const int t = wave + 4 * u;
+            if (t < kInstr)
+                __builtin_amdgcn_global_load_lds(static_cast<const void*>(base + src[u]),
+                                                 (lds_void*)(tile + t * 1024), 16, 0, 0);
         }
     }
 };
 
-template <typename T, int D, int ROWS, int NT>
-struct Stager {
-    static constexpr int kVec = Tr<T>::kVec;
-    static constexpr int kSegs = D / kVec;
-    static constexpr int kQuads = ROWS / 4;
-    using Addr = QuadAddr<ROWS, kSegs, NT>;
-    static constexpr int kItems = Addr::kItems;
-    i32x4 r[kItems][4];
-
-    // tstep: token distance between consecutive rows of a quad
-    __device__ __forceinline__ void load(const T* base, int tid, const Addr& ad, int tstep) {
-#pragma unroll
-        for (int it = 0; it < kItems; ++it) {
-            const int i = tid + it * NT;
-            const int seg = i % kSegs;
-            const T* p = base + (size_t)ad.tok[it] * D + seg * kVec;
-            // branch-free: absent rows re-read the first row and are zeroed
-#pragma unroll
-            for (int rr = 0; rr < 4; ++rr) {
-                const bool ok = rr < ad.cnt[it];
-                const i32x4 v = ld16<i32x4>(p + (ok ? (size_t)(rr * tstep) * D : 0));
-                r[it][rr] = ok ? v : i32x4{0, 0, 0, 0};
-            }
-        }
-    }
-
-    __device__ __forceinline__ void store_rows(T* dst, int row_stride, int tid) const {
-#pragma unroll
-        for (int it = 0; it < kItems; ++it) {
-            const int i = tid + it * NT;
-            if (i < kQuads * kSegs) {
-                const int quad = i / kSegs, seg = i - quad * kSegs;
-#pragma unroll
-                for (int rr = 0; rr < 4; ++rr)
-                    st16<i32x4>(dst + (quad * 4 + rr) * row_stride + seg * kVec, r[it][rr]);
-            }
-        }
-    }
-
-    __device__ __forceinline__ void store_cols(T* dst, int col_stride, int tid) const {
-#pragma unroll
-        for (int it = 0; it < kItems; ++it) {
-            const int i = tid + it * NT;
-            if (i < kQuads * kSegs) {
-                const int quad = i / kSegs, seg = i - quad * kSegs;
-                T* d0 = dst + (seg * kVec) * col_stride + quad * 4;
-                if constexpr (sizeof(T) == 2) {
-                    // 4 rows x 8 elements -> 8 lines of 4 rows (16-bit pair transpose)
-#pragma unroll
-                    for (int w = 0; w < 4; ++w) {
-                        const uint32_t a0 = r[it][0][w], a1 = r[it][1][w];
-                        const uint32_t a2 = r[it][2][w], a3 = r[it][3][w];
-                        const i32x2 lo = {(int)((a0 & 0xffffu) | (a1 << 16)),
-                                          (int)((a2 & 0xffffu) | (a3 << 16))};
-                        const i32x2 hi = {(int)((a0 >> 16) | (a1 & 0xffff0000u)),
-                                          (int)((a2 >> 16) | (a3 & 0xffff0000u))};
-                        *reinterpret_cast<i32x2*>(d0 + (2 * w) * col_stride) = lo;
-                        *reinterpret_cast<i32x2*>(d0 + (2 * w + 1) * col_stride) = hi;
-                    }
-                } else {
-#pragma unroll
-                    for (int w = 0; w < 4; ++w) {
-                        const i32x4 t = {r[it][0][w], r[it][1][w], r[it][2][w], r[it][3][w]};
-                        st16<i32x4>(d0 + w * col_stride, t);
-                    }
-                }
-            }
-        }
-    }
-};
-
-// Row-wise dot products of two stagers loaded from the same addresses, in
-// fp32: the kSegs lanes that hold one quad's segments reduce their partial
-// sums with lane shuffles (a fixed order, so the result is deterministic)
-// and the lane of segment 0 writes the quad's 4 sums to dst[4 * quad ...].
-// Absent rows were zero-filled by load() and give 0.
-template <typename T, int D, int ROWS, int NT>
-__device__ __forceinline__ void store_row_dots(const Stager<T, D, ROWS, NT>& a,
-                                               const Stager<T, D, ROWS, NT>& b, float* dst,
-                                               int tid) {
-    using S = Stager<T, D, ROWS, NT>;
-    using x8 = typename Tr<T>::x8;
-    static_assert(kWave % S::kSegs == 0 && NT % S::kSegs == 0, "a quad's segments share a wave");
-#pragma unroll
-    for (int it = 0; it < S::kItems; ++it) {
-        const int i = tid + it * NT;
-        float s[4];
-#pragma unroll
-        for (int rr = 0; rr < 4; ++rr) {
-            if constexpr (sizeof(T) == 2) {
-                s[rr] = dot8<T>(__builtin_bit_cast(x8, a.r[it][rr]),
-                                __builtin_bit_cast(x8, b.r[it][rr]), 0.f);
-            } else {
-                const f32x4 x = __builtin_bit_cast(f32x4, a.r[it][rr]);
-                const f32x4 y = __builtin_bit_cast(f32x4, b.r[it][rr]);
-                s[rr] = fmaf(x[3], y[3], fmaf(x[2], y[2], fmaf(x[1], y[1], x[0] * y[0])));
-            }
-        }
-#pragma unroll
-        for (int w = 1; w < S::kSegs; w <<= 1)
-#pragma unroll
-            for (int rr = 0; rr < 4; ++rr) s[rr] += __shfl_xor(s[rr], w, kWave);
-        if (i < S::kQuads * S::kSegs && i % S::kSegs == 0)
-            st16<f32x4>(dst + (i / S::kSegs) * 4, f32x4{s[0], s[1], s[2], s[3]});
-    }
+// 16-byte and 8-byte LDS reads.
+__device__ __forceinline__ i32x4 lds16(const unsigned char* p) {
+    return *reinterpret_cast<const i32x4*>(p);
 }
 
-// LDS row strides: row-major rows get a 16-byte pad, transposed lines a
-// 4-element pad (keeps 16-byte alignment for fp32 and 8-byte for 16-bit).
+// Operand fragment of 16 rows x 32 contraction slots whose contraction runs
+// along D (MFMA A/B layout: lane l holds row l % 16, slots 8 (l / 16) .. +7
+// = elements st * 32 + 8 (l / 16) .. +7 of its row).  rowoff[] is from
+// frag_offsets(); tile points at the first of the 16 rows.
 template <typename T, int D>
-struct RowLayout {
-    static constexpr int kRow = D + Tr<T>::kVec;
+struct RowFrag {
+    using L = Rows<T, D>;
+    static constexpr int kKS = D / 32;
+    static constexpr int kN = sizeof(T) == 2 ? 1 : 2;  // 16-byte reads per fragment
+    int off[kKS][kN];
+    __device__ __forceinline__ void init(int lane) {
+        const int r = lane & 15, g = lane >> 4;
+#pragma unroll
+        for (int st = 0; st < kKS; ++st)
+#pragma unroll
+            for (int n = 0; n < kN; ++n) off[st][n] = L::off(r, (st * 32 + g * 8) / L::kVec + n);
+    }
+    __device__ __forceinline__ typename Tr<T>::x8 read(const unsigned char* tile, int st) const {
+        using x8 = typename Tr<T>::x8;
+        if constexpr (sizeof(T) == 2) {
+            return __builtin_bit_cast(x8, lds16(tile + off[st][0]));
+        } else {
+            const f32x4 a = __builtin_bit_cast(f32x4, lds16(tile + off[st][0]));
+            const f32x4 b = __builtin_bit_cast(f32x4, lds16(tile + off[st][1]));
+            return x8{a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
+        }
+    }
 };
-template <int ROWS>
-struct ColLayout {
-    static constexpr int kCol = ROWS + 4;
+
+// Transposed operand fragment: 16 columns d = db*16 + (l % 16) of D against
+// 32 token slots, slot j of lane l holding token row
+//   4 (l / 16) + j          (j < 4)   and   16 + 4 (l / 16) + j - 4   (j >= 4)
+// of a 32-row tile -- the token order of a result tile of two 16-token
+// blocks (result lane l holds rows 4 (l / 16) .. +3 of each block), so a
+// probability or gradient tile feeds the next product without a shuffle.
+// 16-bit types use the gfx950 transposed LDS read (each 16-lane group
+// gathers 4 rows x 16 columns); fp32 reads the eight values one by one.
+template <typename T, int D>
+struct ColFrag {
+    using L = Rows<T, D>;
+    static constexpr int kDB = D / 16;
+    int off[kDB];
+    __device__ __forceinline__ void init(int lane) {
+        const int g = lane >> 4, i = lane & 15;
+        if constexpr (sizeof(T) == 2) {
+            // lane 16g + 4s + q supplies row 4g + s, columns db*16 + 4q .. +3
+            const int r = 4 * g + (i >> 2), q = i & 3;
+#pragma unroll
+            for (int db = 0; db < kDB; ++db)
+                off[db] = L::off(r, (db * 16 + 4 * q) / L::kVec) + (q & 1) * 8;
+        } else {
+#pragma unroll
+            for (int db = 0; db < kDB; ++db) off[db] = 0;
+        }
+    }
+    __device__ __forceinline__ typename Tr<T>::x8 read(const unsigned char* tile, int db,
+                                                       int lane) const {
+        using x8 = typename Tr<T>::x8;
+        if constexpr (sizeof(T) == 2) {
+            typedef short s16x4 __attribute__((ext_vector_type(4)));
+            typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
+            const i32x2 a = __builtin_bit_cast(
+                i32x2, __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(tile + off[db])));
+            const i32x2 b = __builtin_bit_cast(
+                i32x2, __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                           (lds_s16x4*)(tile + 16 * L::kRowBytes + off[db])));
+            return __builtin_bit_cast(x8, i32x4{a[0], a[1], b[0], b[1]});
+        } else {
+            const int g = lane >> 4, d = db * 16 + (lane & 15);
+            x8 v;
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                const int r = (j < 4 ? 0 : 16) + 4 * g + (j & 3);
+                v[j] = *reinterpret_cast<const float*>(tile + L::off(r, d / L::kVec) +
+                                                       (d % L::kVec) * 4);
+            }
+            return v;
+        }
+    }
 };
 
 }  // namespace na
