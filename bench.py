@@ -23,7 +23,7 @@ import torch  # noqa: E402
 
 import workloads  # noqa: E402
 
-WORKLOAD = "2d_fp16_56x56_k7"
+WORKLOAD = workloads.BENCH_WORKLOAD
 PEAK_FP16_TFLOPS = 2516.6   # MI355X dense fp16 MFMA
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
 PMC_FILE = os.path.join(ROOT, "profiles", "na_fwd_kernel.2d_fp16_56x56_k7.pmc.txt")

@@ -33,7 +33,6 @@ struct DqCfg {
     static constexpr int kKeys = SB * 16;
     static constexpr int kTileBytes = kKeys * Rows<T, D>::kRowBytes;
     static constexpr size_t kBufBytes = 2 * kTileBytes;  // K rows, then V rows
-    static constexpr size_t kLdsBytes = 2 * kBufBytes;
     static constexpr int kKS = D / 32;
     static constexpr int kDB = D / 16;
     using Ld = DirectRows<T, D, kKeys>;
@@ -295,7 +294,6 @@ struct DkvCfg {
     static constexpr int kTileBytes = kRows * Rows<T, D>::kRowBytes;
     // Q rows, dO rows, O rows, then fp32 lse (base 2) and Delta per query
     static constexpr size_t kBufBytes = 3 * kTileBytes + 2 * kRows * sizeof(float);
-    static constexpr size_t kLdsBytes = 2 * kBufBytes;
     static constexpr int kKS = D / 32;
     static constexpr int kDB = D / 16;
     using Ld = DirectRows<T, D, kRows>;
@@ -667,24 +665,52 @@ __global__ __launch_bounds__(256, (bwd_min_waves<D, T>())) void na_bwd_kernel(Ge
 // ---------------------------------------------------------------------------
 // host-side launch
 // ---------------------------------------------------------------------------
-template <int R, int D, typename T, int QM, int KM>
-static hipError_t launch_bwd_inst(const Geo& g, const void* q, const void* k, const void* v,
-                                  const void* o, const float* lse, const void* dout, void* dq,
-                                  void* dk, void* dv, float scale, hipStream_t stream) {
-    constexpr int SBQ = sizeof(T) == 4 ? 2 : 4;
-    constexpr int SBK = (sizeof(T) == 4 || D == 128) ? 2 : 4;
-    // rows of the halo (dQ) and of the query box (dK/dV) hold at most 2
-    // blocks: interior extent min(T, n) + k - 1 along the innermost axis
-    bool short_rows = false;
-    if (R > 1) {
-        const int a = R - 1;
-        const int n0 = group_len(g.L[a], g.d[a], 0);
-        short_rows = (std::min(std::min(g.T[a], n0) + g.k[a] - 1, n0) + 15) / 16 <= 2;
+// Longest extent along one axis, over every tile and both group lengths of a
+// dilated axis, of a workgroup's key halo (inverse = false) or of the box of
+// queries attending to its key tile (inverse = true).  Window starts grow by
+// at most one per position, so a halo never exceeds min(T, n) + k - 1; an
+// inverse box can (every key within k - 1 of the start is attended by query
+// 0), so the tiles near a border are evaluated one by one and a single
+// interior tile (extent T + k - 1) stands for the rest.
+static int max_box_extent(int L, int d, int k, int T, bool inverse) {
+    int best = 0;
+    const int n0 = group_len(L, d, 0);
+    for (int n = n0; n >= n0 - 1; --n) {
+        if (n < n0 && L % d == 0) break;  // every group has length n0
+        if (!inverse) {
+            best = std::max(best, std::min(std::min(T, n) + k - 1, n));
+            continue;
+        }
+        const int nt = (n + T - 1) / T;
+        const int edge = k / T + 2;  // tiles that can reach within k of a border
+        for (int i = 0; i < nt; ++i) {
+            if (i > edge && i < nt - edge) continue;
+            const int to = i * T, last = std::min(to + T, n) - 1;
+            best = std::max(best, inv_hi(last, n, k) + 1 - inv_lo(to, n, k));
+        }
     }
+    return best;
+}
+
+// 16-token blocks of the largest box with per-axis extents e[]: rows along
+// the innermost axis are cut into blocks.
+static int box_blocks(const int* e, int rank) {
+    int nb = (e[rank - 1] + 15) / 16;
+    for (int a = 0; a < rank - 1; ++a) nb *= e[a];
+    return nb;
+}
+
+// hq / hk: most blocks in any dQ halo / dK-dV query box; a role whose boxes
+// all fit in one stage gets a single LDS buffer.
+template <int R, int D, typename T, int QM, int KM, int SBQ, int SBK>
+static hipError_t launch_bwd_sb(const Geo& g, bool short_rows, int hq, int hk, const void* q,
+                                const void* k, const void* v, const void* o, const float* lse,
+                                const void* dout, void* dq, void* dk, void* dv, float scale,
+                                hipStream_t stream) {
     auto kern = short_rows ? na_bwd_kernel<R, D, T, QM, KM, SBQ, SBK, 1>
                            : na_bwd_kernel<R, D, T, QM, KM, SBQ, SBK, 0>;
-    const size_t lds = std::max(DqCfg<R, D, T, QM, SBQ>::kLdsBytes,
-                                DkvCfg<R, D, T, KM, SBK>::kLdsBytes);
+    const size_t lds = std::max((hq > SBQ ? 2 : 1) * DqCfg<R, D, T, QM, SBQ>::kBufBytes,
+                                (hk > SBK ? 2 : 1) * DkvCfg<R, D, T, KM, SBK>::kBufBytes);
     if (lds > 65536) {
         hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
@@ -697,6 +723,30 @@ static hipError_t launch_bwd_inst(const Geo& g, const void* q, const void* k, co
                        static_cast<const T*>(dout), lse, static_cast<T*>(dq), static_cast<T*>(dk),
                        static_cast<T*>(dv), scale * kLog2e, scale);
     return hipGetLastError();
+}
+
+template <int R, int D, typename T, int QM, int KM>
+static hipError_t launch_bwd_inst(const Geo& g, const void* q, const void* k, const void* v,
+                                  const void* o, const float* lse, const void* dout, void* dq,
+                                  void* dk, void* dv, float scale, hipStream_t stream) {
+    int eq[kMaxRank], ek[kMaxRank];
+    for (int a = 0; a < R; ++a) {
+        eq[a] = max_box_extent(g.L[a], g.d[a], g.k[a], g.T[a], false);
+        ek[a] = max_box_extent(g.L[a], g.d[a], g.k[a], g.T[a], true);
+    }
+    const int hq = box_blocks(eq, R), hk = box_blocks(ek, R);
+    // rows of every halo (dQ) and query box (dK/dV) hold at most 2 blocks
+    const bool short_rows = R > 1 && (eq[R - 1] + 15) / 16 <= 2 && (ek[R - 1] + 15) / 16 <= 2;
+    // D = 32, 16-bit: boxes of up to 16 blocks are staged whole (one stage)
+    if constexpr (sizeof(T) == 2 && D == 32) {
+        if (hq <= 16 && hk <= 16)
+            return launch_bwd_sb<R, D, T, QM, KM, 16, 16>(g, short_rows, hq, hk, q, k, v, o, lse,
+                                                          dout, dq, dk, dv, scale, stream);
+    }
+    constexpr int SBQ = sizeof(T) == 4 ? 2 : 4;
+    constexpr int SBK = (sizeof(T) == 4 || D == 128) ? 2 : 4;
+    return launch_bwd_sb<R, D, T, QM, KM, SBQ, SBK>(g, short_rows, hq, hk, q, k, v, o, lse, dout,
+                                                    dq, dk, dv, scale, stream);
 }
 
 template <int R, int D, typename T>

@@ -166,6 +166,12 @@ BWD_CASES = [
     ((6, 20, 22), (3, 7, 5), (1, 2, 2), 64, "fp16", 1, 1),
     ((5, 9, 11), (5, 3, 3), (1, 3, 3), 32, "fp32", 1, 2),
     ((8, 12, 12), (7, 7, 7), (1, 1, 1), 128, "bf16", 1, 1),
+    # query boxes of border key tiles wider than the interior T + k - 1
+    # (keys within k - 1 of the start are attended from query 0): 3 blocks
+    # per row where the interior needs 2
+    ((5, 40), (3, 17), (1, 1), 32, "fp16", 1, 1),
+    ((3, 4, 64), (3, 3, 25), (1, 1, 1), 32, "bf16", 1, 1),
+    ((4, 81), (3, 9), (1, 2), 64, "fp16", 1, 1),
 ]
 
 
@@ -242,7 +248,8 @@ def test_full_workload_forward(na, name):
     assert eo <= TOL[p.dtype] and el <= TOL[p.dtype]
 
 
-@pytest.mark.parametrize("name", [n for n in workloads.CONFIG_ORDER if workloads.CONFIGS[n].backward])
+@pytest.mark.parametrize("name", [n for n in workloads.CONFIG_ORDER
+                                  if workloads.CONFIGS[n].backward or n == workloads.BENCH_WORKLOAD])
 def test_full_workload_backward(na, name):
     p = workloads.CONFIGS[name]
     _log(f"[full bwd] {p.describe()}")

@@ -95,6 +95,8 @@ CONFIGS = {
                                         (7, 7, 7), (1, 2, 2), "fp16", backward=True),
 }
 CONFIG_ORDER = list(CONFIGS)
+# The workload the benchmark times (forward and backward): 2-D 7x7 fp16.
+BENCH_WORKLOAD = "2d_fp16_56x56_k7"
 
 TORCH_DTYPE = {"fp32": torch.float32, "fp16": torch.float16, "bf16": torch.bfloat16}
 
