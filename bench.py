@@ -85,7 +85,9 @@ def main():
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
-    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-cpu-baseline", action="store_true",
+                    help="skip the CPU oracle baseline and the MFMA-bound side measurement "
+                         "(profiling runs)")
     ap.add_argument("--workload", default=WORKLOAD, choices=workloads.CONFIG_ORDER,
                     help="profiling aid: run the same step on another workload (the reported "
                          "line is defined on the default one)")
@@ -218,8 +220,40 @@ def main():
         },
     }
     if not args.no_cpu_baseline:
+        if p.name == workloads.BENCH_WORKLOAD:
+            result["mfma_bound"] = mfma_bound_forward(na, dev, head_start, host_step_s)
         result["cpu_baseline"] = cpu_baseline(p, x, args.cpu_seconds)
     print(json.dumps(result), flush=True)
+
+
+# The workload whose arithmetic intensity (about 507 FLOP/B) is above the fp16
+# ridge point, so the forward's fraction of MFMA peak is meaningful there; the
+# 2-D 7x7 workload is HBM- and latency-bound by its shape.
+MFMA_BOUND_WORKLOAD = "1d_fp16_L32768_k1023_d4"
+
+
+def mfma_bound_forward(na, dev, head_start, host_step_s, launches=100):
+    """Back-to-back forward launches on the MFMA-bound workload (side measurement)."""
+    p = workloads.CONFIGS[MFMA_BOUND_WORKLOAD]
+    x = workloads.make_inputs(p, seed=0, with_grad=False)
+    q, k, v = (x[n].to(dev) for n in ("q", "k", "v"))
+    out = torch.empty_like(q)
+    lse = torch.empty(q.shape[:-1], dtype=torch.float32, device=dev)
+    args = (p.kernel_size, p.dilation, p.softmax_scale)
+    for _ in range(10):
+        na.forward(q, k, v, *args, out=out, lse=lse)
+    torch.cuda.synchronize()
+    f0, f1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    head_start(host_step_s)
+    f0.record()
+    for _ in range(launches):
+        na.forward(q, k, v, *args, out=out, lse=lse)
+    f1.record()
+    torch.cuda.synchronize()
+    ms = f0.elapsed_time(f1) / launches
+    tflops = p.fwd_flops() / (ms * 1e-3) / 1e12
+    return {"workload": p.name, "launches": launches, "fwd_ms": round(ms, 5),
+            "tflops": round(tflops, 2), "mfma_peak_frac": round(tflops / PEAK_FP16_TFLOPS, 4)}
 
 
 if __name__ == "__main__":
