@@ -24,7 +24,13 @@
 //   * scores are scaled once into base 2 (so the row maximum maps to exactly
 //     exp2(0) = 1 and a window of one key returns V bit for bit); the running
 //     maximum is only raised (and O rescaled) when a row's maximum grows by
-//     more than kLazy, which keeps every P <= 2^kLazy.
+//     more than kLazy, which keeps every P <= 2^kLazy.  Each lane tests its
+//     own share of a row against the threshold; the cross-lane row maximum is
+//     formed only in the (rare) raising branch;
+//   * with one query block per wave, 16-bit types sum each row of the rounded
+//     P on the matrix cores: one more MFMA with an all-ones V^T block leaves
+//     the full row sum in every lane (with two blocks the extra accumulators
+//     would cost a wave of occupancy, so those sum with v_dot2).
 #include <algorithm>
 #include <cmath>
 
@@ -150,13 +156,21 @@ __global__ __launch_bounds__(256) void na_fwd_kernel(Geo g, const T* __restrict_
     // mref: running reference (base 2, -inf until the row sees a key);
     // negm = -mref (0 while mref = -inf) is the scores' FMA addend and thr the
     // score above which the reference must be raised.
-    f32x4 oacc[QM][C::kDB];
+    // Row sums: with kMfmaSum, lsum[m] accumulates ones^T P^T on the matrix
+    // cores (every entry is the row sum); otherwise each lane sums its share
+    // of P in lrow[m], reduced across the four lane groups at the end.
+    constexpr bool kMfmaSum = sizeof(T) == 2 && QM == 1;
+    x8 ones;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) ones[j] = (T)1.0f;
+    f32x4 oacc[QM][C::kDB], lsum[QM];
     float mref[QM], negm[QM], thr[QM], lrow[QM];
 #pragma unroll
     for (int m = 0; m < QM; ++m) {
         mref[m] = -INFINITY;
         negm[m] = 0.f;
         thr[m] = -INFINITY;
+        lsum[m] = f32x4{0.f, 0.f, 0.f, 0.f};
         lrow[m] = 0.f;
 #pragma unroll
         for (int db = 0; db < C::kDB; ++db) oacc[m][db] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -284,22 +298,26 @@ __global__ __launch_bounds__(256) void na_fwd_kernel(Geo g, const T* __restrict_
                             for (int a = 0; a < R - 1; ++a)
                                 outer_ok = outer_ok &&
                                            (unsigned)(boc[bi][a] - qs[m][a]) < (unsigned)g.k[a];
-                            const int base = bin0[bi] + grp * 4 - qs[m][R - 1];
+                            // slot r is valid when base + r lies in [0, lim): lim folds the
+                            // outer axes in (0 fails every slot) and a full block admits all
+                            const int base = full[bi] ? 0 : bin0[bi] + grp * 4 - qs[m][R - 1];
+                            const unsigned lim = full[bi] ? 4u : outer_ok ? (unsigned)g.k[R - 1] : 0u;
 #pragma unroll
-                            for (int r = 0; r < 4; ++r) {
-                                const bool ok = full[bi] || (outer_ok && (unsigned)(base + r) <
-                                                                             (unsigned)g.k[R - 1]);
-                                y[bi][r] = fmaf(sacc[m][bi][r], c, ok ? negm[m] : -INFINITY);
-                            }
+                            for (int r = 0; r < 4; ++r)
+                                y[bi][r] = fmaf(sacc[m][bi][r], c,
+                                                (unsigned)(base + r) < lim ? negm[m] : -INFINITY);
                         }
                     }
-                    float ymax = fmaxf(fmaxf(fmaxf(y[0][0], y[0][1]), fmaxf(y[0][2], y[0][3])),
-                                       fmaxf(fmaxf(y[1][0], y[1][1]), fmaxf(y[1][2], y[1][3])));
-                    ymax = group_max4(ymax);
+                    // this lane's share of the row; the row maximum exceeds the
+                    // threshold exactly when some lane's share does
+                    const float lmax =
+                        fmaxf(fmaxf(fmaxf(y[0][0], y[0][1]), fmaxf(y[0][2], y[0][3])),
+                              fmaxf(fmaxf(y[1][0], y[1][1]), fmaxf(y[1][2], y[1][3])));
                     // raise the reference on the first valid key of a row, or when
                     // the row grows by more than kLazy (rare, wave-uniform branch)
-                    const bool raise = ymax > thr[m];
-                    if (__builtin_amdgcn_ballot_w64(raise)) {
+                    if (__builtin_amdgcn_ballot_w64(lmax > thr[m])) {
+                        const float ymax = group_max4(lmax);
+                        const bool raise = ymax > thr[m];
                         const float dlt = raise ? ymax : 0.f;
                         const float alpha = fast_exp2(-dlt);
                         mref[m] = raise ? dlt - negm[m] : mref[m];
@@ -307,7 +325,10 @@ __global__ __launch_bounds__(256) void na_fwd_kernel(Geo g, const T* __restrict_
                         negm[m] = seen ? -mref[m] : 0.f;
                         thr[m] = seen ? kLazy : -INFINITY;
                         if (R > 1) refresh_addends(m);
-                        lrow[m] *= alpha;
+                        if constexpr (kMfmaSum)
+                            lsum[m] *= alpha;
+                        else
+                            lrow[m] *= alpha;
 #pragma unroll
                         for (int db = 0; db < C::kDB; ++db) oacc[m][db] *= alpha;
 #pragma unroll
@@ -323,15 +344,19 @@ __global__ __launch_bounds__(256) void na_fwd_kernel(Geo g, const T* __restrict_
                     pf[m] = x8{Tr<T>::cvt(p[0][0]), Tr<T>::cvt(p[0][1]), Tr<T>::cvt(p[0][2]),
                                Tr<T>::cvt(p[0][3]), Tr<T>::cvt(p[1][0]), Tr<T>::cvt(p[1][1]),
                                Tr<T>::cvt(p[1][2]), Tr<T>::cvt(p[1][3])};
-                    lrow[m] = row_sum8<T>(pf[m], p, lrow[m]);
+                    if constexpr (!kMfmaSum) lrow[m] = row_sum8<T>(pf[m], p, lrow[m]);
                 }
 
-                // ---- O^T += V^T P^T ----
+                // ---- O^T += V^T P^T (and the row sums, ones^T P^T) ----
                 if (!kEarlyV) read_v();
 #pragma unroll
                 for (int db = 0; db < C::kDB; ++db)
 #pragma unroll
                     for (int m = 0; m < QM; ++m) oacc[m][db] = Tr<T>::mma(vf[db], pf[m], oacc[m][db]);
+                if constexpr (kMfmaSum) {
+#pragma unroll
+                    for (int m = 0; m < QM; ++m) lsum[m] = Tr<T>::mma(ones, pf[m], lsum[m]);
+                }
             }
         }
 
@@ -342,7 +367,7 @@ __global__ __launch_bounds__(256) void na_fwd_kernel(Geo g, const T* __restrict_
     // ---- epilogue: normalise, store O (rounded once) and the natural-log LSE ----
 #pragma unroll
     for (int m = 0; m < QM; ++m) {
-        const float l = group_sum4(lrow[m]);
+        const float l = kMfmaSum ? lsum[m][0] : group_sum4(lrow[m]);
         if (!qvalid[m]) continue;
         const float inv = 1.f / l;
 #pragma unroll
