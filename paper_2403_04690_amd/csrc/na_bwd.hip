@@ -202,7 +202,8 @@ __device__ __forceinline__ void dq_role(const Geo& g, int braw, unsigned char* s
                     for (int a = 0; a < R - 1; ++a) boc[bi][a] = __builtin_amdgcn_readlane(loc[a], j);
                 }
 
-                // S^T = K Q^T and dP^T = V dO^T
+                // S^T = K Q^T and dP^T - Delta = V dO^T - Delta (the accumulator
+                // starts at -Delta of the lane's query)
                 f32x4 sacc[QM][2], pacc[QM][2];
 #pragma unroll
                 for (int bi = 0; bi < 2; ++bi) {
@@ -215,8 +216,9 @@ __device__ __forceinline__ void dq_role(const Geo& g, int braw, unsigned char* s
 #pragma unroll
                             for (int m = 0; m < QM; ++m) {
                                 const f32x4 z = f32x4{0.f, 0.f, 0.f, 0.f};
+                                const f32x4 nd = f32x4{-dlt[m], -dlt[m], -dlt[m], -dlt[m]};
                                 sacc[m][bi] = Tr<T>::mma(kf, qf[m][st], st == 0 ? z : sacc[m][bi]);
-                                pacc[m][bi] = Tr<T>::mma(vf, gf[m][st], st == 0 ? z : pacc[m][bi]);
+                                pacc[m][bi] = Tr<T>::mma(vf, gf[m][st], st == 0 ? nd : pacc[m][bi]);
                             }
                         }
                     } else {
@@ -239,21 +241,18 @@ __device__ __forceinline__ void dq_role(const Geo& g, int braw, unsigned char* s
 #pragma unroll
                         for (int a = 0; a < R - 1; ++a)
                             outer_ok = outer_ok && (unsigned)(boc[bi][a] - qs[m][a]) < (unsigned)g.k[a];
-                        const int base = bin0[bi] + grp * 4 - qs[m][R - 1];
+                        // generic rows: slot r is valid when base + r lies in [0, lim)
+                        const int base = full[bi] ? 0 : bin0[bi] + grp * 4 - qs[m][R - 1];
+                        const unsigned lim = full[bi] ? 4u : outer_ok ? (unsigned)g.k[R - 1] : 0u;
 #pragma unroll
                         for (int r = 0; r < 4; ++r) {
                             float add;
-                            if (!short_rows && full[bi]) {
-                                add = -lse2[m];
-                            } else if (short_rows) {
+                            if (short_rows)
                                 add = outer_ok ? ain[m][bi][r] : -INFINITY;
-                            } else {
-                                const bool ok =
-                                    outer_ok && (unsigned)(base + r) < (unsigned)g.k[R - 1];
-                                add = ok ? -lse2[m] : -INFINITY;
-                            }
+                            else
+                                add = (unsigned)(base + r) < lim ? -lse2[m] : -INFINITY;
                             const float p = fast_exp2(fmaf(sacc[m][bi][r], scale_log2, add));
-                            ds[bi][r] = p * (pacc[m][bi][r] - dlt[m]);
+                            ds[bi][r] = p * pacc[m][bi][r];
                         }
                     }
                     dsf[m] = x8{Tr<T>::cvt(ds[0][0]), Tr<T>::cvt(ds[0][1]), Tr<T>::cvt(ds[0][2]),
@@ -430,14 +429,15 @@ __device__ __forceinline__ void dkdv_role(const Geo& g, int braw, int nwk,
             const int tok0 = ibox.block_token(g, gc, s * SB + (tid >> 4), valid);
             const bool ok = (tid & 15) < valid;
             const float lv = lb[ok ? tok0 + (tid & 15) * tstep : 0];  // token 0: safe stand-in
-            lse_reg = ok ? lv * kLog2e : 0.f;
+            lse_reg = ok ? -lv * kLog2e : 0.f;  // staged negated: -lse2
         }
     };
     auto floats = [&](int buf) {
         return reinterpret_cast<float*>(smem_raw + buf * C::kBufBytes + 3 * C::kTileBytes);
     };
     // Delta = dO . O of the stage's staged queries, from their LDS rows
-    // (kThreads / kRows lanes per query, reduced with lane shuffles)
+    // (kThreads / kRows lanes per query, reduced with lane shuffles); the
+    // float area holds -lse2 and -Delta per staged query
     auto delta_pass = [&](int buf) {
         using L = Rows<T, D>;
         constexpr int kP = C::kThreads / C::kRows;
@@ -463,7 +463,7 @@ __device__ __forceinline__ void dkdv_role(const Geo& g, int braw, int nwk,
         }
 #pragma unroll
         for (int w = 1; w < kP; w <<= 1) acc += __shfl_xor(acc, w, kWave);
-        if (part == 0) floats(buf)[C::kRows + row] = acc;
+        if (part == 0) floats(buf)[C::kRows + row] = -acc;  // staged negated: -Delta
     };
     RowFrag<T, D> rfr;
     ColFrag<T, D> cfr;
@@ -519,7 +519,17 @@ __device__ __forceinline__ void dkdv_role(const Geo& g, int braw, int nwk,
                     for (int a = 0; a < R - 1; ++a) boc[bi][a] = __builtin_amdgcn_readlane(loc[a], j);
                 }
 
-                // S = Q K^T and dP = dO V^T (rows: queries, columns: this wave's keys)
+                // -lse2 and -Delta of the 2 x 4 queries this lane holds
+                f32x4 nlse[2], ndl[2];
+#pragma unroll
+                for (int bi = 0; bi < 2; ++bi) {
+                    const int srow = (tp * 2 + bi) * 16 + grp * 4;
+                    nlse[bi] = ld16<f32x4>(ls + srow);
+                    ndl[bi] = ld16<f32x4>(dls + srow);
+                }
+
+                // S = Q K^T and dP - Delta = dO V^T - Delta (rows: queries,
+                // columns: this wave's keys; the accumulator starts at -Delta)
                 f32x4 sacc[KM][2], pacc[KM][2];
 #pragma unroll
                 for (int bi = 0; bi < 2; ++bi) {
@@ -533,7 +543,7 @@ __device__ __forceinline__ void dkdv_role(const Geo& g, int braw, int nwk,
                             for (int m = 0; m < KM; ++m) {
                                 const f32x4 z = f32x4{0.f, 0.f, 0.f, 0.f};
                                 sacc[m][bi] = Tr<T>::mma(qa, kf[m][st], st == 0 ? z : sacc[m][bi]);
-                                pacc[m][bi] = Tr<T>::mma(ga, vf[m][st], st == 0 ? z : pacc[m][bi]);
+                                pacc[m][bi] = Tr<T>::mma(ga, vf[m][st], st == 0 ? ndl[bi] : pacc[m][bi]);
                             }
                         }
                     } else {
@@ -542,19 +552,6 @@ __device__ __forceinline__ void dkdv_role(const Geo& g, int braw, int nwk,
                             sacc[m][bi] = f32x4{0.f, 0.f, 0.f, 0.f};
                             pacc[m][bi] = f32x4{0.f, 0.f, 0.f, 0.f};
                         }
-                    }
-                }
-
-                // -LSE and Delta of the 2 x 4 queries this lane holds
-                float nlse[2][4], dlv[2][4];
-#pragma unroll
-                for (int bi = 0; bi < 2; ++bi) {
-                    const int srow = (tp * 2 + bi) * 16 + grp * 4;
-                    const f32x4 lv = ld16<f32x4>(ls + srow), dv4 = ld16<f32x4>(dls + srow);
-#pragma unroll
-                    for (int r = 0; r < 4; ++r) {
-                        nlse[bi][r] = -lv[r];
-                        dlv[bi][r] = dv4[r];
                     }
                 }
 
@@ -570,22 +567,20 @@ __device__ __forceinline__ void dkdv_role(const Geo& g, int braw, int nwk,
                         for (int a = 0; a < R - 1; ++a)
                             outer_ok = outer_ok &&
                                        (unsigned)(boc[bi][a] - ilo[m][a]) <= (unsigned)ispan[m][a];
-                        const int base = bin0[bi] + grp * 4 - ilo[m][R - 1];
+                        // generic rows: slot r is valid when base + r lies in [0, lim)
+                        const int base = full[bi] ? 0 : bin0[bi] + grp * 4 - ilo[m][R - 1];
+                        const unsigned lim =
+                            full[bi] ? 4u : outer_ok ? (unsigned)ispan[m][R - 1] + 1u : 0u;
 #pragma unroll
                         for (int r = 0; r < 4; ++r) {
                             float add;
-                            if (!short_rows && full[bi]) {
-                                add = nlse[bi][r];
-                            } else if (short_rows) {
+                            if (short_rows)
                                 add = outer_ok ? nlse[bi][r] + ain[m][bi][r] : -INFINITY;
-                            } else {
-                                const bool ok =
-                                    outer_ok && (unsigned)(base + r) <= (unsigned)ispan[m][R - 1];
-                                add = ok ? nlse[bi][r] : -INFINITY;
-                            }
+                            else
+                                add = (unsigned)(base + r) < lim ? nlse[bi][r] : -INFINITY;
                             const float pv = fast_exp2(fmaf(sacc[m][bi][r], scale_log2, add));
                             p[bi][r] = pv;
-                            ds[bi][r] = pv * (pacc[m][bi][r] - dlv[bi][r]);
+                            ds[bi][r] = pv * pacc[m][bi][r];
                         }
                     }
                     pf[m] = x8{Tr<T>::cvt(p[0][0]), Tr<T>::cvt(p[0][1]), Tr<T>::cvt(p[0][2]),
