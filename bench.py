@@ -1,11 +1,12 @@
 """Benchmark: fused NA on the 2-D 7x7 fp16 workload (B=4, H=4, 56x56, D=32), one GPU.
 
 A timed step is one pass of the fused path on that workload: na_forward then
-na_backward (Delta pre-pass, dK/dV, dQ), inputs resident in HBM; ms_per_step
-is the whole forward+backward step.  The reported value is the forward's
-useful throughput, 4*B*H*N*ell*D FLOPs (masked halo work is not credited)
-divided by the forward kernel's average duration, measured with HIP events on
-the launch stream over K back-to-back forward launches.
+na_backward (one launch: dK/dV and dQ workgroup roles, Delta in-kernel), inputs
+resident in HBM; ms_per_step is the whole forward+backward step.  Three timed
+regions, each K back-to-back calls with HIP events on the launch stream at its
+two ends only: steps, forwards alone (fwd_ms), backwards alone (bwd_ms).  The
+reported value is the forward's useful throughput, 4*B*H*N*ell*D FLOPs (masked
+halo work is not credited) divided by fwd_ms.
 
 Prints one JSON line.  --gpus above 1 is refused: this build runs on one GPU.
 """
@@ -121,15 +122,15 @@ def main():
     dq, dk, dv = torch.empty_like(q), torch.empty_like(k), torch.empty_like(v)
     ks, ds, sc = p.kernel_size, p.dilation, p.softmax_scale
 
-    def step(e0=None, e1=None, e2=None):
-        if e0 is not None:
-            e0.record()
+    def fwd():
         na.forward(q, k, v, ks, ds, sc, out=out, lse=lse)
-        if e1 is not None:
-            e1.record()
+
+    def bwd():
         na.backward(q, k, v, out, lse, g, ks, ds, sc, dq=dq, dk=dk, dv=dv)
-        if e2 is not None:
-            e2.record()
+
+    def step():
+        fwd()
+        bwd()
 
     for _ in range(args.warmup):
         step()
@@ -150,34 +151,34 @@ def main():
 
     K = args.steps
     torch.cuda.synchronize()
-    # Head start: a GPU-side spin long enough for the host to enqueue all K
-    # steps, so the GPU then runs them back to back (the spin is outside the
-    # events that time the steps).
+
+    def timed(fn):
+        """ms per call of fn over K back-to-back calls, HIP events at the two ends only.
+
+        A GPU-side spin long enough for the host to enqueue all K calls runs
+        first (outside the events), so the GPU then executes them back to back.
+        """
+        head_s = min(2.0 * K * host_step_s + 1e-3, 5.0)
+        torch.cuda._sleep(int(head_s / max(spin_s_per_cycle, 1e-12)))
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(K):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / K
+
+    # Timed region 1: K forward + backward steps (the whole path).
+    step_ms = timed(step)
+    # Timed region 2: K forward launches (the forward kernel's steady-state
+    # duration, which the metric and the roofline use).
+    fwd_ms = timed(fwd)
+    # Timed region 3: K backward launches.
+    bwd_ms = timed(bwd)
+
     def head_start(per_item_s):
         head_s = min(2.0 * K * per_item_s + 1e-3, 5.0)
         torch.cuda._sleep(int(head_s / max(spin_s_per_cycle, 1e-12)))
-
-    # Timed region 1: K forward + backward steps (the whole path).
-    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(K)]
-    ev_end = torch.cuda.Event(enable_timing=True)
-    head_start(host_step_s)
-    for i in range(K):
-        step(*ev[i])
-    ev_end.record()
-    torch.cuda.synchronize()
-    bwd_ms = sum(ev[i][1].elapsed_time(ev[i][2]) for i in range(K)) / K
-    step_ms = ev[0][0].elapsed_time(ev_end) / K
-
-    # Timed region 2: K forward launches back to back (the forward kernel's
-    # steady-state duration, which the metric and the roofline use).
-    f0, f1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    head_start(host_step_s)
-    f0.record()
-    for i in range(K):
-        na.forward(q, k, v, ks, ds, sc, out=out, lse=lse)
-    f1.record()
-    torch.cuda.synchronize()
-    fwd_ms = f0.elapsed_time(f1) / K
 
     fwd_tflops = p.fwd_flops() / (fwd_ms * 1e-3) / 1e12
     fwd_bytes = p.fwd_bytes()
