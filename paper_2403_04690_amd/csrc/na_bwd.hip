@@ -291,8 +291,14 @@ struct DkvCfg {
     static constexpr int kThreads = 4 * kWave;
     static constexpr int kRows = SB * 16;  // queries per stage
     static constexpr int kTileBytes = kRows * Rows<T, D>::kRowBytes;
-    // Q rows, dO rows, O rows, then fp32 lse (base 2) and Delta per query
-    static constexpr size_t kBufBytes = 3 * kTileBytes + 2 * kRows * sizeof(float);
+    // One staged query per thread (the whole box in one stage): each thread
+    // forms Delta of its query from its O row in registers, and no O tile is
+    // staged.  Otherwise O rows are staged beside Q and dO.
+    static constexpr bool kRegDelta = kRows == kThreads;
+    static constexpr int kTiles = kRegDelta ? 2 : 3;
+    // Q rows, dO rows, [O rows,] then fp32 -lse2 and -Delta per query
+    static constexpr size_t kFloatOff = (size_t)kTiles * kTileBytes;
+    static constexpr size_t kBufBytes = kFloatOff + 2 * kRows * sizeof(float);
     static constexpr int kKS = D / 32;
     static constexpr int kDB = D / 16;
     using Ld = DirectRows<T, D, kRows>;
@@ -417,53 +423,70 @@ __device__ __forceinline__ void dkdv_role(const Geo& g, int braw, int nwk,
 
     const int tstep = g.d[R - 1];
     typename C::Ld ld;
+    using L = Rows<T, D>;
     float lse_reg = 0.f;
+    i32x4 orow[L::kSegs];  // kRegDelta: this thread's O row
     auto issue_stage = [&](int s, int buf) {
         ld.compute(ibox, g, gc, s * SB, tstep, wave, lane);
         unsigned char* tile = smem_raw + buf * C::kBufBytes;
         ld.issue(qb, tile, wave);
         ld.issue(gb, tile + C::kTileBytes, wave);
-        ld.issue(ob, tile + 2 * C::kTileBytes, wave);
+        if constexpr (!C::kRegDelta) ld.issue(ob, tile + 2 * C::kTileBytes, wave);
         if (tid < C::kRows) {
             int valid;
             const int tok0 = ibox.block_token(g, gc, s * SB + (tid >> 4), valid);
             const bool ok = (tid & 15) < valid;
-            const float lv = lb[ok ? tok0 + (tid & 15) * tstep : 0];  // token 0: safe stand-in
+            const int tk = ok ? tok0 + (tid & 15) * tstep : 0;  // token 0: safe stand-in
+            const float lv = lb[tk];
             lse_reg = ok ? -lv * kLog2e : 0.f;  // staged negated: -lse2
+            if constexpr (C::kRegDelta) {
+#pragma unroll
+                for (int sg = 0; sg < L::kSegs; ++sg)
+                    orow[sg] = ld16<i32x4>(ob + (size_t)tk * D + sg * L::kVec);
+            }
         }
     };
     auto floats = [&](int buf) {
-        return reinterpret_cast<float*>(smem_raw + buf * C::kBufBytes + 3 * C::kTileBytes);
+        return reinterpret_cast<float*>(smem_raw + buf * C::kBufBytes + C::kFloatOff);
     };
-    // Delta = dO . O of the stage's staged queries, from their LDS rows
-    // (kThreads / kRows lanes per query, reduced with lane shuffles); the
-    // float area holds -lse2 and -Delta per staged query
+    // 16-byte dot product in fp32
+    auto dot16 = [&](i32x4 a, i32x4 b, float acc) {
+        if constexpr (sizeof(T) == 2) {
+            return dot8<T>(__builtin_bit_cast(x8, a), __builtin_bit_cast(x8, b), acc);
+        } else {
+            const f32x4 x = __builtin_bit_cast(f32x4, a), y = __builtin_bit_cast(f32x4, b);
+            return fmaf(x[3], y[3], fmaf(x[2], y[2], fmaf(x[1], y[1], fmaf(x[0], y[0], acc))));
+        }
+    };
+    // Delta = dO . O of the stage's staged queries (dO from its LDS rows; O
+    // from its LDS rows with kThreads / kRows lanes per query reduced by lane
+    // shuffles, or from the thread's registers); the float area holds -lse2
+    // and -Delta per staged query
     auto delta_pass = [&](int buf) {
-        using L = Rows<T, D>;
-        constexpr int kP = C::kThreads / C::kRows;
-        constexpr int kSpt = (L::kSegs + kP - 1) / kP;
         const unsigned char* gt = smem_raw + buf * C::kBufBytes + C::kTileBytes;
-        const unsigned char* ot = gt + C::kTileBytes;
-        const int row = tid / kP, part = tid % kP;
-        float acc = 0.f;
+        if constexpr (C::kRegDelta) {
+            float acc = 0.f;
 #pragma unroll
-        for (int i = 0; i < kSpt; ++i) {
-            const int seg = part * kSpt + i;
-            if (seg < L::kSegs) {
-                const int o = L::off(row, seg);
-                if constexpr (sizeof(T) == 2) {
-                    acc = dot8<T>(__builtin_bit_cast(x8, lds16(gt + o)),
-                                  __builtin_bit_cast(x8, lds16(ot + o)), acc);
-                } else {
-                    const f32x4 a = __builtin_bit_cast(f32x4, lds16(gt + o));
-                    const f32x4 b = __builtin_bit_cast(f32x4, lds16(ot + o));
-                    acc = fmaf(a[3], b[3], fmaf(a[2], b[2], fmaf(a[1], b[1], fmaf(a[0], b[0], acc))));
+            for (int sg = 0; sg < L::kSegs; ++sg) acc = dot16(lds16(gt + L::off(tid, sg)), orow[sg], acc);
+            floats(buf)[C::kRows + tid] = -acc;  // staged negated: -Delta
+        } else {
+            constexpr int kP = C::kThreads / C::kRows;
+            constexpr int kSpt = (L::kSegs + kP - 1) / kP;
+            const unsigned char* ot = gt + C::kTileBytes;
+            const int row = tid / kP, part = tid % kP;
+            float acc = 0.f;
+#pragma unroll
+            for (int i = 0; i < kSpt; ++i) {
+                const int seg = part * kSpt + i;
+                if (seg < L::kSegs) {
+                    const int o = L::off(row, seg);
+                    acc = dot16(lds16(gt + o), lds16(ot + o), acc);
                 }
             }
-        }
 #pragma unroll
-        for (int w = 1; w < kP; w <<= 1) acc += __shfl_xor(acc, w, kWave);
-        if (part == 0) floats(buf)[C::kRows + row] = -acc;  // staged negated: -Delta
+            for (int w = 1; w < kP; w <<= 1) acc += __shfl_xor(acc, w, kWave);
+            if (part == 0) floats(buf)[C::kRows + row] = -acc;  // staged negated: -Delta
+        }
     };
     RowFrag<T, D> rfr;
     ColFrag<T, D> cfr;
