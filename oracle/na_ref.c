@@ -22,10 +22,17 @@
  *     dP = PN(dO, V), dA = P * (dP - Delta), dQ = NN(dA, K) * scale,
  *     dK = IN(dA, Q) * scale, dV = IN(P, dO).
  *
+ *   - Causal masking per axis (Fig. "neighborhoodattention" caption, Sec. 3.4
+ *     "Dilation and causal masking"): along a causal axis a query never
+ *     interacts with context tokens of larger coordinate.
+ *
  * Readings where the paper is silent (listed in the design notes too):
  *   - window start in group coordinates is clamp(p - floor(k/2), 0, n - k);
  *     for odd k this is exactly "the k nearest same-group coordinates"; for
  *     even k it puts one more neighbour before the query than after it.
+ *   - along a causal axis the window is the k nearest same-group positions
+ *     not after the query: [max(0, p - k + 1), p], so queries with p < k - 1
+ *     have only p + 1 neighbours on that axis (a variable window).
  *   - legal parameters: 1 <= rank <= 3, k >= 1, d >= 1, k * d <= extent.
  *   - layout [B, H, X_1 .. X_r, D] row-major, axis 1 outermost.
  *
@@ -72,20 +79,33 @@ static int check_problem(int rank, const int64_t* L, const int32_t* k, const int
 }
 
 /*
- * The k neighbours of coordinate x along one axis of length L at dilation d.
- * The axis splits into d groups (x mod d); inside its group, x sits at
- * position p = x / d of a line of n = ceil((L - g) / d) tokens, and its window
- * is the k consecutive group positions starting at clamp(p - k/2, 0, n - k).
+ * The neighbours of coordinate x along one axis of length L at dilation d;
+ * returns how many there are.  The axis splits into d groups (x mod d);
+ * inside its group, x sits at position p = x / d of a line of
+ * n = ceil((L - g) / d) tokens.  Its window is the k consecutive group
+ * positions starting at clamp(p - k/2, 0, n - k), or, along a causal axis,
+ * the positions max(0, p - k + 1) .. p.
  */
-static void axis_window(int64_t x, int64_t L, int32_t k, int32_t d, int64_t* out) {
+static int32_t axis_window(int64_t x, int64_t L, int32_t k, int32_t d, int causal, int64_t* out) {
     int64_t g = x % d;
     int64_t p = x / d;
     int64_t n = (L - g + d - 1) / d;
-    int64_t s = p - k / 2;
-    if (s < 0) s = 0;
-    if (s > n - k) s = n - k;
-    for (int32_t t = 0; t < k; ++t) out[t] = g + (int64_t)d * (s + t);
+    int64_t s, cnt;
+    if (causal) {
+        s = p - k + 1;
+        if (s < 0) s = 0;
+        cnt = p - s + 1;
+    } else {
+        s = p - k / 2;
+        if (s < 0) s = 0;
+        if (s > n - k) s = n - k;
+        cnt = k;
+    }
+    for (int64_t t = 0; t < cnt; ++t) out[t] = g + (int64_t)d * (s + t);
+    return (int32_t)cnt;
 }
+
+static int is_causal(const int32_t* causal, int a) { return causal != NULL && causal[a] != 0; }
 
 static int64_t tokens_of(int rank, const int64_t* L) {
     int64_t n = 1;
@@ -109,36 +129,45 @@ static void unravel(int rank, const int64_t* L, int64_t t, int64_t* x) {
 
 /*
  * Full neighbour list of token t: the Cartesian product of the per-axis
- * windows, in row-major order (axis 0 outermost).  Writes prod k_a token
- * indices into nb.
+ * windows, in row-major order (axis 0 outermost).  Writes the token indices
+ * into nb and returns how many there are (prod k_a without causal axes).
  */
-static void neighbours_of(int rank, const int64_t* L, const int32_t* k, const int32_t* d,
-                          int64_t t, int64_t* nb) {
+static int64_t neighbours_of(int rank, const int64_t* L, const int32_t* k, const int32_t* d,
+                             const int32_t* causal, int64_t t, int64_t* nb) {
     int64_t x[NA_REF_MAX_RANK];
     int64_t w[NA_REF_MAX_RANK][4096];
+    int32_t cnt[NA_REF_MAX_RANK];
     unravel(rank, L, t, x);
-    for (int a = 0; a < rank; ++a) axis_window(x[a], L[a], k[a], d[a], w[a]);
-    int64_t ell = window_size(rank, k);
+    int64_t ell = 1;
+    for (int a = 0; a < rank; ++a) {
+        cnt[a] = axis_window(x[a], L[a], k[a], d[a], is_causal(causal, a), w[a]);
+        ell *= cnt[a];
+    }
     for (int64_t e = 0; e < ell; ++e) {
         int64_t rem = e, tok = 0;
         int64_t pick[NA_REF_MAX_RANK];
         for (int a = rank - 1; a >= 0; --a) {
-            pick[a] = rem % k[a];
-            rem /= k[a];
+            pick[a] = rem % cnt[a];
+            rem /= cnt[a];
         }
         for (int a = 0; a < rank; ++a) tok = tok * L[a] + w[a][pick[a]];
         nb[e] = tok;
     }
+    return ell;
 }
 
-/* Neighbour lists for every token: idx is [N][ell]. */
-int na_ref_neighbors(int rank, const int64_t* L, const int32_t* k, const int32_t* d, int64_t* idx) {
+/* Neighbour lists for every token: idx is [N][prod k], rows padded with -1. */
+int na_ref_neighbors(int rank, const int64_t* L, const int32_t* k, const int32_t* d,
+                     const int32_t* causal, int64_t* idx) {
     int st = check_problem(rank, L, k, d);
     if (st) return st;
     for (int a = 0; a < rank; ++a)
         if (k[a] > 4096) return REF_ERR_KERNEL_SIZE;
     int64_t N = tokens_of(rank, L), ell = window_size(rank, k);
-    for (int64_t t = 0; t < N; ++t) neighbours_of(rank, L, k, d, t, idx + t * ell);
+    for (int64_t t = 0; t < N; ++t) {
+        int64_t c = neighbours_of(rank, L, k, d, causal, t, idx + t * ell);
+        for (int64_t e = c; e < ell; ++e) idx[t * ell + e] = -1;
+    }
     return REF_OK;
 }
 
@@ -149,8 +178,8 @@ int na_ref_neighbors(int rank, const int64_t* L, const int32_t* k, const int32_t
  *   inv_hi[j] = largest such query coordinate,
  *   inv_cnt[j] = number of such queries.
  */
-int na_ref_axis_relation(int64_t L, int32_t k, int32_t d, int64_t* first, int64_t* inv_lo,
-                         int64_t* inv_hi, int64_t* inv_cnt) {
+int na_ref_axis_relation(int64_t L, int32_t k, int32_t d, int32_t causal, int64_t* first,
+                         int64_t* inv_lo, int64_t* inv_hi, int64_t* inv_cnt) {
     int32_t kk[1] = {k}, dd[1] = {d};
     int64_t LL[1] = {L};
     int st = check_problem(1, LL, kk, dd);
@@ -163,9 +192,9 @@ int na_ref_axis_relation(int64_t L, int32_t k, int32_t d, int64_t* first, int64_
         inv_cnt[j] = 0;
     }
     for (int64_t x = 0; x < L; ++x) {
-        axis_window(x, L, k, d, w);
+        const int32_t c = axis_window(x, L, k, d, causal != 0, w);
         int64_t mn = w[0];
-        for (int32_t t = 0; t < k; ++t) {
+        for (int32_t t = 0; t < c; ++t) {
             if (w[t] < mn) mn = w[t];
             int64_t j = w[t];
             if (inv_lo[j] < 0 || x < inv_lo[j]) inv_lo[j] = x;
@@ -212,9 +241,9 @@ static void attend_row(int64_t D, double scale, const double* qrow, const double
 /*
  * Forward pass.  q, k, v, out are [B, H, N, D]; lse is [B, H, N].
  */
-int na_ref_forward(int rank, const int64_t* L, const int32_t* ks, const int32_t* dil, int64_t B,
-                   int64_t H, int64_t D, double scale, const double* q, const double* k,
-                   const double* v, double* out, double* lse) {
+int na_ref_forward(int rank, const int64_t* L, const int32_t* ks, const int32_t* dil,
+                   const int32_t* causal, int64_t B, int64_t H, int64_t D, double scale,
+                   const double* q, const double* k, const double* v, double* out, double* lse) {
     int st = check_problem(rank, L, ks, dil);
     if (st) return st;
     for (int a = 0; a < rank; ++a)
@@ -233,8 +262,8 @@ int na_ref_forward(int rank, const int64_t* L, const int32_t* ks, const int32_t*
 #pragma omp for schedule(dynamic, 64)
             for (int64_t r = 0; r < rows; ++r) {
                 int64_t slice = r / N, t = r % N;
-                neighbours_of(rank, L, ks, dil, t, nb);
-                attend_row(D, scale, q + r * D, k + slice * N * D, v + slice * N * D, nb, ell, p,
+                int64_t c = neighbours_of(rank, L, ks, dil, causal, t, nb);
+                attend_row(D, scale, q + r * D, k + slice * N * D, v + slice * N * D, nb, c, p,
                            out + r * D, lse + r);
             }
         }
@@ -248,10 +277,10 @@ int na_ref_forward(int rank, const int64_t* L, const int32_t* ks, const int32_t*
  * Forward pass for a subset of query rows only (rows are flat indices into
  * [B*H*N]); out_rows is [nrows, D], lse_rows is [nrows].
  */
-int na_ref_forward_rows(int rank, const int64_t* L, const int32_t* ks, const int32_t* dil, int64_t B,
-                        int64_t H, int64_t D, double scale, const double* q, const double* k,
-                        const double* v, int64_t nrows, const int64_t* rows, double* out_rows,
-                        double* lse_rows) {
+int na_ref_forward_rows(int rank, const int64_t* L, const int32_t* ks, const int32_t* dil,
+                        const int32_t* causal, int64_t B, int64_t H, int64_t D, double scale,
+                        const double* q, const double* k, const double* v, int64_t nrows,
+                        const int64_t* rows, double* out_rows, double* lse_rows) {
     int st = check_problem(rank, L, ks, dil);
     if (st) return st;
     for (int a = 0; a < rank; ++a)
@@ -272,8 +301,8 @@ int na_ref_forward_rows(int rank, const int64_t* L, const int32_t* ks, const int
             for (int64_t i = 0; i < nrows; ++i) {
                 int64_t r = rows[i];
                 int64_t slice = r / N, t = r % N;
-                neighbours_of(rank, L, ks, dil, t, nb);
-                attend_row(D, scale, q + r * D, k + slice * N * D, v + slice * N * D, nb, ell, p,
+                int64_t c = neighbours_of(rank, L, ks, dil, causal, t, nb);
+                attend_row(D, scale, q + r * D, k + slice * N * D, v + slice * N * D, nb, c, p,
                            out_rows + i * D, lse_rows + i);
             }
         }
@@ -294,9 +323,10 @@ int na_ref_forward_rows(int rank, const int64_t* L, const int32_t* ks, const int
  *   dV[j]    += P[x,j] dO[x]                      (IN on P and dO)
  * One (b, h) slice per thread, so the scatter into dK/dV is race-free.
  */
-int na_ref_backward(int rank, const int64_t* L, const int32_t* ks, const int32_t* dil, int64_t B,
-                    int64_t H, int64_t D, double scale, const double* q, const double* k,
-                    const double* v, const double* dout, double* dq, double* dk, double* dv) {
+int na_ref_backward(int rank, const int64_t* L, const int32_t* ks, const int32_t* dil,
+                    const int32_t* causal, int64_t B, int64_t H, int64_t D, double scale,
+                    const double* q, const double* k, const double* v, const double* dout,
+                    double* dq, double* dk, double* dv) {
     int st = check_problem(rank, L, ks, dil);
     if (st) return st;
     for (int a = 0; a < rank; ++a)
@@ -326,14 +356,14 @@ int na_ref_backward(int rank, const int64_t* L, const int32_t* ks, const int32_t
                 double* dvs = dv + sl * N * D;
                 for (int64_t t = 0; t < N; ++t) {
                     double lse_unused;
-                    neighbours_of(rank, L, ks, dil, t, nb);
-                    attend_row(D, scale, qs + t * D, kb, vb, nb, ell, p, o, &lse_unused);
+                    int64_t cnt = neighbours_of(rank, L, ks, dil, causal, t, nb);
+                    attend_row(D, scale, qs + t * D, kb, vb, nb, cnt, p, o, &lse_unused);
                     const double* g = gs + t * D;
                     double delta = 0.0;
                     for (int64_t c = 0; c < D; ++c) delta += g[c] * o[c];
                     double* dqr = dqs + t * D;
                     for (int64_t c = 0; c < D; ++c) dqr[c] = 0.0;
-                    for (int64_t e = 0; e < ell; ++e) {
+                    for (int64_t e = 0; e < cnt; ++e) {
                         int64_t j = nb[e];
                         const double* vr = vb + j * D;
                         double dp = 0.0;
@@ -360,14 +390,14 @@ int na_ref_backward(int rank, const int64_t* L, const int32_t* ks, const int32_t
 
 /* True when token j is among the neighbours of token t (per-axis test). */
 static int is_neighbour(int rank, const int64_t* L, const int32_t* ks, const int32_t* dil,
-                        int64_t t, int64_t j, int64_t* wbuf) {
+                        const int32_t* causal, int64_t t, int64_t j, int64_t* wbuf) {
     int64_t xt[NA_REF_MAX_RANK], xj[NA_REF_MAX_RANK];
     unravel(rank, L, t, xt);
     unravel(rank, L, j, xj);
     for (int a = 0; a < rank; ++a) {
-        axis_window(xt[a], L[a], ks[a], dil[a], wbuf);
+        const int32_t c = axis_window(xt[a], L[a], ks[a], dil[a], is_causal(causal, a), wbuf);
         int hit = 0;
-        for (int32_t e = 0; e < ks[a]; ++e)
+        for (int32_t e = 0; e < c; ++e)
             if (wbuf[e] == xj[a]) hit = 1;
         if (!hit) return 0;
     }
@@ -382,10 +412,10 @@ static int is_neighbour(int rank, const int64_t* L, const int32_t* ks, const int
  *   scanning all queries of the slice).
  */
 int na_ref_backward_rows(int rank, const int64_t* L, const int32_t* ks, const int32_t* dil,
-                         int64_t B, int64_t H, int64_t D, double scale, const double* q,
-                         const double* k, const double* v, const double* dout, int64_t nq,
-                         const int64_t* qrows, double* dq_rows, int64_t nk, const int64_t* krows,
-                         double* dk_rows, double* dv_rows) {
+                         const int32_t* causal, int64_t B, int64_t H, int64_t D, double scale,
+                         const double* q, const double* k, const double* v, const double* dout,
+                         int64_t nq, const int64_t* qrows, double* dq_rows, int64_t nk,
+                         const int64_t* krows, double* dk_rows, double* dv_rows) {
     int st = check_problem(rank, L, ks, dil);
     if (st) return st;
     for (int a = 0; a < rank; ++a)
@@ -414,13 +444,13 @@ int na_ref_backward_rows(int rank, const int64_t* L, const int32_t* ks, const in
                 const double* vb = v + sl * N * D;
                 const double* g = dout + r * D;
                 double lse_unused;
-                neighbours_of(rank, L, ks, dil, t, nb);
-                attend_row(D, scale, q + r * D, kb, vb, nb, ell, p, o, &lse_unused);
+                int64_t cnt = neighbours_of(rank, L, ks, dil, causal, t, nb);
+                attend_row(D, scale, q + r * D, kb, vb, nb, cnt, p, o, &lse_unused);
                 double delta = 0.0;
                 for (int64_t c = 0; c < D; ++c) delta += g[c] * o[c];
                 double* dqr = dq_rows + i * D;
                 for (int64_t c = 0; c < D; ++c) dqr[c] = 0.0;
-                for (int64_t e = 0; e < ell; ++e) {
+                for (int64_t e = 0; e < cnt; ++e) {
                     const double* vr = vb + nb[e] * D;
                     double dp = 0.0;
                     for (int64_t c = 0; c < D; ++c) dp += g[c] * vr[c];
@@ -444,14 +474,14 @@ int na_ref_backward_rows(int rank, const int64_t* L, const int32_t* ks, const in
                     dvr[c] = 0.0;
                 }
                 for (int64_t t = 0; t < N; ++t) {
-                    if (!is_neighbour(rank, L, ks, dil, t, j, wbuf)) continue;
+                    if (!is_neighbour(rank, L, ks, dil, causal, t, j, wbuf)) continue;
                     double lse_unused;
-                    neighbours_of(rank, L, ks, dil, t, nb);
-                    attend_row(D, scale, qs + t * D, kb, vb, nb, ell, p, o, &lse_unused);
+                    int64_t cnt = neighbours_of(rank, L, ks, dil, causal, t, nb);
+                    attend_row(D, scale, qs + t * D, kb, vb, nb, cnt, p, o, &lse_unused);
                     const double* g = gs + t * D;
                     double delta = 0.0;
                     for (int64_t c = 0; c < D; ++c) delta += g[c] * o[c];
-                    for (int64_t e = 0; e < ell; ++e) {
+                    for (int64_t e = 0; e < cnt; ++e) {
                         if (nb[e] != j) continue;
                         const double* vr = vb + j * D;
                         double dp = 0.0;
