@@ -65,7 +65,8 @@ def cpu_baseline(problem, x, budget_s):
     q, k, v = f(x["q"]), f(x["k"]), f(x["v"])
     reps, t0 = 0, time.perf_counter()
     while True:
-        oracle.forward(q, k, v, problem.kernel_size, problem.dilation, problem.softmax_scale)
+        oracle.forward(q, k, v, problem.kernel_size, problem.dilation, problem.softmax_scale,
+                       causal=problem.causal_axes)
         reps += 1
         el = time.perf_counter() - t0
         if el >= budget_s or reps >= 10000:
@@ -121,12 +122,13 @@ def main():
     lse = torch.empty(q.shape[:-1], dtype=torch.float32, device=dev)
     dq, dk, dv = torch.empty_like(q), torch.empty_like(k), torch.empty_like(v)
     ks, ds, sc = p.kernel_size, p.dilation, p.softmax_scale
+    cz = p.causal_axes if any(p.causal_axes) else None
 
     def fwd():
-        na.forward(q, k, v, ks, ds, sc, out=out, lse=lse)
+        na.forward(q, k, v, ks, ds, sc, out=out, lse=lse, causal=cz)
 
     def bwd():
-        na.backward(q, k, v, out, lse, g, ks, ds, sc, dq=dq, dk=dk, dv=dv)
+        na.backward(q, k, v, out, lse, g, ks, ds, sc, dq=dq, dk=dk, dv=dv, causal=cz)
 
     def step():
         fwd()
@@ -202,7 +204,8 @@ def main():
             "workload": p.name,
             "rank": p.rank, "batch": p.batch, "heads": p.heads, "extents": list(p.extents),
             "head_dim": p.head_dim, "kernel_size": list(p.kernel_size),
-            "dilation": list(p.dilation), "step": "na_forward + na_backward",
+            "dilation": list(p.dilation), "causal": list(p.causal_axes),
+            "step": "na_forward + na_backward",
         },
         "fwd_ms": round(fwd_ms, 5),
         "bwd_ms": round(bwd_ms, 5),

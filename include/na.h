@@ -11,6 +11,11 @@
  *   sub-lattices x = g (mod d_a), each an independent non-dilated problem
  *   (Sec. 3.4).  Inside a group of n tokens, the window of position p starts
  *   at clamp(p - floor(k/2), 0, n - k).
+ *   Causal masking per axis (Sec. 3.4; caption of Fig. "neighborhoodattention"):
+ *   along a causal axis a query never attends to a token of larger
+ *   coordinate; its window there is the k nearest same-group positions not
+ *   after it, [max(0, p - k + 1), p], so the first k - 1 positions of each
+ *   group have shorter windows (e.g. 3-D attention with causal time).
  *   The attention itself is Eq. 1 restricted to that neighbourhood, computed
  *   fused (Sec. 3.3, Fig. "fna-vis"): scores, mask, online softmax and the
  *   product with V in one kernel; no attention weights reach global memory.
@@ -28,6 +33,8 @@
  *     NULL means the legacy default stream).  Problem validation is
  *     synchronous and happens before any launch: a non-NA_OK status means
  *     nothing was launched.  NA_ERR_HIP reports a failed launch.
+ *   - causal: NULL (no causal axis) or rank int32 flags, outermost axis first;
+ *     nonzero marks a causal axis.
  *   - B * H * N == 0 (empty batch or heads) is a no-op returning NA_OK.
  *   - Supported: rank 1..3, head_dim in {32, 64, 128}, any k_a >= 1 and
  *     d_a >= 1 with k_a * d_a <= X_a, fp32 / fp16 / bf16.  N * D must stay
@@ -73,24 +80,25 @@ int na_version(void);
 
 /*
  * Host-only check of the problem description used by every entry point
- * (rank, extents, kernel_size, dilation, batch, heads, head_dim, dtype,
- * scale).  Touches no device and no pointer.
+ * (rank, extents, kernel_size, dilation, causal, batch, heads, head_dim,
+ * dtype, scale).  Touches no device and no pointer other than the arrays.
  */
 na_status na_validate(int rank, const int64_t* extents, const int32_t* kernel_size,
-                      const int32_t* dilation, int64_t batch, int64_t heads, int64_t head_dim,
-                      na_dtype dtype, float scale);
+                      const int32_t* dilation, const int32_t* causal, int64_t batch, int64_t heads,
+                      int64_t head_dim, na_dtype dtype, float scale);
 
 /*
  * Fused NA forward (Sec. 3.3): out = softmax(scale * q k^T restricted to each
  * query's neighbourhood) v, and logsumexp per query (kept for the backward,
  * which recomputes the probabilities from it instead of storing them).
- *   extents[rank], kernel_size[rank], dilation[rank]: per axis, outermost first.
+ *   extents[rank], kernel_size[rank], dilation[rank], causal[rank] (or NULL):
+ *   per axis, outermost first.
  *   scale: softmax scale (1/sqrt(head_dim) in Eq. 1; any finite value).
  */
 na_status na_forward(int rank, const int64_t* extents, const int32_t* kernel_size,
-                     const int32_t* dilation, int64_t batch, int64_t heads, int64_t head_dim,
-                     na_dtype dtype, float scale, const void* q, const void* k, const void* v,
-                     void* out, float* logsumexp, na_stream_t stream);
+                     const int32_t* dilation, const int32_t* causal, int64_t batch, int64_t heads,
+                     int64_t head_dim, na_dtype dtype, float scale, const void* q, const void* k,
+                     const void* v, void* out, float* logsumexp, na_stream_t stream);
 
 /*
  * Fused NA backward: gradients of out with respect to q, k and v given
@@ -103,10 +111,10 @@ na_status na_forward(int rank, const int64_t* extents, const int32_t* kernel_siz
  *   Deterministic: the same inputs give bit-identical gradients.
  */
 na_status na_backward(int rank, const int64_t* extents, const int32_t* kernel_size,
-                      const int32_t* dilation, int64_t batch, int64_t heads, int64_t head_dim,
-                      na_dtype dtype, float scale, const void* q, const void* k, const void* v,
-                      const void* out, const float* logsumexp, const void* dout, void* dq,
-                      void* dk, void* dv, na_stream_t stream);
+                      const int32_t* dilation, const int32_t* causal, int64_t batch, int64_t heads,
+                      int64_t head_dim, na_dtype dtype, float scale, const void* q, const void* k,
+                      const void* v, const void* out, const float* logsumexp, const void* dout,
+                      void* dq, void* dk, void* dv, na_stream_t stream);
 
 /*
  * Test hook: evaluates on the device, with the same index functions the
@@ -117,8 +125,8 @@ na_status na_backward(int rank, const int64_t* extents, const int32_t* kernel_si
  *   inv_hi[j] = largest query coordinate whose window contains key j.
  */
 na_status na_debug_windows(int rank, const int64_t* extents, const int32_t* kernel_size,
-                           const int32_t* dilation, int32_t* start, int32_t* inv_lo,
-                           int32_t* inv_hi, na_stream_t stream);
+                           const int32_t* dilation, const int32_t* causal, int32_t* start,
+                           int32_t* inv_lo, int32_t* inv_hi, na_stream_t stream);
 
 #ifdef __cplusplus
 }

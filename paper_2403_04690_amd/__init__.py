@@ -8,7 +8,9 @@ device memory and streams.  If the library is missing, every call raises.
 Neighborhood attention (Faster Neighborhood Attention, arXiv 2403.04690):
 each query attends to its k_a nearest same-group tokens along every axis a
 (window centred where possible, shifted at borders, never truncated), with
-dilation d_a splitting each axis into d_a interleaved sub-lattices.
+dilation d_a splitting each axis into d_a interleaved sub-lattices.  Axes can
+be causal (``causal``, one flag per axis): there a query attends only to the
+k nearest positions not after it.
 """
 import ctypes
 import math
@@ -54,8 +56,8 @@ def load_library():
             f"libna.so not found at {_LIB_PATH}: build it first "
             "(python -c 'import __graft_entry__ as g; g.build()')")
     lib = ctypes.CDLL(_LIB_PATH)
-    prob = [ctypes.c_int, _i64p, _i32p, _i32p, ctypes.c_int64, ctypes.c_int64, ctypes.c_int64,
-            ctypes.c_int, ctypes.c_float]
+    prob = [ctypes.c_int, _i64p, _i32p, _i32p, _i32p, ctypes.c_int64, ctypes.c_int64,
+            ctypes.c_int64, ctypes.c_int, ctypes.c_float]
     lib.na_status_string.argtypes = [ctypes.c_int]
     lib.na_status_string.restype = ctypes.c_char_p
     lib.na_version.restype = ctypes.c_int
@@ -65,7 +67,7 @@ def load_library():
     lib.na_forward.restype = ctypes.c_int
     lib.na_backward.argtypes = prob + [_vp] * 10
     lib.na_backward.restype = ctypes.c_int
-    lib.na_debug_windows.argtypes = [ctypes.c_int, _i64p, _i32p, _i32p, _vp, _vp, _vp, _vp]
+    lib.na_debug_windows.argtypes = [ctypes.c_int, _i64p, _i32p, _i32p, _i32p, _vp, _vp, _vp, _vp]
     lib.na_debug_windows.restype = ctypes.c_int
     _lib = lib
     return lib
@@ -84,12 +86,14 @@ def _per_axis(value, rank, name):
     return vals
 
 
-def _problem_arrays(extents, kernel_size, dilation):
+def _problem_arrays(extents, kernel_size, dilation, causal=None):
     rank = len(extents)
     ext = (ctypes.c_int64 * rank)(*[int(e) for e in extents])
     ks = (ctypes.c_int32 * rank)(*_per_axis(kernel_size, rank, "kernel_size"))
     ds = (ctypes.c_int32 * rank)(*_per_axis(dilation, rank, "dilation"))
-    return rank, ext, ks, ds
+    cs = None if causal is None else (ctypes.c_int32 * rank)(
+        *[int(bool(c)) for c in _per_axis(causal, rank, "causal")])
+    return rank, ext, ks, ds, cs
 
 
 def _stream(device):
@@ -111,20 +115,20 @@ def _check_tensors(ref, *others):
             raise ValueError("q, k, v (and grads) must share dtype, shape and device")
 
 
-def validate(extents, kernel_size, dilation, batch, heads, head_dim, dtype, scale):
+def validate(extents, kernel_size, dilation, batch, heads, head_dim, dtype, scale, causal=None):
     """Host-only validation through na_validate; raises NAError on a bad problem."""
     lib = load_library()
-    rank, ext, ks, ds = _problem_arrays(extents, kernel_size, dilation)
-    _check(lib.na_validate(rank, ext, ks, ds, batch, heads, head_dim, DTYPES[dtype], scale))
+    rank, ext, ks, ds, cs = _problem_arrays(extents, kernel_size, dilation, causal)
+    _check(lib.na_validate(rank, ext, ks, ds, cs, batch, heads, head_dim, DTYPES[dtype], scale))
 
 
-def forward(q, k, v, kernel_size, dilation=1, scale=None, out=None, lse=None):
+def forward(q, k, v, kernel_size, dilation=1, scale=None, out=None, lse=None, causal=None):
     """Fused NA forward.  Returns (out, logsumexp); logsumexp is fp32 [B, H, X..]."""
     lib = load_library()
     _check_tensors(q, k, v)
     B, H, D = q.shape[0], q.shape[1], q.shape[-1]
     extents = tuple(q.shape[2:-1])
-    rank, ext, ks, ds = _problem_arrays(extents, kernel_size, dilation)
+    rank, ext, ks, ds, cs = _problem_arrays(extents, kernel_size, dilation, causal)
     if scale is None:
         scale = 1.0 / math.sqrt(D)
     if out is None:
@@ -134,20 +138,20 @@ def forward(q, k, v, kernel_size, dilation=1, scale=None, out=None, lse=None):
     _check_tensors(q, out)
     if lse.dtype != torch.float32 or lse.shape != q.shape[:-1] or not lse.is_contiguous():
         raise ValueError("lse must be a contiguous fp32 tensor of shape q.shape[:-1]")
-    _check(lib.na_forward(rank, ext, ks, ds, B, H, D, DTYPES[q.dtype], float(scale),
+    _check(lib.na_forward(rank, ext, ks, ds, cs, B, H, D, DTYPES[q.dtype], float(scale),
                           q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(),
                           lse.data_ptr(), _stream(q.device)))
     return out, lse
 
 
 def backward(q, k, v, out, lse, dout, kernel_size, dilation=1, scale=None, dq=None, dk=None,
-             dv=None):
+             dv=None, causal=None):
     """Fused NA backward.  Returns (dq, dk, dv)."""
     lib = load_library()
     _check_tensors(q, k, v, out, dout)
     B, H, D = q.shape[0], q.shape[1], q.shape[-1]
     extents = tuple(q.shape[2:-1])
-    rank, ext, ks, ds = _problem_arrays(extents, kernel_size, dilation)
+    rank, ext, ks, ds, cs = _problem_arrays(extents, kernel_size, dilation, causal)
     if scale is None:
         scale = 1.0 / math.sqrt(D)
     if lse.dtype != torch.float32 or lse.shape != q.shape[:-1] or not lse.is_contiguous():
@@ -156,42 +160,43 @@ def backward(q, k, v, out, lse, dout, kernel_size, dilation=1, scale=None, dq=No
     dk = torch.empty_like(k) if dk is None else dk
     dv = torch.empty_like(v) if dv is None else dv
     _check_tensors(q, dq, dk, dv)
-    _check(lib.na_backward(rank, ext, ks, ds, B, H, D, DTYPES[q.dtype], float(scale),
+    _check(lib.na_backward(rank, ext, ks, ds, cs, B, H, D, DTYPES[q.dtype], float(scale),
                            q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(),
                            lse.data_ptr(), dout.data_ptr(), dq.data_ptr(), dk.data_ptr(),
                            dv.data_ptr(), _stream(q.device)))
     return dq, dk, dv
 
 
-def debug_windows(extents, kernel_size, dilation, device="cuda"):
+def debug_windows(extents, kernel_size, dilation, device="cuda", causal=None):
     """Per-axis window starts and inverse ranges computed on the device (int32, concatenated)."""
     lib = load_library()
-    rank, ext, ks, ds = _problem_arrays(extents, kernel_size, dilation)
+    rank, ext, ks, ds, cs = _problem_arrays(extents, kernel_size, dilation, causal)
     total = int(sum(extents))
     start = torch.empty(total, dtype=torch.int32, device=device)
     ilo = torch.empty_like(start)
     ihi = torch.empty_like(start)
-    _check(lib.na_debug_windows(rank, ext, ks, ds, start.data_ptr(), ilo.data_ptr(),
+    _check(lib.na_debug_windows(rank, ext, ks, ds, cs, start.data_ptr(), ilo.data_ptr(),
                                 ihi.data_ptr(), _stream(start.device)))
     return start, ilo, ihi
 
 
 class _NAFunction(torch.autograd.Function):
     @staticmethod
-    def forward(ctx, q, k, v, kernel_size, dilation, scale):
-        out, lse = forward(q, k, v, kernel_size, dilation, scale)
+    def forward(ctx, q, k, v, kernel_size, dilation, scale, causal):
+        out, lse = forward(q, k, v, kernel_size, dilation, scale, causal=causal)
         ctx.save_for_backward(q, k, v, out, lse)
-        ctx.cfg = (kernel_size, dilation, scale)
+        ctx.cfg = (kernel_size, dilation, scale, causal)
         return out
 
     @staticmethod
     def backward(ctx, dout):
         q, k, v, out, lse = ctx.saved_tensors
-        kernel_size, dilation, scale = ctx.cfg
-        dq, dk, dv = backward(q, k, v, out, lse, dout.contiguous(), kernel_size, dilation, scale)
-        return dq, dk, dv, None, None, None
+        kernel_size, dilation, scale, causal = ctx.cfg
+        dq, dk, dv = backward(q, k, v, out, lse, dout.contiguous(), kernel_size, dilation, scale,
+                              causal=causal)
+        return dq, dk, dv, None, None, None, None
 
 
-def na_attention(q, k, v, kernel_size, dilation=1, scale=None):
+def na_attention(q, k, v, kernel_size, dilation=1, scale=None, causal=None):
     """Autograd-aware fused neighborhood attention on [B, H, X_1..X_r, D] tensors."""
-    return _NAFunction.apply(q, k, v, kernel_size, dilation, scale)
+    return _NAFunction.apply(q, k, v, kernel_size, dilation, scale, causal)

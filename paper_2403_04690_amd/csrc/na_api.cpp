@@ -14,7 +14,7 @@
 
 namespace {
 
-constexpr int kVersion = 100;  // 0.1.0
+constexpr int kVersion = 200;  // 0.2.0
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
@@ -83,14 +83,15 @@ void wave_tile(int rank, const int* glen, int m, int* wt, int* wgd) {
 }
 
 // Fills the geometry of a problem for wave tiles of 16 * m tokens.
-bool make_geo(int rank, const int64_t* extents, const int32_t* ks, const int32_t* ds, int64_t BH,
-              int m, na::Geo& g) {
+bool make_geo(int rank, const int64_t* extents, const int32_t* ks, const int32_t* ds,
+              const int32_t* causal, int64_t BH, int m, na::Geo& g) {
     std::memset(&g, 0, sizeof(g));
     int glen[3] = {1, 1, 1};
     for (int a = 0; a < 3; ++a) {
         g.L[a] = a < rank ? (int)extents[a] : 1;
         g.k[a] = a < rank ? ks[a] : 1;
         g.d[a] = a < rank ? ds[a] : 1;
+        g.causal[a] = a < rank && causal && causal[a] ? 1 : 0;
         glen[a] = na::group_len(g.L[a], g.d[a], 0);
     }
     {
@@ -135,7 +136,7 @@ int choose_m(int rank, const int64_t* extents, const int32_t* ks, const int32_t*
         if (v == 1 || v == 2) return v;
     }
     na::Geo g;
-    if (!make_geo(rank, extents, ks, ds, BH, 2, g)) return 1;
+    if (!make_geo(rank, extents, ks, ds, nullptr, BH, 2, g)) return 1;
     return g.nwg < 1024 ? 1 : 2;
 }
 
@@ -189,16 +190,17 @@ const char* na_status_string(na_status status) {
 int na_version(void) { return kVersion; }
 
 na_status na_validate(int rank, const int64_t* extents, const int32_t* kernel_size,
-                      const int32_t* dilation, int64_t batch, int64_t heads, int64_t head_dim,
-                      na_dtype dtype, float scale) {
+                      const int32_t* dilation, const int32_t* causal, int64_t batch, int64_t heads,
+                      int64_t head_dim, na_dtype dtype, float scale) {
+    (void)causal;  // any value is legal (NULL: no causal axis)
     return check_problem(rank, extents, kernel_size, dilation, batch, heads, head_dim, dtype,
                          scale);
 }
 
 na_status na_forward(int rank, const int64_t* extents, const int32_t* kernel_size,
-                     const int32_t* dilation, int64_t batch, int64_t heads, int64_t head_dim,
-                     na_dtype dtype, float scale, const void* q, const void* k, const void* v,
-                     void* out, float* logsumexp, na_stream_t stream) {
+                     const int32_t* dilation, const int32_t* causal, int64_t batch, int64_t heads,
+                     int64_t head_dim, na_dtype dtype, float scale, const void* q, const void* k,
+                     const void* v, void* out, float* logsumexp, na_stream_t stream) {
     na_status st = check_problem(rank, extents, kernel_size, dilation, batch, heads, head_dim,
                                  dtype, scale);
     if (st != NA_OK) return st;
@@ -210,17 +212,17 @@ na_status na_forward(int rank, const int64_t* extents, const int32_t* kernel_siz
     const int64_t BH = batch * heads;
     const int m = choose_m(rank, extents, kernel_size, dilation, BH);
     na::Geo g;
-    if (!make_geo(rank, extents, kernel_size, dilation, BH, m, g)) return NA_ERR_SHAPE;
+    if (!make_geo(rank, extents, kernel_size, dilation, causal, BH, m, g)) return NA_ERR_SHAPE;
     hipError_t e = na::launch_forward(g, rank, (int)head_dim, (int)dtype, m, q, k, v, out,
                                       logsumexp, scale, reinterpret_cast<hipStream_t>(stream));
     return e == hipSuccess ? NA_OK : NA_ERR_HIP;
 }
 
 na_status na_backward(int rank, const int64_t* extents, const int32_t* kernel_size,
-                      const int32_t* dilation, int64_t batch, int64_t heads, int64_t head_dim,
-                      na_dtype dtype, float scale, const void* q, const void* k, const void* v,
-                      const void* out, const float* logsumexp, const void* dout, void* dq,
-                      void* dk, void* dv, na_stream_t stream) {
+                      const int32_t* dilation, const int32_t* causal, int64_t batch, int64_t heads,
+                      int64_t head_dim, na_dtype dtype, float scale, const void* q, const void* k,
+                      const void* v, const void* out, const float* logsumexp, const void* dout,
+                      void* dq, void* dk, void* dv, na_stream_t stream) {
     na_status st = check_problem(rank, extents, kernel_size, dilation, batch, heads, head_dim,
                                  dtype, scale);
     if (st != NA_OK) return st;
@@ -232,7 +234,7 @@ na_status na_backward(int rank, const int64_t* extents, const int32_t* kernel_si
     const int64_t BH = batch * heads;
     const int m = choose_m(rank, extents, kernel_size, dilation, BH);
     na::Geo g;
-    if (!make_geo(rank, extents, kernel_size, dilation, BH, m, g)) return NA_ERR_SHAPE;
+    if (!make_geo(rank, extents, kernel_size, dilation, causal, BH, m, g)) return NA_ERR_SHAPE;
     hipError_t e = na::launch_backward(g, rank, (int)head_dim, (int)dtype, m, q, k, v, out,
                                        logsumexp, dout, dq, dk, dv, scale,
                                        reinterpret_cast<hipStream_t>(stream));
@@ -240,18 +242,19 @@ na_status na_backward(int rank, const int64_t* extents, const int32_t* kernel_si
 }
 
 na_status na_debug_windows(int rank, const int64_t* extents, const int32_t* kernel_size,
-                           const int32_t* dilation, int32_t* start, int32_t* inv_lo,
-                           int32_t* inv_hi, na_stream_t stream) {
+                           const int32_t* dilation, const int32_t* causal, int32_t* start,
+                           int32_t* inv_lo, int32_t* inv_hi, na_stream_t stream) {
     na_status st = check_problem(rank, extents, kernel_size, dilation, 1, 1, 32, NA_FP16, 1.0f);
     if (st != NA_OK) return st;
     if (!start || !inv_lo || !inv_hi) return NA_ERR_NULL;
-    int L[3], ks[3], ds[3];
+    int L[3], ks[3], ds[3], cs[3];
     for (int a = 0; a < rank; ++a) {
         L[a] = (int)extents[a];
         ks[a] = kernel_size[a];
         ds[a] = dilation[a];
+        cs[a] = causal && causal[a] ? 1 : 0;
     }
-    hipError_t e = na::launch_debug_windows(rank, L, ks, ds, start, inv_lo, inv_hi,
+    hipError_t e = na::launch_debug_windows(rank, L, ks, ds, cs, start, inv_lo, inv_hi,
                                             reinterpret_cast<hipStream_t>(stream));
     return e == hipSuccess ? NA_OK : NA_ERR_HIP;
 }

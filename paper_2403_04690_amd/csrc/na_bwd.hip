@@ -67,8 +67,9 @@ __device__ __forceinline__ void dq_role(const Geo& g, int braw, unsigned char* s
         to[a] = tc[a] * g.T[a];
         if (to[a] >= n[a]) return;
         const int last = min(to[a] + g.T[a], n[a]) - 1;
-        halo.lo[a] = win_start(to[a], n[a], g.k[a]);
-        halo.E[a] = win_start(last, n[a], g.k[a]) + g.k[a] - halo.lo[a];
+        const bool ca = g.causal[a] != 0;
+        halo.lo[a] = win_start(to[a], n[a], g.k[a], ca);
+        halo.E[a] = win_last(last, n[a], g.k[a], ca) + 1 - halo.lo[a];
     }
     halo.finish();
 
@@ -86,11 +87,13 @@ __device__ __forceinline__ void dq_role(const Geo& g, int braw, unsigned char* s
         if (wo[a] >= n[a]) wave_live = false;
         const int f = min(wo[a], n[a] - 1);
         const int l = min(wo[a] + g.WT[a], n[a]) - 1;
-        const int sf = win_start(f, n[a], g.k[a]), sl = win_start(l, n[a], g.k[a]);
+        const bool ca = g.causal[a] != 0;
+        const int sf = win_start(f, n[a], g.k[a], ca), sl = win_start(l, n[a], g.k[a], ca);
+        const int ef = win_last(f, n[a], g.k[a], ca), el = win_last(l, n[a], g.k[a], ca);
         wr.lo[a] = sf - halo.lo[a];
-        wr.hi[a] = sl + g.k[a] - halo.lo[a];
+        wr.hi[a] = el + 1 - halo.lo[a];
         wr.flo[a] = sl - halo.lo[a];
-        wr.fhi[a] = sf + g.k[a] - halo.lo[a];
+        wr.fhi[a] = ef + 1 - halo.lo[a];
     }
 
     int qs[QM][kMaxRank];
@@ -109,7 +112,7 @@ __device__ __forceinline__ void dq_role(const Geo& g, int braw, unsigned char* s
             int p = wo[a] + c[a];
             if (p >= n[a]) ok = false;
             p = min(p, n[a] - 1);
-            qs[m][a] = win_start(p, n[a], g.k[a]) - halo.lo[a];
+            qs[m][a] = mask_start(p, n[a], g.k[a], g.causal[a] != 0) - halo.lo[a];
             tok += (gc[a] + g.d[a] * p) * g.ts[a];
         }
         qvalid[m] = ok;
@@ -335,8 +338,9 @@ __device__ __forceinline__ void dkdv_role(const Geo& g, int braw, int nwk,
         to[a] = tc[a] * g.T[a];
         if (to[a] >= n[a]) return;
         const int last = min(to[a] + g.T[a], n[a]) - 1;
-        ibox.lo[a] = inv_lo(to[a], n[a], g.k[a]);
-        ibox.E[a] = inv_hi(last, n[a], g.k[a]) + 1 - ibox.lo[a];
+        const bool ca = g.causal[a] != 0;
+        ibox.lo[a] = inv_lo(to[a], n[a], g.k[a], ca);
+        ibox.E[a] = inv_hi(last, n[a], g.k[a], ca) + 1 - ibox.lo[a];
     }
     ibox.finish();
 
@@ -357,10 +361,11 @@ __device__ __forceinline__ void dkdv_role(const Geo& g, int braw, int nwk,
         if (wo[a] >= n[a]) wave_live = false;
         const int f = min(wo[a], n[a] - 1);
         const int l = min(wo[a] + g.WT[a], n[a]) - 1;
-        wr.lo[a] = inv_lo(f, n[a], g.k[a]) - ibox.lo[a];
-        wr.hi[a] = inv_hi(l, n[a], g.k[a]) + 1 - ibox.lo[a];
-        wr.flo[a] = inv_lo(l, n[a], g.k[a]) - ibox.lo[a];
-        wr.fhi[a] = inv_hi(f, n[a], g.k[a]) + 1 - ibox.lo[a];
+        const bool ca = g.causal[a] != 0;
+        wr.lo[a] = inv_lo(f, n[a], g.k[a], ca) - ibox.lo[a];
+        wr.hi[a] = inv_hi(l, n[a], g.k[a], ca) + 1 - ibox.lo[a];
+        wr.flo[a] = inv_lo(l, n[a], g.k[a], ca) - ibox.lo[a];
+        wr.fhi[a] = inv_hi(f, n[a], g.k[a], ca) + 1 - ibox.lo[a];
     }
 
     // per-lane keys: group coordinates, K and V fragments
@@ -401,8 +406,10 @@ __device__ __forceinline__ void dkdv_role(const Geo& g, int braw, int nwk,
     for (int m = 0; m < KM; ++m)
 #pragma unroll
         for (int a = 0; a < R; ++a) {
-            ilo[m][a] = inv_lo(kc[m][a], n[a], g.k[a]) - ibox.lo[a];
-            ispan[m][a] = inv_hi(kc[m][a], n[a], g.k[a]) - inv_lo(kc[m][a], n[a], g.k[a]);
+            const bool ca = g.causal[a] != 0;
+            const int lo = inv_lo(kc[m][a], n[a], g.k[a], ca);
+            ilo[m][a] = lo - ibox.lo[a];
+            ispan[m][a] = inv_hi(kc[m][a], n[a], g.k[a], ca) - lo;
         }
     // Query-box rows of at most two 16-query blocks: the inner-axis test of
     // this lane's 4 query slots is fixed, folded into 0 / -inf addends.
@@ -689,13 +696,16 @@ __global__ __launch_bounds__(256, (bwd_min_waves<D, T>())) void na_bwd_kernel(Ge
 // at most one per position, so a halo never exceeds min(T, n) + k - 1; an
 // inverse box can (every key within k - 1 of the start is attended by query
 // 0), so the tiles near a border are evaluated one by one and a single
-// interior tile (extent T + k - 1) stands for the rest.
-static int max_box_extent(int L, int d, int k, int T, bool inverse) {
+// interior tile (extent T + k - 1) stands for the rest.  Causal axes have no
+// such border growth.
+static int max_box_extent(int L, int d, int k, int T, bool causal, bool inverse) {
     int best = 0;
     const int n0 = group_len(L, d, 0);
     for (int n = n0; n >= n0 - 1; --n) {
         if (n < n0 && L % d == 0) break;  // every group has length n0
-        if (!inverse) {
+        // along a causal axis both boxes are [start(first), last] and
+        // [first, min(last + k - 1, n - 1)]: never wider than T + k - 1
+        if (!inverse || causal) {
             best = std::max(best, std::min(std::min(T, n) + k - 1, n));
             continue;
         }
@@ -704,7 +714,7 @@ static int max_box_extent(int L, int d, int k, int T, bool inverse) {
         for (int i = 0; i < nt; ++i) {
             if (i > edge && i < nt - edge) continue;
             const int to = i * T, last = std::min(to + T, n) - 1;
-            best = std::max(best, inv_hi(last, n, k) + 1 - inv_lo(to, n, k));
+            best = std::max(best, inv_hi(last, n, k, false) + 1 - inv_lo(to, n, k, false));
         }
     }
     return best;
@@ -749,8 +759,8 @@ static hipError_t launch_bwd_inst(const Geo& g, const void* q, const void* k, co
                                   void* dk, void* dv, float scale, hipStream_t stream) {
     int eq[kMaxRank], ek[kMaxRank];
     for (int a = 0; a < R; ++a) {
-        eq[a] = max_box_extent(g.L[a], g.d[a], g.k[a], g.T[a], false);
-        ek[a] = max_box_extent(g.L[a], g.d[a], g.k[a], g.T[a], true);
+        eq[a] = max_box_extent(g.L[a], g.d[a], g.k[a], g.T[a], g.causal[a] != 0, false);
+        ek[a] = max_box_extent(g.L[a], g.d[a], g.k[a], g.T[a], g.causal[a] != 0, true);
     }
     const int hq = box_blocks(eq, R), hk = box_blocks(ek, R);
     // rows of every halo (dQ) and query box (dK/dV) hold at most 2 blocks

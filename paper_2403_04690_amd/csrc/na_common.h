@@ -231,6 +231,7 @@ struct FastDiv {
 // the problem's rank are inert (extent 1, window 1, dilation 1).
 struct Geo {
     int L[kMaxRank], k[kMaxRank], d[kMaxRank];
+    int causal[kMaxRank];  // 1: causal axis (window [max(0, p - k + 1), p])
     int ts[kMaxRank];    // token stride of each axis
     int N;               // tokens per (batch, head)
     int BH;              // batch * heads
@@ -259,7 +260,8 @@ __device__ __forceinline__ void fetch_geo(const Geo& g) {
                  "s"(g.fd_ngroups.shr),
                  "s"(g.L[0]), "s"(g.k[0]), "s"(g.d[0]), "s"(g.ts[0]), "s"(g.T[0]), "s"(g.nt[0]),
                  "s"(g.lgWT[0]), "s"(g.lgWGd[0]), "s"(g.fd_d[0].mul), "s"(g.fd_d[0].shr),
-                 "s"(g.fd_nt[0].mul), "s"(g.fd_nt[0].shr),
+                 "s"(g.fd_nt[0].mul), "s"(g.fd_nt[0].shr), "s"(g.causal[0]), "s"(g.causal[r1]),
+                 "s"(g.causal[r2]),
                  "s"(g.L[r1]), "s"(g.k[r1]), "s"(g.d[r1]), "s"(g.ts[r1]), "s"(g.T[r1]),
                  "s"(g.nt[r1]), "s"(g.lgWT[r1]), "s"(g.lgWGd[r1]), "s"(g.fd_d[r1].mul),
                  "s"(g.fd_d[r1].shr), "s"(g.fd_nt[r1].mul), "s"(g.fd_nt[r1].shr),

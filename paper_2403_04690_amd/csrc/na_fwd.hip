@@ -84,8 +84,9 @@ __global__ __launch_bounds__(256) void na_fwd_kernel(Geo g, const T* __restrict_
         to[a] = tc[a] * g.T[a];
         if (to[a] >= n[a]) return;  // tile beyond this (shorter) group: uniform exit
         const int last = min(to[a] + g.T[a], n[a]) - 1;
-        halo.lo[a] = win_start(to[a], n[a], g.k[a]);
-        halo.E[a] = win_start(last, n[a], g.k[a]) + g.k[a] - halo.lo[a];
+        const bool ca = g.causal[a] != 0;
+        halo.lo[a] = win_start(to[a], n[a], g.k[a], ca);
+        halo.E[a] = win_last(last, n[a], g.k[a], ca) + 1 - halo.lo[a];
     }
     halo.finish();
 
@@ -105,11 +106,13 @@ __global__ __launch_bounds__(256) void na_fwd_kernel(Geo g, const T* __restrict_
         if (wo[a] >= n[a]) wave_live = false;
         const int f = min(wo[a], n[a] - 1);
         const int l = min(wo[a] + g.WT[a], n[a]) - 1;
-        const int sf = win_start(f, n[a], g.k[a]), sl = win_start(l, n[a], g.k[a]);
+        const bool ca = g.causal[a] != 0;
+        const int sf = win_start(f, n[a], g.k[a], ca), sl = win_start(l, n[a], g.k[a], ca);
+        const int ef = win_last(f, n[a], g.k[a], ca), el = win_last(l, n[a], g.k[a], ca);
         wr.lo[a] = sf - halo.lo[a];
-        wr.hi[a] = sl + g.k[a] - halo.lo[a];
+        wr.hi[a] = el + 1 - halo.lo[a];
         wr.flo[a] = sl - halo.lo[a];
-        wr.fhi[a] = sf + g.k[a] - halo.lo[a];
+        wr.fhi[a] = ef + 1 - halo.lo[a];
     }
 
     // ---- per-lane queries: validity, window starts (relative to the halo), Q ----
@@ -128,7 +131,7 @@ __global__ __launch_bounds__(256) void na_fwd_kernel(Geo g, const T* __restrict_
             int p = wo[a] + cc[a];
             if (p >= n[a]) ok = false;
             p = min(p, n[a] - 1);
-            qs[m][a] = win_start(p, n[a], g.k[a]) - halo.lo[a];
+            qs[m][a] = mask_start(p, n[a], g.k[a], g.causal[a] != 0) - halo.lo[a];
             tok += (gc[a] + g.d[a] * p) * g.ts[a];
         }
         qvalid[m] = ok;

@@ -5,7 +5,10 @@
 // window is centred where possible and shifted at borders so its size never
 // changes.  Dilation d partitions an axis of length L into d groups
 // (x mod d), each an independent problem over n = ceil((L - g) / d) tokens
-// (Sec. 3.4).  All functions below work in group coordinates p = x / d.
+// (Sec. 3.4).  Along a causal axis (Sec. 3.4) a query never attends to a token
+// of larger coordinate: its window is the k nearest positions not after it,
+// [max(0, p - k + 1), p], shorter than k for the first k - 1 positions.  All
+// functions below work in group coordinates p = x / d.
 #pragma once
 
 #if defined(__HIPCC__)
@@ -19,18 +22,35 @@ namespace na {
 // Tokens in dilation group g of an axis of length L.
 NA_HD int group_len(int L, int d, int g) { return (L - g + d - 1) / d; }
 
-// First window position of the query at group position p (group of n tokens,
-// window k): the window is [win_start, win_start + k).
-NA_HD int win_start(int p, int n, int k) {
+// First and last (inclusive) window positions of the query at group position
+// p (group of n tokens, window k, causal axis or not).
+NA_HD int win_start(int p, int n, int k, bool causal) {
+    if (causal) return p - k + 1 < 0 ? 0 : p - k + 1;
     int s = p - k / 2;
     s = s < 0 ? 0 : s;
     return s > n - k ? n - k : s;
 }
+NA_HD int win_last(int p, int n, int k, bool causal) {
+    return causal ? p : win_start(p, n, k, false) + k - 1;
+}
+
+// Start of the window as the kernels' mask tests use it, (unsigned)(j - s) < k:
+// along a causal axis the unclamped p - k + 1, which with j >= 0 admits exactly
+// the positions max(0, p - k + 1) .. p.
+NA_HD int mask_start(int p, int n, int k, bool causal) {
+    return causal ? p - k + 1 : win_start(p, n, k, false);
+}
 
 // Inverse neighbourhood of key position j (Sec. 3.1, operator IN): the
 // queries whose window contains j form the contiguous range [inv_lo, inv_hi],
-// because win_start is non-decreasing in p.
-NA_HD int inv_lo(int j, int n, int k) { return j <= k - 1 ? 0 : j - k + 1 + k / 2; }
-NA_HD int inv_hi(int j, int n, int k) { return j >= n - k ? n - 1 : j + k / 2; }
+// because window starts and ends are non-decreasing in p.
+NA_HD int inv_lo(int j, int n, int k, bool causal) {
+    if (causal) return j;
+    return j <= k - 1 ? 0 : j - k + 1 + k / 2;
+}
+NA_HD int inv_hi(int j, int n, int k, bool causal) {
+    if (causal) return j + k - 1 < n - 1 ? j + k - 1 : n - 1;
+    return j >= n - k ? n - 1 : j + k / 2;
+}
 
 }  // namespace na

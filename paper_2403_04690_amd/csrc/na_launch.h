@@ -19,7 +19,7 @@ hipError_t launch_backward(const Geo& g, int rank, int D, int dtype, int m, cons
                            hipStream_t s);
 
 // Per-axis window starts and inverse ranges (absolute coordinates), int32.
-hipError_t launch_debug_windows(int rank, const int* L, const int* k, const int* d, int* start,
-                                int* inv_lo, int* inv_hi, hipStream_t s);
+hipError_t launch_debug_windows(int rank, const int* L, const int* k, const int* d, const int* c,
+                                int* start, int* inv_lo, int* inv_hi, hipStream_t s);
 
 }  // namespace na

@@ -57,7 +57,7 @@ def _args(rank=2, ext=(10, 12), ks=(3, 5), ds=(2, 1)):
 
 def _validate(lib, rank=2, ext=(10, 12), ks=(3, 5), ds=(2, 1), B=2, H=3, D=64, dt=1, scale=0.125):
     r, e, k, d = _args(rank, ext, ks, ds)
-    return lib.na_validate(r, e, k, d, B, H, D, dt, scale)
+    return lib.na_validate(r, e, k, d, None, B, H, D, dt, scale)
 
 
 def test_validate_statuses(lib):
@@ -83,6 +83,15 @@ def test_validate_statuses(lib):
     assert _validate(lib, rank=1, ext=(1 << 24,), ks=(3,), ds=(1,), D=64) == NA_OK
 
 
+def test_validate_accepts_causal_flags(lib):
+    r, e, k, d = _args()
+    c = (ctypes.c_int32 * 2)(1, 0)
+    assert lib.na_validate(r, e, k, d, c, 2, 3, 64, 1, 0.125) == NA_OK
+    # the usual window rule still applies on a causal axis
+    r, e, k, d = _args(ks=(6, 5))
+    assert lib.na_validate(r, e, k, d, c, 2, 3, 64, 1, 0.125) == NA_ERR_WINDOW
+
+
 def test_status_strings(lib):
     for s in list(range(10)) + [11, 12]:
         text = lib.na_status_string(s).decode()
@@ -98,7 +107,7 @@ FAKE = 0x10000  # aligned, never dereferenced: validation fails first
 def _fwd(lib, ptrs, **kw):
     r, e, k, d = _args()
     B, H, D = kw.get("B", 2), kw.get("H", 3), kw.get("D", 64)
-    return lib.na_forward(r, e, k, d, B, H, D, 1, 0.125, *ptrs, None)
+    return lib.na_forward(r, e, k, d, None, B, H, D, 1, 0.125, *ptrs, None)
 
 
 def test_forward_rejects_before_launch(lib):
@@ -116,18 +125,18 @@ def test_forward_rejects_before_launch(lib):
 def test_backward_rejects_before_launch(lib):
     r, e, k, d = _args()
     ptrs = [FAKE] * 9
-    bwd = lambda p, B=2: lib.na_backward(r, e, k, d, B, 3, 64, 1, 0.125, *p, None)
+    bwd = lambda p, B=2: lib.na_backward(r, e, k, d, None, B, 3, 64, 1, 0.125, *p, None)
     assert bwd([None] + ptrs[1:]) == NA_ERR_NULL
     assert bwd(ptrs[:8] + [None]) == NA_ERR_NULL
     assert bwd(ptrs[:8] + [FAKE + 1]) == NA_ERR_ALIGNMENT
     assert bwd([FAKE + 8] + ptrs[1:]) == NA_ERR_ALIGNMENT
     assert bwd([None] * 9, B=0) == NA_OK
-    bad_rank = lib.na_backward(0, e, k, d, 2, 3, 64, 1, 0.125, *ptrs, None)
+    bad_rank = lib.na_backward(0, e, k, d, None, 2, 3, 64, 1, 0.125, *ptrs, None)
     assert bad_rank == NA_ERR_RANK
 
 
 def test_debug_windows_rejects_before_launch(lib):
     r, e, k, d = _args(ks=(6, 5))
-    assert lib.na_debug_windows(r, e, k, d, FAKE, FAKE, FAKE, None) == NA_ERR_WINDOW
+    assert lib.na_debug_windows(r, e, k, d, None, FAKE, FAKE, FAKE, None) == NA_ERR_WINDOW
     r, e, k, d = _args()
-    assert lib.na_debug_windows(r, e, k, d, None, FAKE, FAKE, None) == NA_ERR_NULL
+    assert lib.na_debug_windows(r, e, k, d, None, None, FAKE, FAKE, None) == NA_ERR_NULL

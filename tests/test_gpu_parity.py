@@ -232,16 +232,18 @@ def test_full_workload_forward(na, name):
     p = workloads.CONFIGS[name]
     _log(f"[full fwd] {p.describe()}")
     x = workloads.make_inputs(p, seed=0, with_grad=False)
+    cz = p.causal_axes
     out, lse = na.forward(*_dev(x["q"], x["k"], x["v"]), p.kernel_size, p.dilation,
-                          p.softmax_scale)
+                          p.softmax_scale, causal=cz)
     torch.cuda.synchronize()
     qd, kd, vd = (_f64(x[n]) for n in ("q", "k", "v"))
     if p.tokens * p.batch * p.heads * p.window <= 4_000_000:
-        ro, rl = oracle.forward(qd, kd, vd, p.kernel_size, p.dilation, p.softmax_scale)
+        ro, rl = oracle.forward(qd, kd, vd, p.kernel_size, p.dilation, p.softmax_scale, causal=cz)
         eo, el = _maxerr(out, ro), _maxerr(lse, rl)
     else:
         rows = _border_rows(p, 1536, seed=3)
-        ro, rl = oracle.forward_rows(qd, kd, vd, p.kernel_size, p.dilation, p.softmax_scale, rows)
+        ro, rl = oracle.forward_rows(qd, kd, vd, p.kernel_size, p.dilation, p.softmax_scale, rows,
+                                     causal=cz)
         eo = float(np.max(np.abs(_f64(out).reshape(-1, p.head_dim)[rows] - ro)))
         el = float(np.max(np.abs(_f64(lse).reshape(-1)[rows] - rl)))
     _log(f"[full fwd] {name}: max|dO|={eo:.3g} max|dLSE|={el:.3g}")
@@ -255,16 +257,94 @@ def test_full_workload_backward(na, name):
     _log(f"[full bwd] {p.describe()}")
     x = workloads.make_inputs(p, seed=0, with_grad=True)
     q, k, v, g = _dev(x["q"], x["k"], x["v"], x["dout"])
-    out, lse = na.forward(q, k, v, p.kernel_size, p.dilation, p.softmax_scale)
-    dq, dk, dv = na.backward(q, k, v, out, lse, g, p.kernel_size, p.dilation, p.softmax_scale)
+    cz = p.causal_axes
+    out, lse = na.forward(q, k, v, p.kernel_size, p.dilation, p.softmax_scale, causal=cz)
+    dq, dk, dv = na.backward(q, k, v, out, lse, g, p.kernel_size, p.dilation, p.softmax_scale,
+                             causal=cz)
     torch.cuda.synchronize()
     qrows = _border_rows(p, 384, seed=4)
     krows = _border_rows(p, 96, seed=5)
     rq, rk, rv = oracle.backward_rows(*(_f64(x[n]) for n in ("q", "k", "v", "dout")),
-                                      p.kernel_size, p.dilation, p.softmax_scale, qrows, krows)
+                                      p.kernel_size, p.dilation, p.softmax_scale, qrows, krows,
+                                      causal=cz)
     D = p.head_dim
     e = [float(np.max(np.abs(_f64(dq).reshape(-1, D)[qrows] - rq))),
          float(np.max(np.abs(_f64(dk).reshape(-1, D)[krows] - rk))),
          float(np.max(np.abs(_f64(dv).reshape(-1, D)[krows] - rv)))]
     _log(f"[full bwd] {name}: max err dq/dk/dv = {e}")
     assert max(e) <= TOL[p.dtype]
+
+
+# ---------------------------------------------------------------- causal axes
+CAUSAL_WINDOWS = [
+    ((40,), (7,), (1,), (1,)), ((37,), (4,), (3,), (1,)), ((16, 64, 64), (7, 7, 7), (1, 2, 2), (1, 0, 0)),
+    ((10, 9), (3, 2), (3, 4), (1, 1)),
+]
+
+
+@pytest.mark.parametrize("ext,ks,ds,cs", CAUSAL_WINDOWS)
+def test_causal_debug_windows_bit_exact(na, ext, ks, ds, cs):
+    start, ilo, ihi = (t.cpu().numpy() for t in na.debug_windows(ext, ks, ds, causal=cs))
+    off = 0
+    for a, L in enumerate(ext):
+        first, lo, hi, _ = oracle.axis_relation(L, ks[a], ds[a], causal=bool(cs[a]))
+        np.testing.assert_array_equal(start[off:off + L], first)
+        np.testing.assert_array_equal(ilo[off:off + L], lo)
+        np.testing.assert_array_equal(ihi[off:off + L], hi)
+        off += L
+
+
+@pytest.mark.parametrize("ext,ks,ds,cs,dtype", [
+    ((70,), (9,), (1,), (1,), "fp16"), ((21, 26), (5, 3), (2, 3), (1, 0), "fp16"),
+    ((6, 9, 10), (3, 5, 3), (2, 1, 3), (1, 0, 1), "bf16"), ((60,), (7,), (2,), (1,), "fp32"),
+])
+def test_causal_neighbour_support_probe(na, ext, ks, ds, cs, dtype):
+    """Q = 0: P uniform on N(i), so one-hot V rows expose the causal N(i) exactly."""
+    D = 32
+    N = int(np.prod(ext))
+    lists = bf.neighbours(ext, ks, ds, [bool(c) for c in cs])
+    q = torch.zeros((1, 1) + ext + (D,), dtype=TDT[dtype])
+    k = _inputs(q.shape, dtype, 5, 1)[0]
+    for chunk in range((N + D - 1) // D):
+        v = torch.zeros(1, 1, N, D)
+        for c in range(D):
+            if chunk * D + c < N:
+                v[0, 0, chunk * D + c, c] = 1.0
+        v = v.reshape(q.shape).to(TDT[dtype])
+        out, lse = na.forward(*_dev(q, k, v), ks, ds, causal=cs)
+        o = out.float().cpu().reshape(N, D).numpy()
+        for i in range(N):
+            want = set(t - chunk * D for t in lists[i] if chunk * D <= t < (chunk + 1) * D)
+            assert set(np.nonzero(o[i])[0].tolist()) == want, (i, chunk)
+        sizes = np.array([math.log(len(r)) for r in lists]).reshape(lse.shape[2:])
+        np.testing.assert_allclose(lse.cpu().numpy()[0, 0], sizes, atol=1e-5)
+
+
+CAUSAL_CASES = [
+    # (extents, kernel, dilation, causal, head_dim, dtype, batch, heads)
+    ((200,), (7,), (1,), (1,), 32, "fp32", 1, 2),
+    ((300,), (13,), (3,), (1,), 64, "fp16", 1, 2),
+    ((1000,), (255,), (2,), (1,), 64, "bf16", 1, 1),
+    ((37, 45), (7, 5), (2, 1), (1, 0), 32, "fp16", 1, 2),
+    ((20, 23), (3, 3), (3, 2), (0, 1), 64, "bf16", 1, 2),
+    ((33, 31), (13, 13), (2, 2), (1, 1), 64, "bf16", 1, 1),
+    ((9, 50), (9, 25), (1, 2), (0, 1), 128, "fp16", 1, 1),
+    ((6, 20, 22), (3, 7, 5), (1, 2, 2), (1, 0, 0), 64, "fp16", 1, 1),
+    ((8, 12, 12), (7, 7, 7), (1, 1, 1), (1, 0, 0), 32, "fp16", 1, 2),
+    ((5, 9, 11), (5, 3, 3), (1, 3, 3), (1, 1, 1), 32, "fp32", 1, 1),
+]
+
+
+@pytest.mark.parametrize("ext,ks,ds,cs,D,dtype,B,H", CAUSAL_CASES)
+def test_causal_forward_and_backward_small(na, ext, ks, ds, cs, D, dtype, B, H):
+    shape = (B, H) + ext + (D,)
+    q, k, v, g = _inputs(shape, dtype, 31, 4)
+    dq_, dk_, dv_, dg_ = _dev(q, k, v, g)
+    out, lse = na.forward(dq_, dk_, dv_, ks, ds, causal=cs)
+    dq, dk, dv = na.backward(dq_, dk_, dv_, out, lse, dg_, ks, ds, causal=cs)
+    sc = 1.0 / math.sqrt(D)
+    ro, rl = oracle.forward(_f64(q), _f64(k), _f64(v), ks, ds, sc, causal=cs)
+    rq, rk, rv = oracle.backward(_f64(q), _f64(k), _f64(v), _f64(g), ks, ds, sc, causal=cs)
+    e = [_maxerr(out, ro), _maxerr(lse, rl), _maxerr(dq, rq), _maxerr(dk, rk), _maxerr(dv, rv)]
+    _log(f"causal {ext} k={ks} d={ds} c={cs} D={D} {dtype}: max err o/lse/dq/dk/dv = {e}")
+    assert max(e) <= TOL[dtype]

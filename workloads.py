@@ -6,7 +6,8 @@ method's arithmetic: it only draws iid N(0, 1) tensors and rounds them to the
 working dtype.
 
 Recipe (the paper benchmarks random tensors of many shapes, Sec. 4; its sweep
-sizes are not published, so these five problems stand in for it):
+sizes are not published, so these five problems, plus a causal-time variant
+of the 3-D one, stand in for it):
   * torch.randn on a CPU generator seeded with ``seed`` (0 by default),
     drawn in the order q, k, v, dO, each fp32 with shape [B, H, X_1..X_r, D];
   * then cast to the working dtype with round-to-nearest-even;
@@ -31,6 +32,7 @@ class Problem:
     dtype: str  # "fp32" | "fp16" | "bf16"
     backward: bool = False
     scale: float = field(default=None)
+    causal: Tuple[bool, ...] = field(default=None)  # per axis; None: no causal axis
 
     @property
     def rank(self):
@@ -45,6 +47,22 @@ class Problem:
         return int(math.prod(self.kernel_size))
 
     @property
+    def causal_axes(self):
+        return tuple(bool(c) for c in self.causal) if self.causal else (False,) * self.rank
+
+    def pairs_per_slice(self):
+        """Query-neighbour pairs of one (batch, head): N * ell without causal axes.
+
+        The neighbourhood is a product of per-axis windows, so the count is a
+        product of per-axis sums; along a causal axis position p of a group
+        has min(k, p + 1) neighbours.
+        """
+        total = 1
+        for L, k, d, c in zip(self.extents, self.kernel_size, self.dilation, self.causal_axes):
+            total *= sum(min(k, x // d + 1) for x in range(L)) if c else L * k
+        return total
+
+    @property
     def softmax_scale(self):
         return self.scale if self.scale is not None else 1.0 / math.sqrt(self.head_dim)
 
@@ -57,12 +75,13 @@ class Problem:
         return 4 if self.dtype == "fp32" else 2
 
     def fwd_flops(self):
-        """Useful forward FLOPs: 4 * B * H * N * ell * D (unmasked neighbourhood work only)."""
-        return 4 * self.batch * self.heads * self.tokens * self.window * self.head_dim
+        """Useful forward FLOPs: 4 * D per query-neighbour pair, i.e. 4 * B * H * N * ell * D
+        without causal axes (unmasked neighbourhood work only)."""
+        return 4 * self.batch * self.heads * self.pairs_per_slice() * self.head_dim
 
     def bwd_flops(self):
-        """Useful backward FLOPs: 10 * B * H * N * ell * D (S, dP, dV, dQ, dK contractions)."""
-        return 10 * self.batch * self.heads * self.tokens * self.window * self.head_dim
+        """Useful backward FLOPs: 10 * D per pair (S, dP, dV, dQ, dK contractions)."""
+        return 10 * self.batch * self.heads * self.pairs_per_slice() * self.head_dim
 
     def fwd_bytes(self):
         """Algorithmic forward HBM bytes: read q, k, v; write out and fp32 logsumexp."""
@@ -78,8 +97,10 @@ class Problem:
         ext = "x".join(str(e) for e in self.extents)
         ks = "x".join(str(k) for k in self.kernel_size)
         ds = "x".join(str(d) for d in self.dilation)
+        cs = "".join("c" if c else "-" for c in self.causal_axes)
         return (f"{self.rank}-D NA {'fwd+bwd' if self.backward else 'fwd'} {self.dtype}: "
-                f"B={self.batch} H={self.heads} X={ext} D={self.head_dim} k={ks} d={ds}")
+                f"B={self.batch} H={self.heads} X={ext} D={self.head_dim} k={ks} d={ds}"
+                + (f" causal={cs}" if any(self.causal_axes) else ""))
 
 
 # The five workloads: shapes, windows and dilations of the paper's 1-D, 2-D and
@@ -93,6 +114,11 @@ CONFIGS = {
                                        (4,), "fp16"),
     "3d_fp16_16x64x64_k7_d122": Problem("3d_fp16_16x64x64_k7_d122", 1, 8, (16, 64, 64), 64,
                                         (7, 7, 7), (1, 2, 2), "fp16", backward=True),
+    # the same volume with causal masking along time (T), the spatio-temporal
+    # use of causal NA that Sec. 3.4 names
+    "3d_fp16_16x64x64_k7_d122_causal_t": Problem(
+        "3d_fp16_16x64x64_k7_d122_causal_t", 1, 8, (16, 64, 64), 64, (7, 7, 7), (1, 2, 2), "fp16",
+        backward=True, causal=(True, False, False)),
 }
 CONFIG_ORDER = list(CONFIGS)
 # The workload the benchmark times (forward and backward): 2-D 7x7 fp16.
