@@ -348,3 +348,59 @@ def test_causal_forward_and_backward_small(na, ext, ks, ds, cs, D, dtype, B, H):
     e = [_maxerr(out, ro), _maxerr(lse, rl), _maxerr(dq, rq), _maxerr(dk, rk), _maxerr(dv, rv)]
     _log(f"causal {ext} k={ks} d={ds} c={cs} D={D} {dtype}: max err o/lse/dq/dk/dv = {e}")
     assert max(e) <= TOL[dtype]
+
+
+# ---------------------------------------------------------------- maximum sizes
+def _gpu_inputs(shape, dtype, seed, n):
+    """Seeded synthetic inputs drawn on the GPU (the tensors are too large to stage from the host)."""
+    gen = torch.Generator(device="cuda").manual_seed(seed)
+    return [torch.randn(shape, generator=gen, device="cuda", dtype=torch.float32).to(TDT[dtype])
+            for _ in range(n)]
+
+
+def test_max_grid_many_slices(na):
+    """65,536 (batch, head) slices, 2 GiB per tensor: 64-bit slice offsets and a large grid.
+    Each slice is an independent problem, so sampled slices are checked alone."""
+    B, H, L, D, ks, ds = 256, 256, 256, 64, (7,), (2,)
+    q, k, v, g = _gpu_inputs((B, H, L, D), "fp16", 71, 4)
+    out, lse = na.forward(q, k, v, ks, ds)
+    dq, dk, dv = na.backward(q, k, v, out, lse, g, ks, ds)
+    torch.cuda.synchronize()
+    sc = 1.0 / math.sqrt(D)
+    for b, h in [(0, 0), (B - 1, H - 1), (17, 200), (128, 3), (255, 0)]:
+        sl = lambda t: _f64(t[b:b + 1, h:h + 1])
+        ro, rl = oracle.forward(sl(q), sl(k), sl(v), ks, ds, sc)
+        rq, rk, rv = oracle.backward(sl(q), sl(k), sl(v), sl(g), ks, ds, sc)
+        e = [float(np.max(np.abs(sl(a) - r))) for a, r in
+             ((out, ro), (lse, rl), (dq, rq), (dk, rk), (dv, rv))]
+        _log(f"max grid slice ({b},{h}): max err o/lse/dq/dk/dv = {e}")
+        assert max(e) <= TOL["fp16"]
+    del q, k, v, g, out, lse, dq, dk, dv
+    torch.cuda.empty_cache()
+
+
+def test_max_tokens_times_head_dim(na):
+    """One 1-D slice with N * D = 2^30 (the 32-bit token-offset limit is 2^31): the rows of
+    sampled queries and keys are checked on sub-sequences large enough that their windows and
+    inverse neighbourhoods are those of the full sequence (anchored at the true borders)."""
+    L, D, kk = 1 << 24, 64, 9
+    q, k, v, g = _gpu_inputs((1, 1, L, D), "fp16", 72, 4)
+    out, lse = na.forward(q, k, v, (kk,), (1,))
+    dq, dk, dv = na.backward(q, k, v, out, lse, g, (kk,), (1,))
+    torch.cuda.synchronize()
+    sc = 1.0 / math.sqrt(D)
+    margin = 3 * kk
+    for x in [0, 3, 4099, L // 2 + 1, L - 5, L - 1]:
+        lo, hi = max(0, x - margin), min(L, x + margin + 1)
+        sub = lambda t: _f64(t[:, :, lo:hi])
+        ro, rl = oracle.forward(sub(q), sub(k), sub(v), (kk,), (1,), sc)
+        rq, rk, rv = oracle.backward(sub(q), sub(k), sub(v), sub(g), (kk,), (1,), sc)
+        i = x - lo
+        at = lambda t: _f64(t[0, 0, x])
+        e = [float(np.max(np.abs(at(out) - ro[0, 0, i]))), abs(float(lse[0, 0, x]) - rl[0, 0, i]),
+             float(np.max(np.abs(at(dq) - rq[0, 0, i]))), float(np.max(np.abs(at(dk) - rk[0, 0, i]))),
+             float(np.max(np.abs(at(dv) - rv[0, 0, i])))]
+        _log(f"max N*D row {x}: max err o/lse/dq/dk/dv = {e}")
+        assert max(e) <= TOL["fp16"]
+    del q, k, v, g, out, lse, dq, dk, dv
+    torch.cuda.empty_cache()
