@@ -250,9 +250,9 @@ def test_full_workload_forward(na, name):
     assert eo <= TOL[p.dtype] and el <= TOL[p.dtype]
 
 
-@pytest.mark.parametrize("name", [n for n in workloads.CONFIG_ORDER
-                                  if workloads.CONFIGS[n].backward or n == workloads.BENCH_WORKLOAD])
+@pytest.mark.parametrize("name", workloads.CONFIG_ORDER)
 def test_full_workload_backward(na, name):
+    """Every workload's backward at full size (bench.py times the backward of any of them)."""
     p = workloads.CONFIGS[name]
     _log(f"[full bwd] {p.describe()}")
     x = workloads.make_inputs(p, seed=0, with_grad=True)
