@@ -149,6 +149,9 @@ __device__ __forceinline__ void dq_role(const Geo& g, int braw, unsigned char* s
     // Halo rows of at most two 16-key blocks: the inner-axis test of this
     // lane's 4 key slots is fixed, folded with -lse2 into per-slot addends.
     constexpr bool short_rows = SHORT != 0 && R > 1;
+    // Score addends folded into the accumulators (not for D = 128 or bf16,
+    // as in the forward)
+    constexpr bool kFoldAdd = D <= 64 && !std::is_same_v<T, __bf16>;
     float ain[QM][2][4];
 #pragma unroll
     for (int m = 0; m < QM; ++m)
@@ -175,6 +178,14 @@ __device__ __forceinline__ void dq_role(const Geo& g, int braw, unsigned char* s
     }
     wait_vmem();
     __syncthreads();
+    // kFoldAdd: Q scaled once by c = scale*log2(e) and rounded to T
+    if constexpr (kFoldAdd)
+#pragma unroll
+    for (int m = 0; m < QM; ++m)
+#pragma unroll
+        for (int st = 0; st < C::kKS; ++st)
+#pragma unroll
+            for (int j = 0; j < 8; ++j) qf[m][st][j] = Tr<T>::cvt((float)qf[m][st][j] * scale_log2);
 
     for (int s = 0; s < nst; ++s) {
         if (s + 1 < nst) issue_stage(s + 1, (s + 1) & 1);
@@ -205,8 +216,29 @@ __device__ __forceinline__ void dq_role(const Geo& g, int braw, unsigned char* s
                     for (int a = 0; a < R - 1; ++a) boc[bi][a] = __builtin_amdgcn_readlane(loc[a], j);
                 }
 
-                // S^T = K Q^T and dP^T - Delta = V dO^T - Delta (the accumulator
-                // starts at -Delta of the lane's query)
+                // Y^T = c K Q^T + A (A: -lse2 on valid pairs, -inf on masked; with
+                // kFoldAdd the accumulator starts at A and Q is prescaled by c) and
+                // dP^T - Delta = V dO^T - Delta (the accumulator starts at -Delta)
+                auto score_addend = [&](int m, int bi) {
+                    f32x4 add;
+                    if (!short_rows && full[bi]) {
+                        add = f32x4{-lse2[m], -lse2[m], -lse2[m], -lse2[m]};
+                    } else {
+                        bool outer_ok = rel[bi];
+#pragma unroll
+                        for (int a = 0; a < R - 1; ++a)
+                            outer_ok =
+                                outer_ok && (unsigned)(boc[bi][a] - qs[m][a]) < (unsigned)g.k[a];
+                        // generic rows: slot r is valid when base + r lies in [0, lim)
+                        const int base = bin0[bi] + grp * 4 - qs[m][R - 1];
+                        const unsigned lim = outer_ok ? (unsigned)g.k[R - 1] : 0u;
+#pragma unroll
+                        for (int r = 0; r < 4; ++r)
+                            add[r] = short_rows ? (outer_ok ? ain[m][bi][r] : -INFINITY)
+                                     : (unsigned)(base + r) < lim ? -lse2[m] : -INFINITY;
+                    }
+                    return add;
+                };
                 f32x4 sacc[QM][2], pacc[QM][2];
 #pragma unroll
                 for (int bi = 0; bi < 2; ++bi) {
@@ -218,45 +250,39 @@ __device__ __forceinline__ void dq_role(const Geo& g, int braw, unsigned char* s
                             const x8 vf = rfr.read(vs + boff, st);
 #pragma unroll
                             for (int m = 0; m < QM; ++m) {
-                                const f32x4 z = f32x4{0.f, 0.f, 0.f, 0.f};
+                                f32x4 s0 = f32x4{0.f, 0.f, 0.f, 0.f};
+                                if constexpr (kFoldAdd)
+                                    if (st == 0) s0 = score_addend(m, bi);
                                 const f32x4 nd = f32x4{-dlt[m], -dlt[m], -dlt[m], -dlt[m]};
-                                sacc[m][bi] = Tr<T>::mma(kf, qf[m][st], st == 0 ? z : sacc[m][bi]);
+                                sacc[m][bi] = Tr<T>::mma(kf, qf[m][st], st == 0 ? s0 : sacc[m][bi]);
                                 pacc[m][bi] = Tr<T>::mma(vf, gf[m][st], st == 0 ? nd : pacc[m][bi]);
                             }
                         }
                     } else {
 #pragma unroll
                         for (int m = 0; m < QM; ++m) {
-                            sacc[m][bi] = f32x4{0.f, 0.f, 0.f, 0.f};
+                            const float s0 = kFoldAdd ? -INFINITY : 0.f;
+                            sacc[m][bi] = f32x4{s0, s0, s0, s0};
                             pacc[m][bi] = f32x4{0.f, 0.f, 0.f, 0.f};
                         }
                     }
                 }
 
-                // dA^T = P^T (dP^T - Delta), P = exp2(scale*log2(e)*s - lse2) on valid pairs
+                // dA^T = P^T (dP^T - Delta), P = exp2(Y^T)
                 x8 dsf[QM];
 #pragma unroll
                 for (int m = 0; m < QM; ++m) {
                     float ds[2][4];
 #pragma unroll
                     for (int bi = 0; bi < 2; ++bi) {
-                        bool outer_ok = rel[bi];
+                        f32x4 y = sacc[m][bi];
+                        if constexpr (!kFoldAdd) {
+                            const f32x4 add = score_addend(m, bi);
 #pragma unroll
-                        for (int a = 0; a < R - 1; ++a)
-                            outer_ok = outer_ok && (unsigned)(boc[bi][a] - qs[m][a]) < (unsigned)g.k[a];
-                        // generic rows: slot r is valid when base + r lies in [0, lim)
-                        const int base = full[bi] ? 0 : bin0[bi] + grp * 4 - qs[m][R - 1];
-                        const unsigned lim = full[bi] ? 4u : outer_ok ? (unsigned)g.k[R - 1] : 0u;
-#pragma unroll
-                        for (int r = 0; r < 4; ++r) {
-                            float add;
-                            if (short_rows)
-                                add = outer_ok ? ain[m][bi][r] : -INFINITY;
-                            else
-                                add = (unsigned)(base + r) < lim ? -lse2[m] : -INFINITY;
-                            const float p = fast_exp2(fmaf(sacc[m][bi][r], scale_log2, add));
-                            ds[bi][r] = p * pacc[m][bi][r];
+                            for (int r = 0; r < 4; ++r) y[r] = fmaf(y[r], scale_log2, add[r]);
                         }
+#pragma unroll
+                        for (int r = 0; r < 4; ++r) ds[bi][r] = fast_exp2(y[r]) * pacc[m][bi][r];
                     }
                     dsf[m] = x8{Tr<T>::cvt(ds[0][0]), Tr<T>::cvt(ds[0][1]), Tr<T>::cvt(ds[0][2]),
                                 Tr<T>::cvt(ds[0][3]), Tr<T>::cvt(ds[1][0]), Tr<T>::cvt(ds[1][1]),
@@ -414,6 +440,9 @@ __device__ __forceinline__ void dkdv_role(const Geo& g, int braw, int nwk,
     // Query-box rows of at most two 16-query blocks: the inner-axis test of
     // this lane's 4 query slots is fixed, folded into 0 / -inf addends.
     constexpr bool short_rows = SHORT != 0 && R > 1;
+    // Score addends folded into the accumulators (not for D = 128 or bf16,
+    // as in the forward)
+    constexpr bool kFoldAdd = D <= 64 && !std::is_same_v<T, __bf16>;
     float ain[KM][2][4];
 #pragma unroll
     for (int m = 0; m < KM; ++m)
@@ -516,6 +545,14 @@ __device__ __forceinline__ void dkdv_role(const Geo& g, int braw, int nwk,
     wait_vmem();
     __syncthreads();
     delta_pass(0);
+    // kFoldAdd: K scaled once by c = scale*log2(e) and rounded to T
+    if constexpr (kFoldAdd)
+#pragma unroll
+    for (int m = 0; m < KM; ++m)
+#pragma unroll
+        for (int st = 0; st < C::kKS; ++st)
+#pragma unroll
+            for (int j = 0; j < 8; ++j) kf[m][st][j] = Tr<T>::cvt((float)kf[m][st][j] * scale_log2);
     __syncthreads();
 
     for (int s = 0; s < nst; ++s) {
@@ -558,8 +595,30 @@ __device__ __forceinline__ void dkdv_role(const Geo& g, int braw, int nwk,
                     ndl[bi] = ld16<f32x4>(dls + srow);
                 }
 
-                // S = Q K^T and dP - Delta = dO V^T - Delta (rows: queries,
-                // columns: this wave's keys; the accumulator starts at -Delta)
+                // Y = c Q K^T + A (A: -lse2 on valid pairs, -inf on masked; with
+                // kFoldAdd the accumulator starts at A and K is prescaled by c) and
+                // dP - Delta = dO V^T - Delta (rows: queries, columns: this wave's
+                // keys; the accumulator starts at -Delta)
+                auto score_addend = [&](int m, int bi) {
+                    f32x4 add;
+                    if (!short_rows && full[bi]) {
+                        add = nlse[bi];
+                    } else {
+                        bool outer_ok = rel[bi];
+#pragma unroll
+                        for (int a = 0; a < R - 1; ++a)
+                            outer_ok = outer_ok && (unsigned)(boc[bi][a] - ilo[m][a]) <=
+                                                       (unsigned)ispan[m][a];
+                        // generic rows: slot r is valid when base + r lies in [0, lim)
+                        const int base = bin0[bi] + grp * 4 - ilo[m][R - 1];
+                        const unsigned lim = outer_ok ? (unsigned)ispan[m][R - 1] + 1u : 0u;
+#pragma unroll
+                        for (int r = 0; r < 4; ++r)
+                            add[r] = short_rows ? (outer_ok ? nlse[bi][r] + ain[m][bi][r] : -INFINITY)
+                                     : (unsigned)(base + r) < lim ? nlse[bi][r] : -INFINITY;
+                    }
+                    return add;
+                };
                 f32x4 sacc[KM][2], pacc[KM][2];
 #pragma unroll
                 for (int bi = 0; bi < 2; ++bi) {
@@ -571,44 +630,39 @@ __device__ __forceinline__ void dkdv_role(const Geo& g, int braw, int nwk,
                             const x8 ga = rfr.read(gs + boff, st);
 #pragma unroll
                             for (int m = 0; m < KM; ++m) {
-                                const f32x4 z = f32x4{0.f, 0.f, 0.f, 0.f};
-                                sacc[m][bi] = Tr<T>::mma(qa, kf[m][st], st == 0 ? z : sacc[m][bi]);
+                                f32x4 s0 = f32x4{0.f, 0.f, 0.f, 0.f};
+                                if constexpr (kFoldAdd)
+                                    if (st == 0) s0 = score_addend(m, bi);
+                                sacc[m][bi] = Tr<T>::mma(qa, kf[m][st], st == 0 ? s0 : sacc[m][bi]);
                                 pacc[m][bi] = Tr<T>::mma(ga, vf[m][st], st == 0 ? ndl[bi] : pacc[m][bi]);
                             }
                         }
                     } else {
 #pragma unroll
                         for (int m = 0; m < KM; ++m) {
-                            sacc[m][bi] = f32x4{0.f, 0.f, 0.f, 0.f};
+                            const float s0 = kFoldAdd ? -INFINITY : 0.f;
+                            sacc[m][bi] = f32x4{s0, s0, s0, s0};
                             pacc[m][bi] = f32x4{0.f, 0.f, 0.f, 0.f};
                         }
                     }
                 }
 
-                // P = exp2(scale*log2(e)*s - lse2) on valid pairs, dA = P (dP - Delta)
+                // P = exp2(Y), dA = P (dP - Delta)
                 x8 pf[KM], dsf[KM];
 #pragma unroll
                 for (int m = 0; m < KM; ++m) {
                     float p[2][4], ds[2][4];
 #pragma unroll
                     for (int bi = 0; bi < 2; ++bi) {
-                        bool outer_ok = rel[bi];
+                        f32x4 y = sacc[m][bi];
+                        if constexpr (!kFoldAdd) {
+                            const f32x4 add = score_addend(m, bi);
 #pragma unroll
-                        for (int a = 0; a < R - 1; ++a)
-                            outer_ok = outer_ok &&
-                                       (unsigned)(boc[bi][a] - ilo[m][a]) <= (unsigned)ispan[m][a];
-                        // generic rows: slot r is valid when base + r lies in [0, lim)
-                        const int base = full[bi] ? 0 : bin0[bi] + grp * 4 - ilo[m][R - 1];
-                        const unsigned lim =
-                            full[bi] ? 4u : outer_ok ? (unsigned)ispan[m][R - 1] + 1u : 0u;
+                            for (int r = 0; r < 4; ++r) y[r] = fmaf(y[r], scale_log2, add[r]);
+                        }
 #pragma unroll
                         for (int r = 0; r < 4; ++r) {
-                            float add;
-                            if (short_rows)
-                                add = outer_ok ? nlse[bi][r] + ain[m][bi][r] : -INFINITY;
-                            else
-                                add = (unsigned)(base + r) < lim ? nlse[bi][r] : -INFINITY;
-                            const float pv = fast_exp2(fmaf(sacc[m][bi][r], scale_log2, add));
+                            const float pv = fast_exp2(y[r]);
                             p[bi][r] = pv;
                             ds[bi][r] = pv * pacc[m][bi][r];
                         }

@@ -157,12 +157,16 @@ __global__ __launch_bounds__(256) void na_fwd_kernel(Geo g, const T* __restrict_
 
     // ---- online-softmax state (per lane: its query column) ----
     // mref: running reference (base 2, -inf until the row sees a key);
-    // negm = -mref (0 while mref = -inf) is the scores' FMA addend and thr the
+    // negm = -mref (0 while mref = -inf) is the scores' addend and thr the
     // score above which the reference must be raised.
     // Row sums: with kMfmaSum, lsum[m] accumulates ones^T P^T on the matrix
     // cores (every entry is the row sum); otherwise each lane sums its share
     // of P in lrow[m], reduced across the four lane groups at the end.
     constexpr bool kMfmaSum = sizeof(T) == 2 && QM == 1;
+    // Score addends folded into the accumulators.  Not for D = 128 (the
+    // addend vectors would cost it occupancy) nor bf16 (rounding c*Q to 8
+    // mantissa bits would add an error comparable to that of P itself).
+    constexpr bool kFoldAdd = D <= 64 && !std::is_same_v<T, __bf16>;
     x8 ones;
 #pragma unroll
     for (int j = 0; j < 8; ++j) ones[j] = (T)1.0f;
@@ -205,6 +209,16 @@ __global__ __launch_bounds__(256) void na_fwd_kernel(Geo g, const T* __restrict_
     issue_stage(0, 0);
     wait_vmem();
     __syncthreads();
+    // kFoldAdd: Q scaled once by c = scale*log2(e) and rounded to T, so the
+    // matrix cores produce base-2 scores (after the wait: the loads above are
+    // in flight together)
+    if constexpr (kFoldAdd)
+#pragma unroll
+    for (int m = 0; m < QM; ++m)
+#pragma unroll
+        for (int st = 0; st < C::kKS; ++st)
+#pragma unroll
+            for (int j = 0; j < 8; ++j) qf[m][st][j] = Tr<T>::cvt((float)qf[m][st][j] * c);
 
     for (int s = 0; s < nst; ++s) {
         if (s + 1 < nst) issue_stage(s + 1, (s + 1) & 1);
@@ -257,58 +271,59 @@ __global__ __launch_bounds__(256) void na_fwd_kernel(Geo g, const T* __restrict_
                         vf[db] = vfr.read(vs + tp * 32 * kRowB, db, lane);
                 };
                 if (kEarlyV) read_v();
+                // ---- Y^T = c K Q^T + A, A the addend: -m on valid pairs, -inf on masked ----
+                // (base 2, relative to the running reference m).  With kFoldAdd the
+                // accumulator starts at A and Q is prescaled, so the matrix cores
+                // produce Y; otherwise one FMA per score applies c and A.
+                auto score_addend = [&](int m, int bi) {
+                    f32x4 add;
+                    if (!short_rows && full[bi]) {
+                        add = f32x4{negm[m], negm[m], negm[m], negm[m]};
+                    } else {
+                        bool outer_ok = rel[bi];
+#pragma unroll
+                        for (int a = 0; a < R - 1; ++a)
+                            outer_ok =
+                                outer_ok && (unsigned)(boc[bi][a] - qs[m][a]) < (unsigned)g.k[a];
+                        // generic rows: slot r is valid when base + r lies in [0, lim),
+                        // lim folding the outer axes in (0 fails every slot)
+                        const int base = bin0[bi] + grp * 4 - qs[m][R - 1];
+                        const unsigned lim = outer_ok ? (unsigned)g.k[R - 1] : 0u;
+#pragma unroll
+                        for (int r = 0; r < 4; ++r)
+                            add[r] = short_rows ? (outer_ok ? ain[m][bi][r] : -INFINITY)
+                                     : (unsigned)(base + r) < lim ? negm[m] : -INFINITY;
+                    }
+                    return add;
+                };
                 f32x4 sacc[QM][2];
 #pragma unroll
                 for (int bi = 0; bi < 2; ++bi)
 #pragma unroll
                     for (int m = 0; m < QM; ++m) {
-                        sacc[m][bi] = f32x4{0.f, 0.f, 0.f, 0.f};
+                        if constexpr (kFoldAdd)
+                            sacc[m][bi] = score_addend(m, bi);
+                        else
+                            sacc[m][bi] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
                         for (int st = 0; st < C::kKS; ++st)
                             sacc[m][bi] = Tr<T>::mma(kf[bi][st], qf[m][st], sacc[m][bi]);
                     }
 
-                // ---- mask + online softmax per query block ----
-                // y = scale*log2(e)*s - m (base 2, relative to the running
-                // reference m; masked pairs get -inf through the FMA addend)
+                // ---- online softmax per query block ----
                 x8 pf[QM];
 #pragma unroll
                 for (int m = 0; m < QM; ++m) {
                     float y[2][4];
-                    if (!short_rows && full[0] && full[1]) {
 #pragma unroll
-                        for (int bi = 0; bi < 2; ++bi)
+                    for (int bi = 0; bi < 2; ++bi) {
+                        if constexpr (kFoldAdd) {
 #pragma unroll
-                            for (int r = 0; r < 4; ++r) y[bi][r] = fmaf(sacc[m][bi][r], c, negm[m]);
-                    } else if (short_rows) {
+                            for (int r = 0; r < 4; ++r) y[bi][r] = sacc[m][bi][r];
+                        } else {
+                            const f32x4 add = score_addend(m, bi);
 #pragma unroll
-                        for (int bi = 0; bi < 2; ++bi) {
-                            bool outer_ok = rel[bi];
-#pragma unroll
-                            for (int a = 0; a < R - 1; ++a)
-                                outer_ok = outer_ok &&
-                                           (unsigned)(boc[bi][a] - qs[m][a]) < (unsigned)g.k[a];
-#pragma unroll
-                            for (int r = 0; r < 4; ++r)
-                                y[bi][r] = fmaf(sacc[m][bi][r], c,
-                                                outer_ok ? ain[m][bi][r] : -INFINITY);
-                        }
-                    } else {
-#pragma unroll
-                        for (int bi = 0; bi < 2; ++bi) {
-                            bool outer_ok = rel[bi];
-#pragma unroll
-                            for (int a = 0; a < R - 1; ++a)
-                                outer_ok = outer_ok &&
-                                           (unsigned)(boc[bi][a] - qs[m][a]) < (unsigned)g.k[a];
-                            // slot r is valid when base + r lies in [0, lim): lim folds the
-                            // outer axes in (0 fails every slot) and a full block admits all
-                            const int base = full[bi] ? 0 : bin0[bi] + grp * 4 - qs[m][R - 1];
-                            const unsigned lim = full[bi] ? 4u : outer_ok ? (unsigned)g.k[R - 1] : 0u;
-#pragma unroll
-                            for (int r = 0; r < 4; ++r)
-                                y[bi][r] = fmaf(sacc[m][bi][r], c,
-                                                (unsigned)(base + r) < lim ? negm[m] : -INFINITY);
+                            for (int r = 0; r < 4; ++r) y[bi][r] = fmaf(sacc[m][bi][r], c, add[r]);
                         }
                     }
                     // this lane's share of the row; the row maximum exceeds the
