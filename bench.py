@@ -4,9 +4,14 @@ A timed step is one pass of the fused path on that workload: na_forward then
 na_backward (one launch: dK/dV and dQ workgroup roles, Delta in-kernel), inputs
 resident in HBM; ms_per_step is the whole forward+backward step.  Three timed
 regions, each K back-to-back calls with HIP events on the launch stream at its
-two ends only: steps, forwards alone (fwd_ms), backwards alone (bwd_ms).  The
-reported value is the forward's useful throughput, 4*B*H*N*ell*D FLOPs (masked
-halo work is not credited) divided by fwd_ms.
+two ends only: steps, forwards alone (fwd_ms), backwards alone (bwd_ms).  Each
+region is timed --reps times and the median is reported (all repetitions are
+listed too).  The reported value is the forward's useful throughput,
+4*B*H*N*ell*D FLOPs (masked halo work is not credited) divided by fwd_ms.
+
+A "cold" forward figure is measured beside it: single launches, each after a
+512 MiB write that evicts the inputs from L2 and the MALL, timed one by one
+with events (which adds the event overhead of one launch).
 
 Prints one JSON line.  --gpus above 1 is refused: this build runs on one GPU.
 """
@@ -57,28 +62,57 @@ def measured_traffic():
         return None
 
 
-def cpu_baseline(problem, x, budget_s):
-    """The fp64 oracle's forward on the full workload, repeated for about budget_s seconds."""
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def cpu_baseline(problem, x, budget_s, single_thread_s):
+    """The fp64 oracle's forward on the full workload, repeated for about budget_s seconds
+    on all host threads, then for about single_thread_s seconds on one thread."""
     import oracle
 
     f = lambda t: t.double().numpy()
     q, k, v = f(x["q"]), f(x["k"]), f(x["v"])
-    reps, t0 = 0, time.perf_counter()
-    while True:
-        oracle.forward(q, k, v, problem.kernel_size, problem.dilation, problem.softmax_scale,
-                       causal=problem.causal_axes)
-        reps += 1
-        el = time.perf_counter() - t0
-        if el >= budget_s or reps >= 10000:
-            break
-    return {
+
+    def run(budget):
+        reps, t0 = 0, time.perf_counter()
+        while True:
+            oracle.forward(q, k, v, problem.kernel_size, problem.dilation,
+                           problem.softmax_scale, causal=problem.causal_axes)
+            reps += 1
+            el = time.perf_counter() - t0
+            if el >= budget or reps >= 10000:
+                return reps, el
+
+    threads = oracle.num_threads()
+    reps, el = run(budget_s)
+    out = {
         "value": problem.fwd_flops() * reps / el / 1e12,
         "unit": "TFLOP/s",
-        "cores": oracle.num_threads(),
+        "cores": threads,
         "kind": "oracle",
         "sample": f"full {problem.name} forward (all {problem.batch * problem.heads * problem.tokens}"
                   f" queries) x {reps} repetitions in {el:.1f} s, fp64",
+        "cpu_model": cpu_model(),
+        "ms_per_forward": round(el / reps * 1e3, 3),
     }
+    if single_thread_s > 0:
+        try:
+            oracle.set_num_threads(1)
+            reps1, el1 = run(single_thread_s)
+        finally:
+            oracle.set_num_threads(threads)
+        out["single_thread"] = {"value": problem.fwd_flops() * reps1 / el1 / 1e12,
+                                "ms_per_forward": round(el1 / reps1 * 1e3, 3),
+                                "repetitions": reps1}
+    return out
 
 
 def main():
@@ -86,7 +120,12 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--reps", type=int, default=5,
+                    help="repetitions of each timed region (the median is reported)")
+    ap.add_argument("--cold-launches", type=int, default=20,
+                    help="single forward launches after a cache-evicting write (0: skip)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    ap.add_argument("--cpu-single-thread-seconds", type=float, default=3.0)
     ap.add_argument("--no-cpu-baseline", action="store_true",
                     help="skip the CPU oracle baseline and the MFMA-bound side measurement "
                          "(profiling runs)")
@@ -170,13 +209,39 @@ def main():
         torch.cuda.synchronize()
         return e0.elapsed_time(e1) / K
 
-    # Timed region 1: K forward + backward steps (the whole path).
-    step_ms = timed(step)
-    # Timed region 2: K forward launches (the forward kernel's steady-state
-    # duration, which the metric and the roofline use).
-    fwd_ms = timed(fwd)
-    # Timed region 3: K backward launches.
-    bwd_ms = timed(bwd)
+    def median(xs):
+        ys = sorted(xs)
+        n = len(ys)
+        return ys[n // 2] if n % 2 else 0.5 * (ys[n // 2 - 1] + ys[n // 2])
+
+    reps = max(args.reps, 1)
+    step_reps, fwd_reps, bwd_reps = [], [], []
+    for _ in range(reps):
+        # Timed region 1: K forward + backward steps (the whole path).
+        step_reps.append(timed(step))
+        # Timed region 2: K forward launches (the forward kernel's steady-state
+        # duration, which the metric and the roofline use).
+        fwd_reps.append(timed(fwd))
+        # Timed region 3: K backward launches.
+        bwd_reps.append(timed(bwd))
+    step_ms, fwd_ms, bwd_ms = median(step_reps), median(fwd_reps), median(bwd_reps)
+
+    # Cold forward: each launch after a write of 512 MiB (beyond L2 and the
+    # 256 MiB MALL), so Q, K and V come from HBM.
+    cold_ms = None
+    if args.cold_launches > 0:
+        flush = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
+        cold = []
+        for _ in range(args.cold_launches):
+            flush.fill_(1)
+            c0, c1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            c0.record()
+            fwd()
+            c1.record()
+            torch.cuda.synchronize()
+            cold.append(c0.elapsed_time(c1))
+        del flush
+        cold_ms = median(cold)
 
     def head_start(per_item_s):
         head_s = min(2.0 * K * per_item_s + 1e-3, 5.0)
@@ -210,6 +275,11 @@ def main():
         "fwd_ms": round(fwd_ms, 5),
         "bwd_ms": round(bwd_ms, 5),
         "fwd_bwd_ms": round(step_ms, 5),
+        "reps": reps,
+        "fwd_ms_reps": [round(t, 5) for t in fwd_reps],
+        "bwd_ms_reps": [round(t, 5) for t in bwd_reps],
+        "step_ms_reps": [round(t, 5) for t in step_reps],
+        "fwd_ms_cold": None if cold_ms is None else round(cold_ms, 5),
         "host_enqueue_ms_per_step": round(host_step_s * 1e3, 4),
         "mfma_peak_frac": round(fwd_tflops / PEAK_FP16_TFLOPS, 5),
         "roofline": {
@@ -226,7 +296,8 @@ def main():
     if not args.no_cpu_baseline:
         if p.name == workloads.BENCH_WORKLOAD:
             result["mfma_bound"] = mfma_bound_forward(na, dev, head_start, host_step_s)
-        result["cpu_baseline"] = cpu_baseline(p, x, args.cpu_seconds)
+        result["cpu_baseline"] = cpu_baseline(p, x, args.cpu_seconds,
+                                              args.cpu_single_thread_seconds)
     print(json.dumps(result), flush=True)
 
 
@@ -236,8 +307,9 @@ def main():
 MFMA_BOUND_WORKLOAD = "1d_fp16_L32768_k1023_d4"
 
 
-def mfma_bound_forward(na, dev, head_start, host_step_s, launches=100):
-    """Back-to-back forward launches on the MFMA-bound workload (side measurement)."""
+def mfma_bound_forward(na, dev, head_start, host_step_s, launches=100, reps=5):
+    """Back-to-back forward launches on the MFMA-bound workload (side measurement,
+    median of reps regions of `launches` launches)."""
     p = workloads.CONFIGS[MFMA_BOUND_WORKLOAD]
     x = workloads.make_inputs(p, seed=0, with_grad=False)
     q, k, v = (x[n].to(dev) for n in ("q", "k", "v"))
@@ -247,16 +319,19 @@ def mfma_bound_forward(na, dev, head_start, host_step_s, launches=100):
     for _ in range(10):
         na.forward(q, k, v, *args, out=out, lse=lse)
     torch.cuda.synchronize()
-    f0, f1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    head_start(host_step_s)
-    f0.record()
-    for _ in range(launches):
-        na.forward(q, k, v, *args, out=out, lse=lse)
-    f1.record()
-    torch.cuda.synchronize()
-    ms = f0.elapsed_time(f1) / launches
+    times = []
+    for _ in range(reps):
+        f0, f1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        head_start(host_step_s)
+        f0.record()
+        for _ in range(launches):
+            na.forward(q, k, v, *args, out=out, lse=lse)
+        f1.record()
+        torch.cuda.synchronize()
+        times.append(f0.elapsed_time(f1) / launches)
+    ms = sorted(times)[len(times) // 2]
     tflops = p.fwd_flops() / (ms * 1e-3) / 1e12
-    return {"workload": p.name, "launches": launches, "fwd_ms": round(ms, 5),
+    return {"workload": p.name, "launches": launches, "reps": reps, "fwd_ms": round(ms, 5),
             "tflops": round(tflops, 2), "mfma_peak_frac": round(tflops / PEAK_FP16_TFLOPS, 4)}
 
 

@@ -49,6 +49,8 @@ def _load():
         _build.build()
     lib = ctypes.CDLL(_LIB_PATH)
     lib.na_ref_num_threads.restype = ctypes.c_int
+    lib.na_ref_set_num_threads.argtypes = [ctypes.c_int]
+    lib.na_ref_set_num_threads.restype = None
     lib.na_ref_neighbors.argtypes = [ctypes.c_int, _i64p, _i32p, _i32p, _i32p, _i64p]
     lib.na_ref_axis_relation.argtypes = [ctypes.c_int64, ctypes.c_int32, ctypes.c_int32,
                                          ctypes.c_int32, _i64p, _i64p, _i64p, _i64p]
@@ -96,6 +98,11 @@ def _f64(a):
 
 def num_threads():
     return int(_load().na_ref_num_threads())
+
+
+def set_num_threads(n):
+    """Threads used by later calls (the results do not depend on it)."""
+    _load().na_ref_set_num_threads(int(n))
 
 
 def neighbors(extents, kernel_size, dilation, causal=None):

@@ -67,6 +67,16 @@ int na_ref_num_threads(void) {
 #endif
 }
 
+/* Threads for later calls (n >= 1); each thread still owns whole (b, h)
+ * slices, so the results do not depend on n. */
+void na_ref_set_num_threads(int n) {
+#ifdef _OPENMP
+    if (n >= 1) omp_set_num_threads(n);
+#else
+    (void)n;
+#endif
+}
+
 static int check_problem(int rank, const int64_t* L, const int32_t* k, const int32_t* d) {
     if (rank < 1 || rank > NA_REF_MAX_RANK) return REF_ERR_RANK;
     for (int a = 0; a < rank; ++a) {

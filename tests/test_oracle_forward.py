@@ -167,3 +167,26 @@ def test_rejects_illegal_problems():
         oracle.forward(x, x, x, [0], [1], 1.0)
     with pytest.raises(ValueError):
         oracle.forward(x, x, x, [1], [0], 1.0)
+
+
+def test_thread_count_does_not_change_results():
+    """Each thread owns whole (b, h) slices, so one thread gives the same bits."""
+    B, H, D = 3, 2, 8
+    ext, ks, ds = (11, 9), (5, 3), (2, 1)
+    shape = (B, H) + ext + (D,)
+    q, k, v, g = (_rand(shape, s) for s in (31, 32, 33, 34))
+    n0 = oracle.num_threads()
+    out, lse = oracle.forward(q, k, v, ks, ds, 0.4)
+    grads = oracle.backward(q, k, v, g, ks, ds, 0.4)
+    try:
+        oracle.set_num_threads(1)
+        assert oracle.num_threads() == 1
+        out1, lse1 = oracle.forward(q, k, v, ks, ds, 0.4)
+        grads1 = oracle.backward(q, k, v, g, ks, ds, 0.4)
+    finally:
+        oracle.set_num_threads(n0)
+    assert oracle.num_threads() == n0
+    np.testing.assert_array_equal(out1, out)
+    np.testing.assert_array_equal(lse1, lse)
+    for a, b in zip(grads1, grads):
+        np.testing.assert_array_equal(a, b)
