@@ -178,6 +178,10 @@ __device__ __forceinline__ void dq_role(const Geo& g, int braw, unsigned char* s
     }
     wait_vmem();
     __syncthreads();
+    // -lse2 in all four slots: the accumulator seed of full tiles (kFoldAdd)
+    f32x4 nlse4[QM];
+#pragma unroll
+    for (int m = 0; m < QM; ++m) nlse4[m] = f32x4{-lse2[m], -lse2[m], -lse2[m], -lse2[m]};
     // kFoldAdd: Q scaled once by c = scale*log2(e) and rounded to T
     if constexpr (kFoldAdd)
 #pragma unroll
@@ -250,11 +254,15 @@ __device__ __forceinline__ void dq_role(const Geo& g, int braw, unsigned char* s
                             const x8 vf = rfr.read(vs + boff, st);
 #pragma unroll
                             for (int m = 0; m < QM; ++m) {
-                                f32x4 s0 = f32x4{0.f, 0.f, 0.f, 0.f};
-                                if constexpr (kFoldAdd)
-                                    if (st == 0) s0 = score_addend(m, bi);
+                                if (st > 0)
+                                    sacc[m][bi] = Tr<T>::mma(kf, qf[m][st], sacc[m][bi]);
+                                else if (kFoldAdd && !short_rows && full[bi])
+                                    sacc[m][bi] = Tr<T>::mma(kf, qf[m][0], nlse4[m]);  // in place
+                                else
+                                    sacc[m][bi] = Tr<T>::mma(kf, qf[m][0],
+                                                             kFoldAdd ? score_addend(m, bi)
+                                                                      : f32x4{0.f, 0.f, 0.f, 0.f});
                                 const f32x4 nd = f32x4{-dlt[m], -dlt[m], -dlt[m], -dlt[m]};
-                                sacc[m][bi] = Tr<T>::mma(kf, qf[m][st], st == 0 ? s0 : sacc[m][bi]);
                                 pacc[m][bi] = Tr<T>::mma(vf, gf[m][st], st == 0 ? nd : pacc[m][bi]);
                             }
                         }
@@ -630,10 +638,14 @@ __device__ __forceinline__ void dkdv_role(const Geo& g, int braw, int nwk,
                             const x8 ga = rfr.read(gs + boff, st);
 #pragma unroll
                             for (int m = 0; m < KM; ++m) {
-                                f32x4 s0 = f32x4{0.f, 0.f, 0.f, 0.f};
-                                if constexpr (kFoldAdd)
-                                    if (st == 0) s0 = score_addend(m, bi);
-                                sacc[m][bi] = Tr<T>::mma(qa, kf[m][st], st == 0 ? s0 : sacc[m][bi]);
+                                if (st > 0)
+                                    sacc[m][bi] = Tr<T>::mma(qa, kf[m][st], sacc[m][bi]);
+                                else if (kFoldAdd && !short_rows && full[bi])
+                                    sacc[m][bi] = Tr<T>::mma(qa, kf[m][0], nlse[bi]);  // in place
+                                else
+                                    sacc[m][bi] = Tr<T>::mma(qa, kf[m][0],
+                                                             kFoldAdd ? score_addend(m, bi)
+                                                                      : f32x4{0.f, 0.f, 0.f, 0.f});
                                 pacc[m][bi] = Tr<T>::mma(ga, vf[m][st], st == 0 ? ndl[bi] : pacc[m][bi]);
                             }
                         }

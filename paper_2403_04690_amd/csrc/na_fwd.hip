@@ -172,10 +172,14 @@ __global__ __launch_bounds__(256) void na_fwd_kernel(Geo g, const T* __restrict_
     for (int j = 0; j < 8; ++j) ones[j] = (T)1.0f;
     f32x4 oacc[QM][C::kDB], lsum[QM];
     float mref[QM], negm[QM], thr[QM], lrow[QM];
+    // kFoldAdd: negm in all four slots, the accumulator seed of full tiles,
+    // kept as a vector so the matrix cores read it in place (no per-tile splat)
+    f32x4 negm4[QM];
 #pragma unroll
     for (int m = 0; m < QM; ++m) {
         mref[m] = -INFINITY;
         negm[m] = 0.f;
+        negm4[m] = f32x4{0.f, 0.f, 0.f, 0.f};
         thr[m] = -INFINITY;
         lsum[m] = f32x4{0.f, 0.f, 0.f, 0.f};
         lrow[m] = 0.f;
@@ -301,12 +305,15 @@ __global__ __launch_bounds__(256) void na_fwd_kernel(Geo g, const T* __restrict_
                 for (int bi = 0; bi < 2; ++bi)
 #pragma unroll
                     for (int m = 0; m < QM; ++m) {
-                        if constexpr (kFoldAdd)
-                            sacc[m][bi] = score_addend(m, bi);
+                        // (the first product of a full tile reads negm4 in place)
+                        if (kFoldAdd && !short_rows && full[bi])
+                            sacc[m][bi] = Tr<T>::mma(kf[bi][0], qf[m][0], negm4[m]);
                         else
-                            sacc[m][bi] = f32x4{0.f, 0.f, 0.f, 0.f};
+                            sacc[m][bi] = Tr<T>::mma(kf[bi][0], qf[m][0],
+                                                     kFoldAdd ? score_addend(m, bi)
+                                                              : f32x4{0.f, 0.f, 0.f, 0.f});
 #pragma unroll
-                        for (int st = 0; st < C::kKS; ++st)
+                        for (int st = 1; st < C::kKS; ++st)
                             sacc[m][bi] = Tr<T>::mma(kf[bi][st], qf[m][st], sacc[m][bi]);
                     }
 
@@ -341,6 +348,7 @@ __global__ __launch_bounds__(256) void na_fwd_kernel(Geo g, const T* __restrict_
                         mref[m] = raise ? dlt - negm[m] : mref[m];
                         const bool seen = mref[m] != -INFINITY;
                         negm[m] = seen ? -mref[m] : 0.f;
+                        negm4[m] = f32x4{negm[m], negm[m], negm[m], negm[m]};
                         thr[m] = seen ? kLazy : -INFINITY;
                         if (R > 1) refresh_addends(m);
                         if constexpr (kMfmaSum)
