@@ -43,12 +43,12 @@ int64_t token_count(int rank, const int64_t* extents) {
 // Wave tile (queries or keys owned by one wave, 16 * m of them) along each
 // axis, sized from the innermost axis outwards and never longer than the
 // longest dilation group of an axis (rounded up to a power of two).
-void wave_tile(int rank, const int* glen, int m, int* wt, int* wgd) {
+void wave_tile(int rank, const int* glen, int m, int waves, int* wt, int* wgd) {
     const int q = 16 * m;
     for (int a = 0; a < 3; ++a) wt[a] = wgd[a] = 1;
     if (rank == 1) {
         wt[0] = q;
-        wgd[0] = 4;
+        wgd[0] = waves;
         return;
     }
     const int inner = rank - 1;
@@ -84,7 +84,7 @@ void wave_tile(int rank, const int* glen, int m, int* wt, int* wgd) {
 
 // Fills the geometry of a problem for wave tiles of 16 * m tokens.
 bool make_geo(int rank, const int64_t* extents, const int32_t* ks, const int32_t* ds,
-              const int32_t* causal, int64_t BH, int m, na::Geo& g) {
+              const int32_t* causal, int64_t BH, int m, na::Geo& g, int waves = 4) {
     std::memset(&g, 0, sizeof(g));
     int glen[3] = {1, 1, 1};
     for (int a = 0; a < 3; ++a) {
@@ -106,7 +106,7 @@ bool make_geo(int rank, const int64_t* extents, const int32_t* ks, const int32_t
     g.BH = (int)BH;
     g.ngroups = 1;
     for (int a = 0; a < rank; ++a) g.ngroups *= g.d[a];
-    wave_tile(rank, glen, m, g.WT, g.WGd);
+    wave_tile(rank, glen, m, rank == 1 ? waves : 4, g.WT, g.WGd);
     int64_t ntiles = 1;
     for (int a = 0; a < 3; ++a) {
         g.T[a] = g.WT[a] * g.WGd[a];
@@ -138,6 +138,18 @@ int choose_m(int rank, const int64_t* extents, const int32_t* ks, const int32_t*
     na::Geo g;
     if (!make_geo(rank, extents, ks, ds, nullptr, BH, 2, g)) return 1;
     return g.nwg < 1024 ? 1 : 2;
+}
+
+// Forward workgroup size: 1-D problems of 16-bit types with plenty of
+// 4-wave workgroups run 8-wave ones instead (each stage of K/V rows then
+// serves twice the queries).  NA_FWD_WAVES=4|8 overrides.
+int forward_waves(int rank, na_dtype dtype, const na::Geo& g4) {
+    if (rank != 1 || dtype == NA_FP32) return 4;
+    if (const char* env = std::getenv("NA_FWD_WAVES")) {
+        const int v = std::atoi(env);
+        if (v == 4 || v == 8) return v;
+    }
+    return g4.nwg >= 2048 ? 8 : 4;
 }
 
 na_status check_problem(int rank, const int64_t* extents, const int32_t* ks, const int32_t* ds,
@@ -213,6 +225,9 @@ na_status na_forward(int rank, const int64_t* extents, const int32_t* kernel_siz
     const int m = choose_m(rank, extents, kernel_size, dilation, BH);
     na::Geo g;
     if (!make_geo(rank, extents, kernel_size, dilation, causal, BH, m, g)) return NA_ERR_SHAPE;
+    if (forward_waves(rank, dtype, g) == 8 &&
+        !make_geo(rank, extents, kernel_size, dilation, causal, BH, m, g, 8))
+        return NA_ERR_SHAPE;
     hipError_t e = na::launch_forward(g, rank, (int)head_dim, (int)dtype, m, q, k, v, out,
                                       logsumexp, scale, reinterpret_cast<hipStream_t>(stream));
     return e == hipSuccess ? NA_OK : NA_ERR_HIP;

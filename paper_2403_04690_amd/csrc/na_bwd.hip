@@ -801,8 +801,9 @@ static hipError_t launch_bwd_sb(const Geo& g, bool short_rows, int hq, int hk, c
                                 const void* k, const void* v, const void* o, const float* lse,
                                 const void* dout, void* dq, void* dk, void* dv, float scale,
                                 hipStream_t stream) {
-    auto kern = short_rows ? na_bwd_kernel<R, D, T, QM, KM, SBQ, SBK, 1>
-                           : na_bwd_kernel<R, D, T, QM, KM, SBQ, SBK, 0>;
+    auto kern = na_bwd_kernel<R, D, T, QM, KM, SBQ, SBK, 0>;
+    if constexpr (R > 1)  // (1-D boxes have one row: never short)
+        if (short_rows) kern = na_bwd_kernel<R, D, T, QM, KM, SBQ, SBK, 1>;
     const size_t lds = std::max((hq > SBQ ? 2 : 1) * DqCfg<R, D, T, QM, SBQ>::kBufBytes,
                                 (hk > SBK ? 2 : 1) * DkvCfg<R, D, T, KM, SBK>::kBufBytes);
     if (lds > 65536) {

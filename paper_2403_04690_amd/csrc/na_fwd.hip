@@ -8,8 +8,9 @@
 // workgroups over the sub-lattices x = g (mod d) (Sec. 3.4).
 //
 // MI355X mapping:
-//   * workgroup = 4 waves = one query tile of one (batch, head, dilation
-//     group); each wave owns QM x 16 queries of it (a sub-box);
+//   * workgroup = W waves (4; 8 for large 1-D problems) = one query tile of
+//     one (batch, head, dilation group); each wave owns QM x 16 queries of it
+//     (a sub-box);
 //   * the workgroup's key halo is cut into blocks of 16 keys that run along
 //     the innermost axis; stages of SB blocks go straight from HBM to LDS
 //     (16-byte direct-to-LDS loads, double buffered when there is more than
@@ -41,27 +42,29 @@ namespace na {
 
 constexpr float kLazy = 8.f;  // base-2 headroom before the running max is raised
 
-template <int R, int D, typename T, int QM, int SB>
+template <int R, int D, typename T, int QM, int SB, int W = 4>
 struct FwdCfg {
-    static constexpr int kThreads = 4 * kWave;
+    static constexpr int kWaves = W;
+    static constexpr int kThreads = W * kWave;
     static constexpr int kKeys = SB * 16;  // keys per stage
     static constexpr int kTileBytes = kKeys * Rows<T, D>::kRowBytes;
     static constexpr size_t kBufBytes = 2 * kTileBytes;  // K rows, then V rows
     static constexpr int kKS = D / 32;  // contraction steps over D
     static constexpr int kDB = D / 16;  // 16-wide blocks of D
-    using Ld = DirectRows<T, D, kKeys>;
+    using Ld = DirectRows<T, D, kKeys, W>;
     static_assert(SB % 2 == 0 && SB <= 32, "stage blocks are tested by one lane each");
 };
 
 // c = scale * log2(e): scores are kept in base 2.  SHORT = 1: every halo row
 // holds at most two 16-key blocks (rank >= 2), so the inner-axis mask is a
 // per-lane constant; SHORT = 0: general masking with mask-free full blocks.
-template <int R, int D, typename T, int QM, int SB, int SHORT>
-__global__ __launch_bounds__(256) void na_fwd_kernel(Geo g, const T* __restrict__ qg,
-                                                     const T* __restrict__ kg,
-                                                     const T* __restrict__ vg, T* __restrict__ og,
-                                                     float* __restrict__ lseg, float c) {
-    using C = FwdCfg<R, D, T, QM, SB>;
+template <int R, int D, typename T, int QM, int SB, int SHORT, int W>
+__global__ __launch_bounds__(W * kWave) void na_fwd_kernel(Geo g, const T* __restrict__ qg,
+                                                           const T* __restrict__ kg,
+                                                           const T* __restrict__ vg,
+                                                           T* __restrict__ og,
+                                                           float* __restrict__ lseg, float c) {
+    using C = FwdCfg<R, D, T, QM, SB, W>;
     using x8 = typename Tr<T>::x8;
     extern __shared__ __align__(16) unsigned char smem_raw[];
 
@@ -424,12 +427,15 @@ static int max_row_blocks(const Geo& g, int rank) {
     return (e + 15) / 16;
 }
 
-template <int R, int D, typename T, int QM, int SB>
+template <int R, int D, typename T, int QM, int SB, int W = 4>
 static hipError_t launch_fwd_inst(const Geo& g, const void* q, const void* k, const void* v,
                                   void* o, float* lse, float scale, hipStream_t stream) {
-    using C = FwdCfg<R, D, T, QM, SB>;
+    using C = FwdCfg<R, D, T, QM, SB, W>;
+    if (g.WGd[0] * g.WGd[1] * g.WGd[2] != W) return hipErrorInvalidConfiguration;
     const bool short_rows = R > 1 && max_row_blocks(g, R) <= 2;
-    auto kern = short_rows ? na_fwd_kernel<R, D, T, QM, SB, 1> : na_fwd_kernel<R, D, T, QM, SB, 0>;
+    auto kern = na_fwd_kernel<R, D, T, QM, SB, 0, W>;
+    if constexpr (R > 1)  // (1-D halos have one row: never short)
+        if (short_rows) kern = na_fwd_kernel<R, D, T, QM, SB, 1, W>;
     const int nst_max = (max_halo_blocks(g, R) + SB - 1) / SB;
     const size_t lds = (nst_max > 1 ? 2 : 1) * C::kBufBytes;
     if (lds > 65536) {
@@ -450,6 +456,13 @@ static hipError_t launch_fwd_qm(const Geo& g, int qm, const void* q, const void*
         if (qm == 1) return launch_fwd_inst<R, D, T, 1, 2>(g, q, k, v, o, lse, scale, stream);
         return launch_fwd_inst<R, D, T, 2, 2>(g, q, k, v, o, lse, scale, stream);
     } else {
+        // 1-D: eight waves share each (twice as large) stage
+        if constexpr (R == 1) {
+            if (g.WGd[0] == 8) {
+                if (qm == 1) return launch_fwd_inst<R, D, T, 1, 8, 8>(g, q, k, v, o, lse, scale, stream);
+                return launch_fwd_inst<R, D, T, 2, 8, 8>(g, q, k, v, o, lse, scale, stream);
+            }
+        }
         // one LDS stage covering the whole halo when it is small and D is 32
         if constexpr (D == 32) {
             if (max_halo_blocks(g, R) <= 16) {

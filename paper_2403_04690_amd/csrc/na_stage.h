@@ -128,13 +128,14 @@ typedef __attribute__((address_space(3))) void lds_void;
 // lane l loads the segment that the swizzle puts at position 64 t + l.
 // Tokens missing from the box are replaced by token 0 of the slice (finite
 // data that the masks exclude).  Several tensors with the same rows share one
-// set of per-lane source offsets.
-template <typename T, int D, int ROWS>
+// set of per-lane source offsets.  The W waves of the workgroup take the
+// instructions round-robin.
+template <typename T, int D, int ROWS, int W = 4>
 struct DirectRows {
     using L = Rows<T, D>;
     static constexpr int kRowsPerInstr = 64 / L::kSegs;
     static constexpr int kInstr = ROWS * L::kSegs / 64;  // wave instructions per tensor
-    static constexpr int kPerWave = (kInstr + 3) / 4;
+    static constexpr int kPerWave = (kInstr + W - 1) / W;
     static_assert(ROWS % 16 == 0 && kInstr >= 1, "whole blocks per stage");
     int src[kPerWave];  // element offset (within the slice) of this lane's segment
 
@@ -145,7 +146,7 @@ struct DirectRows {
                                             int tstep, int wave, int lane) {
 #pragma unroll
         for (int u = 0; u < kPerWave; ++u) {
-            const int t = wave + 4 * u;
+            const int t = wave + W * u;
             src[u] = 0;
             if (t < kInstr) {
                 const int row0 = t * kRowsPerInstr;  // first stage-local row (uniform)
@@ -162,7 +163,7 @@ struct DirectRows {
     __device__ __forceinline__ void issue(const T* base, unsigned char* tile, int wave) const {
 #pragma unroll
         for (int u = 0; u < kPerWave; ++u) {
-            const int t = wave + 4 * u;
+            const int t = wave + W * u;
             if (t < kInstr)
                 __builtin_amdgcn_global_load_lds(static_cast<const void*>(base + src[u]),
                                                  (lds_void*)(tile + t * 1024), 16, 0, 0);

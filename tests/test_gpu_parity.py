@@ -132,6 +132,33 @@ def test_forward_small(na, ext, ks, ds, D, dtype, B, H):
     assert eo <= TOL[dtype] and el <= TOL[dtype]
 
 
+# 1-D forwards run on 8-wave workgroups when the problem is large; the
+# environment forces that launch shape (and the query blocks per wave) on
+# small ragged, dilated and causal problems too.
+EIGHT_WAVE_CASES = [
+    # (extents, kernel, dilation, causal, head_dim, dtype, batch, heads, blocks per wave)
+    ((300,), (13,), (3,), None, 64, "fp16", 2, 2, 1),
+    ((1000,), (255,), (2,), None, 64, "bf16", 1, 2, 2),
+    ((777,), (129,), (1,), (True,), 32, "fp16", 1, 2, 2),
+    ((513,), (31,), (4,), None, 128, "fp16", 1, 1, 1),
+    ((2100,), (1023,), (2,), None, 64, "fp16", 1, 1, 2),
+]
+
+
+@pytest.mark.parametrize("ext,ks,ds,cs,D,dtype,B,H,m", EIGHT_WAVE_CASES)
+def test_forward_eight_wave_workgroups(na, monkeypatch, ext, ks, ds, cs, D, dtype, B, H, m):
+    monkeypatch.setenv("NA_FWD_WAVES", "8")
+    monkeypatch.setenv("NA_WAVE_BLOCKS", str(m))
+    shape = (B, H) + ext + (D,)
+    q, k, v = _inputs(shape, dtype, 13, 3)
+    out, lse = na.forward(*_dev(q, k, v), ks, ds, causal=cs)
+    ro, rl = oracle.forward(_f64(q), _f64(k), _f64(v), ks, ds, 1.0 / math.sqrt(D), causal=cs)
+    eo, el = _maxerr(out, ro), _maxerr(lse, rl)
+    _log(f"fwd 8 waves {ext} k={ks} d={ds} c={cs} D={D} {dtype} m={m}: "
+         f"max|dO|={eo:.3g} max|dLSE|={el:.3g}")
+    assert eo <= TOL[dtype] and el <= TOL[dtype]
+
+
 def test_forward_window_one_is_exact_copy(na):
     for dtype in ("fp16", "bf16", "fp32"):
         shape = (2, 2, 13, 17, 64)
