@@ -132,6 +132,11 @@ def main():
     ap.add_argument("--workload", default=WORKLOAD, choices=workloads.CONFIG_ORDER,
                     help="profiling aid: run the same step on another workload (the reported "
                          "line is defined on the default one)")
+    ap.add_argument("--tune", action="store_true",
+                    help="run the library's tiling tuner (na_tune) on the workload before the "
+                         "timed regions, so they use the tuned tilings")
+    ap.add_argument("--tune-report", action="store_true",
+                    help="only run the tuner on the workload and print its choice and timings")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="counter calibration: only run 5 device-to-device copies of this many "
                          "MiB (the HBM traffic of each is known) and exit")
@@ -162,6 +167,21 @@ def main():
     dq, dk, dv = torch.empty_like(q), torch.empty_like(k), torch.empty_like(v)
     ks, ds, sc = p.kernel_size, p.dilation, p.softmax_scale
     cz = p.causal_axes if any(p.causal_axes) else None
+
+    tuning = None
+    if args.tune or args.tune_report:
+        na.tune_clear()
+        bf, bb, tms = na.tune(q, k, v, g, ks, ds, sc, causal=cz, repeats=10, out=out, lse=lse,
+                              dq=dq, dk=dk, dv=dv)
+        tuning = {"forward_tiling": list(bf), "backward_tiling": list(bb),
+                  "fwd_ms_tuned": round(tms[0], 5), "bwd_ms_tuned": round(tms[1], 5),
+                  "fwd_ms_heuristic": round(tms[2], 5), "bwd_ms_heuristic": round(tms[3], 5),
+                  "candidates": [len(na.candidate_tilings(p.extents, ks, ds, p.batch, p.heads,
+                                                          p.head_dim, q.dtype, forward=f))
+                                 for f in (True, False)]}
+        if args.tune_report:
+            print(json.dumps({"workload": p.name, **tuning}), flush=True)
+            return
 
     def fwd():
         na.forward(q, k, v, ks, ds, sc, out=out, lse=lse, causal=cz)
@@ -264,7 +284,8 @@ def main():
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": {"fp16": "f16", "bf16": "bf16", "fp32": "f32"}[p.dtype],
-        "data": "synthetic: iid N(0,1) q, k, v, dO (torch CPU generator, seed 0), rounded to fp16",
+        "data": f"synthetic: iid N(0,1) q, k, v, dO (torch CPU generator, seed 0), rounded to "
+                f"{p.dtype}",
         "config": {
             "workload": p.name,
             "rank": p.rank, "batch": p.batch, "heads": p.heads, "extents": list(p.extents),
@@ -280,6 +301,7 @@ def main():
         "bwd_ms_reps": [round(t, 5) for t in bwd_reps],
         "step_ms_reps": [round(t, 5) for t in step_reps],
         "fwd_ms_cold": None if cold_ms is None else round(cold_ms, 5),
+        "tuned": tuning,
         "host_enqueue_ms_per_step": round(host_step_s * 1e3, 4),
         "mfma_peak_frac": round(fwd_tflops / PEAK_FP16_TFLOPS, 5),
         "roofline": {

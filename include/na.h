@@ -27,8 +27,9 @@
  *     log, scale included: lse = log sum_j exp(scale * q.k_j).
  *   - Every device pointer must be 16-byte aligned.
  *   - The caller owns all memory; the library never allocates or frees
- *     device memory, needs no workspace, keeps no global state and is
- *     re-entrant.
+ *     device memory and needs no workspace.  Its only global state is the
+ *     tiling cache that na_tune fills (guarded by a mutex); every entry point
+ *     is re-entrant.
  *   - Calls are asynchronous and stream-ordered on `stream` (a hipStream_t;
  *     NULL means the legacy default stream).  Problem validation is
  *     synchronous and happens before any launch: a non-NA_OK status means
@@ -69,8 +70,29 @@ typedef enum {
     NA_ERR_ALIGNMENT = 9,             /* a device pointer is not 16-byte aligned */
     /* 10 is not used */
     NA_ERR_HIP = 11,                  /* a HIP launch or query failed */
-    NA_ERR_SCALE = 12                 /* scale is not finite */
+    NA_ERR_SCALE = 12,                /* scale is not finite */
+    NA_ERR_TILING = 13                /* an explicit tiling is not valid for the problem */
 } na_status;
+
+/*
+ * How a launch cuts the problem into work (query tiles for the forward and
+ * the dQ role, key tiles for the dK/dV role; multi-axis tiles as in the
+ * paper's fused kernels, Sec. 3.3 and App. A):
+ *   blocks_per_wave: 16-token blocks per wave, 1 or 2;
+ *   wave_tile[a]:    tokens per wave along axis a (group coordinates), powers
+ *                    of two whose product over the problem's axes is
+ *                    16 * blocks_per_wave;
+ *   waves[a]:        waves per workgroup along axis a, powers of two whose
+ *                    product is 4 (8 is also allowed along the only axis of a
+ *                    1-D forward of fp16 / bf16).
+ * Entries for axes beyond the rank must be 1.  A workgroup tile is
+ * wave_tile[a] * waves[a] tokens along axis a.
+ */
+typedef struct {
+    int32_t blocks_per_wave;
+    int32_t wave_tile[3];
+    int32_t waves[3];
+} na_tiling;
 
 /* Human-readable text for a status code (static storage, never NULL). */
 const char* na_status_string(na_status status);
@@ -115,6 +137,66 @@ na_status na_backward(int rank, const int64_t* extents, const int32_t* kernel_si
                       int64_t head_dim, na_dtype dtype, float scale, const void* q, const void* k,
                       const void* v, const void* out, const float* logsumexp, const void* dout,
                       void* dq, void* dk, void* dv, na_stream_t stream);
+
+/*
+ * Tilings (see na_tiling).  The plain entry points above use the tiling
+ * cached for the problem by na_tune, else a heuristic one.  The problem key
+ * of the cache is (rank, extents, kernel_size, dilation, causal, batch * heads,
+ * head_dim, dtype); the scale does not matter.
+ *
+ * na_candidate_tilings (host only): writes up to `max` tilings that na_tune
+ * considers for the forward (forward != 0) or the backward of the problem,
+ * the heuristic one first, and returns how many there are in all (so a
+ * return value above `max` means the list was cut), or a negative na_status
+ * for an invalid problem.
+ *
+ * na_current_tiling (host only): the tiling na_forward (forward != 0) or
+ * na_backward would use now for the problem.
+ *
+ * na_forward_tiled / na_backward_tiled: na_forward / na_backward with an
+ * explicit tiling, which is validated first (NA_ERR_TILING, nothing launched).
+ * Every valid tiling gives the same result up to summation order.
+ *
+ * na_tune (auto-tuner over the query-tile factorisations, App. A): after a
+ * warm-up, times every candidate tiling of the forward and of the backward,
+ * each over `repeats` launches (>= 1) after one warm-up launch, then times the
+ * three fastest and the heuristic tiling again; the heuristic one is kept
+ * unless a finalist beats it by more than 2 %.  Runs on the caller's buffers,
+ * which end up holding the results of the chosen tilings (out and logsumexp
+ * of the forward of q, k, v; dq, dk, dv of the backward with dout).  Records
+ * the chosen forward and backward tilings in the cache.  Synchronises
+ * `stream`; must not run concurrently with other work on these buffers.
+ * Optional outputs (NULL to skip): best_forward, best_backward, and
+ * times_ms[4] = {best forward, best backward, heuristic forward, heuristic
+ * backward} in milliseconds per launch.
+ *
+ * na_tune_clear: empties the cache.
+ */
+int na_candidate_tilings(int rank, const int64_t* extents, const int32_t* kernel_size,
+                         const int32_t* dilation, int64_t batch, int64_t heads, int64_t head_dim,
+                         na_dtype dtype, int forward, na_tiling* out, int max);
+na_status na_current_tiling(int rank, const int64_t* extents, const int32_t* kernel_size,
+                            const int32_t* dilation, const int32_t* causal, int64_t batch,
+                            int64_t heads, int64_t head_dim, na_dtype dtype, int forward,
+                            na_tiling* out);
+na_status na_forward_tiled(int rank, const int64_t* extents, const int32_t* kernel_size,
+                           const int32_t* dilation, const int32_t* causal, int64_t batch,
+                           int64_t heads, int64_t head_dim, na_dtype dtype, float scale,
+                           const na_tiling* tiling, const void* q, const void* k, const void* v,
+                           void* out, float* logsumexp, na_stream_t stream);
+na_status na_backward_tiled(int rank, const int64_t* extents, const int32_t* kernel_size,
+                            const int32_t* dilation, const int32_t* causal, int64_t batch,
+                            int64_t heads, int64_t head_dim, na_dtype dtype, float scale,
+                            const na_tiling* tiling, const void* q, const void* k, const void* v,
+                            const void* out, const float* logsumexp, const void* dout, void* dq,
+                            void* dk, void* dv, na_stream_t stream);
+na_status na_tune(int rank, const int64_t* extents, const int32_t* kernel_size,
+                  const int32_t* dilation, const int32_t* causal, int64_t batch, int64_t heads,
+                  int64_t head_dim, na_dtype dtype, float scale, const void* q, const void* k,
+                  const void* v, void* out, float* logsumexp, const void* dout, void* dq, void* dk,
+                  void* dv, int repeats, na_stream_t stream, na_tiling* best_forward,
+                  na_tiling* best_backward, float* times_ms);
+void na_tune_clear(void);
 
 /*
  * Test hook: evaluates on the device, with the same index functions the

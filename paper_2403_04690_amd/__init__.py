@@ -19,7 +19,8 @@ import os
 import torch
 
 __all__ = ["NAError", "forward", "backward", "na_attention", "debug_windows", "validate",
-           "library_path", "load_library", "DTYPES"]
+           "library_path", "load_library", "DTYPES", "Tiling", "candidate_tilings",
+           "current_tiling", "tune", "tune_clear"]
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
 # NA_LIBRARY may point at another build of the same library (A/B comparisons
@@ -32,6 +33,30 @@ DTYPES = {torch.float32: 0, torch.float16: 1, torch.bfloat16: 2}
 _i64p = ctypes.POINTER(ctypes.c_int64)
 _i32p = ctypes.POINTER(ctypes.c_int32)
 _vp = ctypes.c_void_p
+
+
+class _NaTiling(ctypes.Structure):
+    _fields_ = [("blocks_per_wave", ctypes.c_int32), ("wave_tile", ctypes.c_int32 * 3),
+                ("waves", ctypes.c_int32 * 3)]
+
+
+class Tiling(tuple):
+    """(blocks_per_wave, wave_tile[3], waves[3]) of a launch (na_tiling in na.h)."""
+
+    def __new__(cls, blocks_per_wave, wave_tile, waves):
+        return super().__new__(cls, (int(blocks_per_wave), tuple(int(x) for x in wave_tile),
+                                     tuple(int(x) for x in waves)))
+
+    blocks_per_wave = property(lambda self: self[0])
+    wave_tile = property(lambda self: self[1])
+    waves = property(lambda self: self[2])
+
+    def _c(self):
+        return _NaTiling(self[0], (ctypes.c_int32 * 3)(*self[1]), (ctypes.c_int32 * 3)(*self[2]))
+
+    @staticmethod
+    def _from_c(t):
+        return Tiling(t.blocks_per_wave, tuple(t.wave_tile), tuple(t.waves))
 
 
 class NAError(RuntimeError):
@@ -69,6 +94,22 @@ def load_library():
     lib.na_backward.restype = ctypes.c_int
     lib.na_debug_windows.argtypes = [ctypes.c_int, _i64p, _i32p, _i32p, _i32p, _vp, _vp, _vp, _vp]
     lib.na_debug_windows.restype = ctypes.c_int
+    tp = ctypes.POINTER(_NaTiling)
+    lib.na_candidate_tilings.argtypes = [ctypes.c_int, _i64p, _i32p, _i32p, ctypes.c_int64,
+                                         ctypes.c_int64, ctypes.c_int64, ctypes.c_int,
+                                         ctypes.c_int, tp, ctypes.c_int]
+    lib.na_candidate_tilings.restype = ctypes.c_int
+    lib.na_current_tiling.argtypes = prob[:-1] + [ctypes.c_int, tp]
+    lib.na_current_tiling.restype = ctypes.c_int
+    lib.na_forward_tiled.argtypes = prob + [tp] + [_vp] * 6
+    lib.na_forward_tiled.restype = ctypes.c_int
+    lib.na_backward_tiled.argtypes = prob + [tp] + [_vp] * 10
+    lib.na_backward_tiled.restype = ctypes.c_int
+    lib.na_tune.argtypes = prob + [_vp] * 9 + [ctypes.c_int, _vp, tp, tp,
+                                               ctypes.POINTER(ctypes.c_float)]
+    lib.na_tune.restype = ctypes.c_int
+    lib.na_tune_clear.argtypes = []
+    lib.na_tune_clear.restype = None
     _lib = lib
     return lib
 
@@ -122,8 +163,69 @@ def validate(extents, kernel_size, dilation, batch, heads, head_dim, dtype, scal
     _check(lib.na_validate(rank, ext, ks, ds, cs, batch, heads, head_dim, DTYPES[dtype], scale))
 
 
-def forward(q, k, v, kernel_size, dilation=1, scale=None, out=None, lse=None, causal=None):
-    """Fused NA forward.  Returns (out, logsumexp); logsumexp is fp32 [B, H, X..]."""
+def candidate_tilings(extents, kernel_size, dilation, batch, heads, head_dim, dtype,
+                      forward=True):
+    """The tilings na_tune considers (the heuristic one first), host only."""
+    lib = load_library()
+    rank, ext, ks, ds, _ = _problem_arrays(extents, kernel_size, dilation)
+    n = lib.na_candidate_tilings(rank, ext, ks, ds, batch, heads, head_dim, DTYPES[dtype],
+                                 int(bool(forward)), None, 0)
+    if n < 0:
+        _check(-n)
+    buf = (_NaTiling * max(n, 1))()
+    lib.na_candidate_tilings(rank, ext, ks, ds, batch, heads, head_dim, DTYPES[dtype],
+                             int(bool(forward)), buf, n)
+    return [Tiling._from_c(buf[i]) for i in range(n)]
+
+
+def current_tiling(extents, kernel_size, dilation, batch, heads, head_dim, dtype, forward=True,
+                   causal=None):
+    """The tiling na_forward (or na_backward) uses now for this problem, host only."""
+    lib = load_library()
+    rank, ext, ks, ds, cs = _problem_arrays(extents, kernel_size, dilation, causal)
+    t = _NaTiling()
+    _check(lib.na_current_tiling(rank, ext, ks, ds, cs, batch, heads, head_dim, DTYPES[dtype],
+                                 int(bool(forward)), ctypes.byref(t)))
+    return Tiling._from_c(t)
+
+
+def tune(q, k, v, dout, kernel_size, dilation=1, scale=None, causal=None, repeats=5,
+         out=None, lse=None, dq=None, dk=None, dv=None):
+    """Auto-tune the tilings of this problem (na_tune): times every candidate forward and
+    backward tiling, caches the fastest for later calls and returns
+    (best_forward, best_backward, times_ms) with times_ms = [best fwd, best bwd,
+    heuristic fwd, heuristic bwd].  Synchronises the current stream."""
+    lib = load_library()
+    _check_tensors(q, k, v, dout)
+    B, H, D = q.shape[0], q.shape[1], q.shape[-1]
+    rank, ext, ks, ds, cs = _problem_arrays(tuple(q.shape[2:-1]), kernel_size, dilation, causal)
+    if scale is None:
+        scale = 1.0 / math.sqrt(D)
+    out = torch.empty_like(q) if out is None else out
+    lse = torch.empty(q.shape[:-1], dtype=torch.float32, device=q.device) if lse is None else lse
+    dq = torch.empty_like(q) if dq is None else dq
+    dk = torch.empty_like(k) if dk is None else dk
+    dv = torch.empty_like(v) if dv is None else dv
+    _check_tensors(q, out, dq, dk, dv)
+    bf, bb = _NaTiling(), _NaTiling()
+    times = (ctypes.c_float * 4)()
+    _check(lib.na_tune(rank, ext, ks, ds, cs, B, H, D, DTYPES[q.dtype], float(scale),
+                       q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(), lse.data_ptr(),
+                       dout.data_ptr(), dq.data_ptr(), dk.data_ptr(), dv.data_ptr(),
+                       int(repeats), _stream(q.device), ctypes.byref(bf), ctypes.byref(bb),
+                       times))
+    return Tiling._from_c(bf), Tiling._from_c(bb), list(times)
+
+
+def tune_clear():
+    """Forget every tiling na_tune recorded."""
+    load_library().na_tune_clear()
+
+
+def forward(q, k, v, kernel_size, dilation=1, scale=None, out=None, lse=None, causal=None,
+            tiling=None):
+    """Fused NA forward.  Returns (out, logsumexp); logsumexp is fp32 [B, H, X..].
+    tiling: an explicit Tiling (na_forward_tiled); None uses the cached or heuristic one."""
     lib = load_library()
     _check_tensors(q, k, v)
     B, H, D = q.shape[0], q.shape[1], q.shape[-1]
@@ -138,15 +240,20 @@ def forward(q, k, v, kernel_size, dilation=1, scale=None, out=None, lse=None, ca
     _check_tensors(q, out)
     if lse.dtype != torch.float32 or lse.shape != q.shape[:-1] or not lse.is_contiguous():
         raise ValueError("lse must be a contiguous fp32 tensor of shape q.shape[:-1]")
-    _check(lib.na_forward(rank, ext, ks, ds, cs, B, H, D, DTYPES[q.dtype], float(scale),
-                          q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(),
-                          lse.data_ptr(), _stream(q.device)))
+    args = (q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(), lse.data_ptr(),
+            _stream(q.device))
+    if tiling is None:
+        _check(lib.na_forward(rank, ext, ks, ds, cs, B, H, D, DTYPES[q.dtype], float(scale), *args))
+    else:
+        _check(lib.na_forward_tiled(rank, ext, ks, ds, cs, B, H, D, DTYPES[q.dtype], float(scale),
+                                    ctypes.byref(Tiling(*tiling)._c()), *args))
     return out, lse
 
 
 def backward(q, k, v, out, lse, dout, kernel_size, dilation=1, scale=None, dq=None, dk=None,
-             dv=None, causal=None):
-    """Fused NA backward.  Returns (dq, dk, dv)."""
+             dv=None, causal=None, tiling=None):
+    """Fused NA backward.  Returns (dq, dk, dv).
+    tiling: an explicit Tiling (na_backward_tiled); None uses the cached or heuristic one."""
     lib = load_library()
     _check_tensors(q, k, v, out, dout)
     B, H, D = q.shape[0], q.shape[1], q.shape[-1]
@@ -160,10 +267,14 @@ def backward(q, k, v, out, lse, dout, kernel_size, dilation=1, scale=None, dq=No
     dk = torch.empty_like(k) if dk is None else dk
     dv = torch.empty_like(v) if dv is None else dv
     _check_tensors(q, dq, dk, dv)
-    _check(lib.na_backward(rank, ext, ks, ds, cs, B, H, D, DTYPES[q.dtype], float(scale),
-                           q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(),
-                           lse.data_ptr(), dout.data_ptr(), dq.data_ptr(), dk.data_ptr(),
-                           dv.data_ptr(), _stream(q.device)))
+    args = (q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(), lse.data_ptr(),
+            dout.data_ptr(), dq.data_ptr(), dk.data_ptr(), dv.data_ptr(), _stream(q.device))
+    if tiling is None:
+        _check(lib.na_backward(rank, ext, ks, ds, cs, B, H, D, DTYPES[q.dtype], float(scale),
+                               *args))
+    else:
+        _check(lib.na_backward_tiled(rank, ext, ks, ds, cs, B, H, D, DTYPES[q.dtype],
+                                     float(scale), ctypes.byref(Tiling(*tiling)._c()), *args))
     return dq, dk, dv
 
 

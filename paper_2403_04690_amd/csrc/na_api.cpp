@@ -1,6 +1,7 @@
-// na_api.cpp -- the C ABI of libna.so: problem validation, tile selection and
-// kernel dispatch.  Everything before the launch is plain host code; no entry
-// point allocates, frees or synchronises.
+// na_api.cpp -- the C ABI of libna.so: problem validation, tile selection,
+// the tiling tuner and kernel dispatch.  Everything before the launch is plain
+// host code; no entry point allocates or frees device memory, and only
+// na_tune synchronises.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -8,13 +9,16 @@
 #include <cstdint>
 #include <cstdlib>
 #include <cstring>
+#include <map>
+#include <mutex>
+#include <vector>
 
 #include "na.h"
 #include "na_launch.h"
 
 namespace {
 
-constexpr int kVersion = 200;  // 0.2.0
+constexpr int kVersion = 300;  // 0.3.0
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
@@ -43,7 +47,12 @@ int64_t token_count(int rank, const int64_t* extents) {
 // Wave tile (queries or keys owned by one wave, 16 * m of them) along each
 // axis, sized from the innermost axis outwards and never longer than the
 // longest dilation group of an axis (rounded up to a power of two).
-void wave_tile(int rank, const int* glen, int m, int waves, int* wt, int* wgd) {
+// An inner window of 10 to 13 keys: a 4-wide wave tile keeps the union of its
+// windows along the inner axis inside one 16-key block, so each halo row is
+// one block instead of two (mask density 0.66 instead of 0.41 at k = 13).
+bool narrow_inner_tile(int rank, int k_inner) { return rank > 1 && k_inner >= 10 && k_inner <= 13; }
+
+void wave_tile(int rank, const int* glen, int m, int waves, int k_inner, int* wt, int* wgd) {
     const int q = 16 * m;
     for (int a = 0; a < 3; ++a) wt[a] = wgd[a] = 1;
     if (rank == 1) {
@@ -52,7 +61,7 @@ void wave_tile(int rank, const int* glen, int m, int waves, int* wt, int* wgd) {
         return;
     }
     const int inner = rank - 1;
-    const int cap = rank == 2 ? (m == 1 ? 8 : 16) : 8;
+    const int cap = narrow_inner_tile(rank, k_inner) ? 4 : rank == 2 ? (m == 1 ? 8 : 16) : 8;
     wt[inner] = std::min(cap, pow2ceil(glen[inner]));
     int rem = q / wt[inner];
     // hand out the remaining factor 2 at a time over the outer axes, outermost first
@@ -82,17 +91,25 @@ void wave_tile(int rank, const int* glen, int m, int waves, int* wt, int* wgd) {
     }
 }
 
-// Fills the geometry of a problem for wave tiles of 16 * m tokens.
-bool make_geo(int rank, const int64_t* extents, const int32_t* ks, const int32_t* ds,
-              const int32_t* causal, int64_t BH, int m, na::Geo& g, int waves = 4) {
+// Longest dilation group along each axis (inert axes: 1).
+void group_lengths(int rank, const int64_t* extents, const int32_t* ds, int* glen) {
+    for (int a = 0; a < 3; ++a)
+        glen[a] = a < rank ? na::group_len((int)extents[a], ds[a], 0) : 1;
+}
+
+// Fills the geometry of a problem for a tiling (validated by the caller).
+bool geo_from_tiling(int rank, const int64_t* extents, const int32_t* ks, const int32_t* ds,
+                     const int32_t* causal, int64_t BH, const na_tiling& t, na::Geo& g) {
     std::memset(&g, 0, sizeof(g));
-    int glen[3] = {1, 1, 1};
+    int glen[3];
+    group_lengths(rank, extents, ds, glen);
     for (int a = 0; a < 3; ++a) {
         g.L[a] = a < rank ? (int)extents[a] : 1;
         g.k[a] = a < rank ? ks[a] : 1;
         g.d[a] = a < rank ? ds[a] : 1;
         g.causal[a] = a < rank && causal && causal[a] ? 1 : 0;
-        glen[a] = na::group_len(g.L[a], g.d[a], 0);
+        g.WT[a] = t.wave_tile[a];
+        g.WGd[a] = t.waves[a];
     }
     {
         int s = 1;  // token strides of the problem's own axes (row-major)
@@ -106,7 +123,6 @@ bool make_geo(int rank, const int64_t* extents, const int32_t* ks, const int32_t
     g.BH = (int)BH;
     g.ngroups = 1;
     for (int a = 0; a < rank; ++a) g.ngroups *= g.d[a];
-    wave_tile(rank, glen, m, rank == 1 ? waves : 4, g.WT, g.WGd);
     int64_t ntiles = 1;
     for (int a = 0; a < 3; ++a) {
         g.T[a] = g.WT[a] * g.WGd[a];
@@ -128,6 +144,24 @@ bool make_geo(int rank, const int64_t* extents, const int32_t* ks, const int32_t
     return true;
 }
 
+// The heuristic tiling for wave tiles of 16 * m tokens and `waves` waves
+// (waves != 4 only for rank 1).
+na_tiling heuristic_tiling(int rank, const int64_t* extents, const int32_t* ks,
+                          const int32_t* ds, int m, int waves) {
+    int glen[3];
+    group_lengths(rank, extents, ds, glen);
+    na_tiling t;
+    t.blocks_per_wave = m;
+    wave_tile(rank, glen, m, rank == 1 ? waves : 4, ks[rank - 1], t.wave_tile, t.waves);
+    return t;
+}
+
+bool make_geo(int rank, const int64_t* extents, const int32_t* ks, const int32_t* ds,
+              const int32_t* causal, int64_t BH, int m, na::Geo& g, int waves = 4) {
+    return geo_from_tiling(rank, extents, ks, ds, causal, BH,
+                           heuristic_tiling(rank, extents, ks, ds, m, waves), g);
+}
+
 // Wave size multiplier: two 16-token blocks per wave unless that leaves the
 // GPU (256 CUs) with too few workgroups.  NA_WAVE_BLOCKS=1|2 overrides.
 int choose_m(int rank, const int64_t* extents, const int32_t* ks, const int32_t* ds, int64_t BH) {
@@ -135,6 +169,8 @@ int choose_m(int rank, const int64_t* extents, const int32_t* ks, const int32_t*
         const int v = std::atoi(env);
         if (v == 1 || v == 2) return v;
     }
+    // 4 x 4 wave tiles of narrow inner windows: two of them would share few rows
+    if (narrow_inner_tile(rank, ks[rank - 1])) return 1;
     na::Geo g;
     if (!make_geo(rank, extents, ks, ds, nullptr, BH, 2, g)) return 1;
     return g.nwg < 1024 ? 1 : 2;
@@ -177,6 +213,134 @@ bool empty_problem(int rank, const int64_t* extents, int64_t batch, int64_t head
     return batch == 0 || heads == 0 || token_count(rank, extents) == 0;
 }
 
+bool is_pow2(int x) { return x >= 1 && (x & (x - 1)) == 0; }
+
+// A tiling the kernels accept for this problem (see na_tiling).
+bool valid_tiling(int rank, na_dtype dtype, bool forward, const na_tiling& t) {
+    if (t.blocks_per_wave != 1 && t.blocks_per_wave != 2) return false;
+    int64_t pw = 1, pg = 1;
+    for (int a = 0; a < 3; ++a) {
+        const int wt = t.wave_tile[a], wg = t.waves[a];
+        if (!is_pow2(wt) || !is_pow2(wg) || wt > 4096) return false;
+        if (a >= rank && (wt != 1 || wg != 1)) return false;
+        pw *= wt;
+        pg *= wg;
+    }
+    if (pw != 16 * t.blocks_per_wave) return false;
+    if (pg == 4) return true;
+    // 8 waves: the 1-D forward of 16-bit types only
+    return pg == 8 && forward && rank == 1 && dtype != NA_FP32;
+}
+
+// Heuristic tilings of na_forward / na_backward.
+na_tiling default_forward_tiling(int rank, const int64_t* extents, const int32_t* ks,
+                                 const int32_t* ds, int64_t BH, na_dtype dtype) {
+    const int m = choose_m(rank, extents, ks, ds, BH);
+    na::Geo g4;
+    int waves = 4;
+    if (make_geo(rank, extents, ks, ds, nullptr, BH, m, g4)) waves = forward_waves(rank, dtype, g4);
+    return heuristic_tiling(rank, extents, ks, ds, m, waves);
+}
+
+na_tiling default_backward_tiling(int rank, const int64_t* extents, const int32_t* ks,
+                                  const int32_t* ds, int64_t BH) {
+    return heuristic_tiling(rank, extents, ks, ds, choose_m(rank, extents, ks, ds, BH), 4);
+}
+
+// ---- tiling cache (filled by na_tune) ----
+struct Tuned {
+    bool has_fwd = false, has_bwd = false;
+    na_tiling fwd{}, bwd{};
+};
+std::mutex g_cache_mu;
+std::map<std::vector<int64_t>, Tuned>& tiling_cache() {
+    static std::map<std::vector<int64_t>, Tuned> cache;
+    return cache;
+}
+
+std::vector<int64_t> problem_key(int rank, const int64_t* extents, const int32_t* ks,
+                                 const int32_t* ds, const int32_t* causal, int64_t BH,
+                                 int64_t head_dim, na_dtype dtype) {
+    std::vector<int64_t> key = {rank, BH, head_dim, (int64_t)dtype};
+    for (int a = 0; a < rank; ++a) {
+        key.push_back(extents[a]);
+        key.push_back(ks[a]);
+        key.push_back(ds[a]);
+        key.push_back(causal && causal[a] ? 1 : 0);
+    }
+    return key;
+}
+
+na_tiling current_tiling(int rank, const int64_t* extents, const int32_t* ks, const int32_t* ds,
+                         const int32_t* causal, int64_t BH, int64_t head_dim, na_dtype dtype,
+                         bool forward) {
+    {
+        std::lock_guard<std::mutex> lock(g_cache_mu);
+        auto& cache = tiling_cache();
+        auto it = cache.find(problem_key(rank, extents, ks, ds, causal, BH, head_dim, dtype));
+        if (it != cache.end()) {
+            if (forward && it->second.has_fwd) return it->second.fwd;
+            if (!forward && it->second.has_bwd) return it->second.bwd;
+        }
+    }
+    return forward ? default_forward_tiling(rank, extents, ks, ds, BH, dtype)
+                   : default_backward_tiling(rank, extents, ks, ds, BH);
+}
+
+bool same_tiling(const na_tiling& a, const na_tiling& b) {
+    if (a.blocks_per_wave != b.blocks_per_wave) return false;
+    for (int i = 0; i < 3; ++i)
+        if (a.wave_tile[i] != b.wave_tile[i] || a.waves[i] != b.waves[i]) return false;
+    return true;
+}
+
+// Candidate tilings: the heuristic one, then every valid factorisation
+// whose workgroup tile is no longer than twice an axis's longest group
+// (rounded up to a power of two) and whose wave tile along the innermost
+// axis is at least 4 (2-D, 3-D), at most kMaxCandidates in all.
+constexpr int kMaxCandidates = 64;
+std::vector<na_tiling> candidates(int rank, const int64_t* extents, const int32_t* ks,
+                                  const int32_t* ds, int64_t BH, na_dtype dtype, bool forward) {
+    std::vector<na_tiling> out;
+    out.push_back(forward ? default_forward_tiling(rank, extents, ks, ds, BH, dtype)
+                          : default_backward_tiling(rank, extents, ks, ds, BH));
+    int glen[3];
+    group_lengths(rank, extents, ds, glen);
+    const int maxwg = forward && rank == 1 && dtype != NA_FP32 ? 8 : 4;
+    for (int m = 1; m <= 2; ++m) {
+        const int q = 16 * m;
+        for (int w0 = 1; w0 <= q; w0 *= 2)
+            for (int w1 = 1; w1 <= (rank > 1 ? q : 1); w1 *= 2)
+                for (int w2 = 1; w2 <= (rank > 2 ? q : 1); w2 *= 2) {
+                    if (w0 * w1 * w2 != q) continue;
+                    const int wt[3] = {w0, w1, w2};
+                    if (rank > 1 && wt[rank - 1] < 4) continue;
+                    for (int p = 4; p <= maxwg; p *= 2)
+                        for (int g0 = 1; g0 <= p; g0 *= 2)
+                            for (int g1 = 1; g1 <= (rank > 1 ? p : 1); g1 *= 2)
+                                for (int g2 = 1; g2 <= (rank > 2 ? p : 1); g2 *= 2) {
+                                    if (g0 * g1 * g2 != p) continue;
+                                    const int wg[3] = {g0, g1, g2};
+                                    na_tiling t;
+                                    t.blocks_per_wave = m;
+                                    bool ok = true;
+                                    for (int a = 0; a < 3; ++a) {
+                                        t.wave_tile[a] = wt[a];
+                                        t.waves[a] = wg[a];
+                                        if (a < rank && wt[a] * wg[a] > 2 * pow2ceil(glen[a]) &&
+                                            !(rank == 1 && wg[a] == 4))
+                                            ok = false;
+                                    }
+                                    if (!ok || !valid_tiling(rank, dtype, forward, t)) continue;
+                                    bool dup = false;
+                                    for (const auto& c : out) dup = dup || same_tiling(c, t);
+                                    if (!dup && (int)out.size() < kMaxCandidates) out.push_back(t);
+                                }
+                }
+    }
+    return out;
+}
+
 }  // namespace
 
 extern "C" {
@@ -195,6 +359,7 @@ const char* na_status_string(na_status status) {
         case NA_ERR_ALIGNMENT: return "device pointers must be 16-byte aligned";
         case NA_ERR_HIP: return "HIP launch failed";
         case NA_ERR_SCALE: return "scale must be finite";
+        case NA_ERR_TILING: return "the tiling is not valid for this problem";
     }
     return "unknown status";
 }
@@ -209,6 +374,56 @@ na_status na_validate(int rank, const int64_t* extents, const int32_t* kernel_si
                          scale);
 }
 
+}  // extern "C"
+
+namespace {
+
+// Launchers for a validated, non-empty problem with checked pointers.
+na_status run_forward(int rank, const int64_t* extents, const int32_t* ks, const int32_t* ds,
+                      const int32_t* causal, int64_t BH, int64_t head_dim, na_dtype dtype,
+                      float scale, const na_tiling& t, const void* q, const void* k,
+                      const void* v, void* out, float* lse, hipStream_t s) {
+    na::Geo g;
+    if (!geo_from_tiling(rank, extents, ks, ds, causal, BH, t, g)) return NA_ERR_SHAPE;
+    hipError_t e = na::launch_forward(g, rank, (int)head_dim, (int)dtype, t.blocks_per_wave, q, k,
+                                      v, out, lse, scale, s);
+    return e == hipSuccess ? NA_OK : NA_ERR_HIP;
+}
+
+na_status run_backward(int rank, const int64_t* extents, const int32_t* ks, const int32_t* ds,
+                       const int32_t* causal, int64_t BH, int64_t head_dim, na_dtype dtype,
+                       float scale, const na_tiling& t, const void* q, const void* k,
+                       const void* v, const void* out, const float* lse, const void* dout,
+                       void* dq, void* dk, void* dv, hipStream_t s) {
+    na::Geo g;
+    if (!geo_from_tiling(rank, extents, ks, ds, causal, BH, t, g)) return NA_ERR_SHAPE;
+    hipError_t e = na::launch_backward(g, rank, (int)head_dim, (int)dtype, t.blocks_per_wave, q,
+                                       k, v, out, lse, dout, dq, dk, dv, scale, s);
+    return e == hipSuccess ? NA_OK : NA_ERR_HIP;
+}
+
+na_status forward_pointers(const void* q, const void* k, const void* v, const void* out,
+                           const float* lse) {
+    if (!q || !k || !v || !out || !lse) return NA_ERR_NULL;
+    if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(out) || !aligned16(lse))
+        return NA_ERR_ALIGNMENT;
+    return NA_OK;
+}
+
+na_status backward_pointers(const void* q, const void* k, const void* v, const void* out,
+                            const float* lse, const void* dout, const void* dq, const void* dk,
+                            const void* dv) {
+    if (!q || !k || !v || !out || !lse || !dout || !dq || !dk || !dv) return NA_ERR_NULL;
+    const void* ptrs[] = {q, k, v, out, lse, dout, dq, dk, dv};
+    for (const void* p : ptrs)
+        if (!aligned16(p)) return NA_ERR_ALIGNMENT;
+    return NA_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
 na_status na_forward(int rank, const int64_t* extents, const int32_t* kernel_size,
                      const int32_t* dilation, const int32_t* causal, int64_t batch, int64_t heads,
                      int64_t head_dim, na_dtype dtype, float scale, const void* q, const void* k,
@@ -217,20 +432,13 @@ na_status na_forward(int rank, const int64_t* extents, const int32_t* kernel_siz
                                  dtype, scale);
     if (st != NA_OK) return st;
     if (empty_problem(rank, extents, batch, heads)) return NA_OK;
-    if (!q || !k || !v || !out || !logsumexp) return NA_ERR_NULL;
-    if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(out) ||
-        !aligned16(logsumexp))
-        return NA_ERR_ALIGNMENT;
+    st = forward_pointers(q, k, v, out, logsumexp);
+    if (st != NA_OK) return st;
     const int64_t BH = batch * heads;
-    const int m = choose_m(rank, extents, kernel_size, dilation, BH);
-    na::Geo g;
-    if (!make_geo(rank, extents, kernel_size, dilation, causal, BH, m, g)) return NA_ERR_SHAPE;
-    if (forward_waves(rank, dtype, g) == 8 &&
-        !make_geo(rank, extents, kernel_size, dilation, causal, BH, m, g, 8))
-        return NA_ERR_SHAPE;
-    hipError_t e = na::launch_forward(g, rank, (int)head_dim, (int)dtype, m, q, k, v, out,
-                                      logsumexp, scale, reinterpret_cast<hipStream_t>(stream));
-    return e == hipSuccess ? NA_OK : NA_ERR_HIP;
+    const na_tiling t = current_tiling(rank, extents, kernel_size, dilation, causal, BH, head_dim,
+                                       dtype, true);
+    return run_forward(rank, extents, kernel_size, dilation, causal, BH, head_dim, dtype, scale, t,
+                       q, k, v, out, logsumexp, reinterpret_cast<hipStream_t>(stream));
 }
 
 na_status na_backward(int rank, const int64_t* extents, const int32_t* kernel_size,
@@ -242,18 +450,197 @@ na_status na_backward(int rank, const int64_t* extents, const int32_t* kernel_si
                                  dtype, scale);
     if (st != NA_OK) return st;
     if (empty_problem(rank, extents, batch, heads)) return NA_OK;
-    if (!q || !k || !v || !out || !logsumexp || !dout || !dq || !dk || !dv) return NA_ERR_NULL;
-    const void* ptrs[] = {q, k, v, out, logsumexp, dout, dq, dk, dv};
-    for (const void* p : ptrs)
-        if (!aligned16(p)) return NA_ERR_ALIGNMENT;
+    st = backward_pointers(q, k, v, out, logsumexp, dout, dq, dk, dv);
+    if (st != NA_OK) return st;
     const int64_t BH = batch * heads;
-    const int m = choose_m(rank, extents, kernel_size, dilation, BH);
-    na::Geo g;
-    if (!make_geo(rank, extents, kernel_size, dilation, causal, BH, m, g)) return NA_ERR_SHAPE;
-    hipError_t e = na::launch_backward(g, rank, (int)head_dim, (int)dtype, m, q, k, v, out,
-                                       logsumexp, dout, dq, dk, dv, scale,
-                                       reinterpret_cast<hipStream_t>(stream));
-    return e == hipSuccess ? NA_OK : NA_ERR_HIP;
+    const na_tiling t = current_tiling(rank, extents, kernel_size, dilation, causal, BH, head_dim,
+                                       dtype, false);
+    return run_backward(rank, extents, kernel_size, dilation, causal, BH, head_dim, dtype, scale,
+                        t, q, k, v, out, logsumexp, dout, dq, dk, dv,
+                        reinterpret_cast<hipStream_t>(stream));
+}
+
+int na_candidate_tilings(int rank, const int64_t* extents, const int32_t* kernel_size,
+                         const int32_t* dilation, int64_t batch, int64_t heads, int64_t head_dim,
+                         na_dtype dtype, int forward, na_tiling* out, int max) {
+    na_status st = check_problem(rank, extents, kernel_size, dilation, batch, heads, head_dim,
+                                 dtype, 1.0f);
+    if (st != NA_OK) return -(int)st;
+    const auto c = candidates(rank, extents, kernel_size, dilation, batch * heads, dtype,
+                              forward != 0);
+    for (int i = 0; i < (int)c.size() && i < max && out; ++i) out[i] = c[i];
+    return (int)c.size();
+}
+
+na_status na_current_tiling(int rank, const int64_t* extents, const int32_t* kernel_size,
+                            const int32_t* dilation, const int32_t* causal, int64_t batch,
+                            int64_t heads, int64_t head_dim, na_dtype dtype, int forward,
+                            na_tiling* out) {
+    na_status st = check_problem(rank, extents, kernel_size, dilation, batch, heads, head_dim,
+                                 dtype, 1.0f);
+    if (st != NA_OK) return st;
+    if (!out) return NA_ERR_NULL;
+    *out = current_tiling(rank, extents, kernel_size, dilation, causal, batch * heads, head_dim,
+                          dtype, forward != 0);
+    return NA_OK;
+}
+
+na_status na_forward_tiled(int rank, const int64_t* extents, const int32_t* kernel_size,
+                           const int32_t* dilation, const int32_t* causal, int64_t batch,
+                           int64_t heads, int64_t head_dim, na_dtype dtype, float scale,
+                           const na_tiling* tiling, const void* q, const void* k, const void* v,
+                           void* out, float* logsumexp, na_stream_t stream) {
+    na_status st = check_problem(rank, extents, kernel_size, dilation, batch, heads, head_dim,
+                                 dtype, scale);
+    if (st != NA_OK) return st;
+    if (!tiling) return NA_ERR_NULL;
+    if (!valid_tiling(rank, dtype, true, *tiling)) return NA_ERR_TILING;
+    if (empty_problem(rank, extents, batch, heads)) return NA_OK;
+    st = forward_pointers(q, k, v, out, logsumexp);
+    if (st != NA_OK) return st;
+    return run_forward(rank, extents, kernel_size, dilation, causal, batch * heads, head_dim,
+                       dtype, scale, *tiling, q, k, v, out, logsumexp,
+                       reinterpret_cast<hipStream_t>(stream));
+}
+
+na_status na_backward_tiled(int rank, const int64_t* extents, const int32_t* kernel_size,
+                            const int32_t* dilation, const int32_t* causal, int64_t batch,
+                            int64_t heads, int64_t head_dim, na_dtype dtype, float scale,
+                            const na_tiling* tiling, const void* q, const void* k, const void* v,
+                            const void* out, const float* logsumexp, const void* dout, void* dq,
+                            void* dk, void* dv, na_stream_t stream) {
+    na_status st = check_problem(rank, extents, kernel_size, dilation, batch, heads, head_dim,
+                                 dtype, scale);
+    if (st != NA_OK) return st;
+    if (!tiling) return NA_ERR_NULL;
+    if (!valid_tiling(rank, dtype, false, *tiling)) return NA_ERR_TILING;
+    if (empty_problem(rank, extents, batch, heads)) return NA_OK;
+    st = backward_pointers(q, k, v, out, logsumexp, dout, dq, dk, dv);
+    if (st != NA_OK) return st;
+    return run_backward(rank, extents, kernel_size, dilation, causal, batch * heads, head_dim,
+                        dtype, scale, *tiling, q, k, v, out, logsumexp, dout, dq, dk, dv,
+                        reinterpret_cast<hipStream_t>(stream));
+}
+
+na_status na_tune(int rank, const int64_t* extents, const int32_t* kernel_size,
+                  const int32_t* dilation, const int32_t* causal, int64_t batch, int64_t heads,
+                  int64_t head_dim, na_dtype dtype, float scale, const void* q, const void* k,
+                  const void* v, void* out, float* logsumexp, const void* dout, void* dq, void* dk,
+                  void* dv, int repeats, na_stream_t stream, na_tiling* best_forward,
+                  na_tiling* best_backward, float* times_ms) {
+    na_status st = check_problem(rank, extents, kernel_size, dilation, batch, heads, head_dim,
+                                 dtype, scale);
+    if (st != NA_OK) return st;
+    const int64_t BH = batch * heads;
+    na_tiling bf = default_forward_tiling(rank, extents, kernel_size, dilation, BH, dtype);
+    na_tiling bb = default_backward_tiling(rank, extents, kernel_size, dilation, BH);
+    float tm[4] = {0.f, 0.f, 0.f, 0.f};
+    if (!empty_problem(rank, extents, batch, heads)) {
+        st = backward_pointers(q, k, v, out, logsumexp, dout, dq, dk, dv);
+        if (st != NA_OK) return st;
+        const int reps = repeats < 1 ? 1 : repeats;
+        hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+        hipEvent_t e0 = nullptr, e1 = nullptr;
+        if (hipEventCreate(&e0) != hipSuccess || hipEventCreate(&e1) != hipSuccess) {
+            if (e0) (void)hipEventDestroy(e0);
+            return NA_ERR_HIP;
+        }
+        // ms per launch of `launch` (one warm-up launch first), or < 0 on failure
+        auto time_it = [&](auto launch) -> float {
+            if (launch() != NA_OK) return -1.f;
+            if (hipEventRecord(e0, s) != hipSuccess) return -1.f;
+            for (int r = 0; r < reps; ++r)
+                if (launch() != NA_OK) return -1.f;
+            float ms = 0.f;
+            if (hipEventRecord(e1, s) != hipSuccess || hipEventSynchronize(e1) != hipSuccess ||
+                hipEventElapsedTime(&ms, e0, e1) != hipSuccess)
+                return -1.f;
+            return ms / reps;
+        };
+        // Picks a tiling: every candidate timed once, then the three fastest and
+        // the heuristic (candidate 0) timed again back to back; the heuristic
+        // stays unless another finalist beats it by more than 2 %.  A warm-up
+        // of the heuristic comes first, so no candidate pays for a cold GPU.
+        auto pick = [&](const std::vector<na_tiling>& c, auto launch, na_tiling& chosen,
+                        float& t_best, float& t_heur) -> na_status {
+            for (int r = 0; r < 3 * reps; ++r)
+                if (launch(c[0]) != NA_OK) return NA_ERR_HIP;
+            std::vector<float> t1(c.size());
+            for (size_t i = 0; i < c.size(); ++i) {
+                t1[i] = time_it([&] { return launch(c[i]); });
+                if (t1[i] < 0.f) return NA_ERR_HIP;
+            }
+            std::vector<size_t> order(c.size());
+            for (size_t i = 0; i < c.size(); ++i) order[i] = i;
+            std::sort(order.begin(), order.end(), [&](size_t a, size_t b) { return t1[a] < t1[b]; });
+            std::vector<size_t> fin = {0};
+            for (size_t j = 0; j < order.size() && fin.size() < 4; ++j)
+                if (order[j] != 0) fin.push_back(order[j]);
+            size_t best = 0;
+            float tb = -1.f;
+            for (size_t i : fin) {
+                const float t = time_it([&] { return launch(c[i]); });
+                if (t < 0.f) return NA_ERR_HIP;
+                if (i == 0) t_heur = t;
+                if (tb < 0.f || t < tb) {
+                    tb = t;
+                    best = i;
+                }
+            }
+            if (best != 0 && tb > 0.98f * t_heur) {
+                best = 0;
+                tb = t_heur;
+            }
+            chosen = c[best];
+            t_best = tb;
+            return NA_OK;
+        };
+        const auto fc = candidates(rank, extents, kernel_size, dilation, BH, dtype, true);
+        st = pick(
+            fc,
+            [&](const na_tiling& t) {
+                return run_forward(rank, extents, kernel_size, dilation, causal, BH, head_dim,
+                                   dtype, scale, t, q, k, v, out, logsumexp, s);
+            },
+            bf, tm[0], tm[2]);
+        // out and logsumexp from the chosen forward, then the backward tilings
+        if (st == NA_OK)
+            st = run_forward(rank, extents, kernel_size, dilation, causal, BH, head_dim, dtype,
+                             scale, bf, q, k, v, out, logsumexp, s);
+        const auto bc = candidates(rank, extents, kernel_size, dilation, BH, dtype, false);
+        if (st == NA_OK)
+            st = pick(
+                bc,
+                [&](const na_tiling& t) {
+                    return run_backward(rank, extents, kernel_size, dilation, causal, BH,
+                                        head_dim, dtype, scale, t, q, k, v, out, logsumexp, dout,
+                                        dq, dk, dv, s);
+                },
+                bb, tm[1], tm[3]);
+        if (st == NA_OK)
+            st = run_backward(rank, extents, kernel_size, dilation, causal, BH, head_dim, dtype,
+                              scale, bb, q, k, v, out, logsumexp, dout, dq, dk, dv, s);
+        if (st == NA_OK && hipStreamSynchronize(s) != hipSuccess) st = NA_ERR_HIP;
+        (void)hipEventDestroy(e0);
+        (void)hipEventDestroy(e1);
+        if (st != NA_OK) return st;
+        std::lock_guard<std::mutex> lock(g_cache_mu);
+        Tuned& e = tiling_cache()[problem_key(rank, extents, kernel_size, dilation, causal, BH,
+                                              head_dim, dtype)];
+        e.has_fwd = e.has_bwd = true;
+        e.fwd = bf;
+        e.bwd = bb;
+    }
+    if (best_forward) *best_forward = bf;
+    if (best_backward) *best_backward = bb;
+    if (times_ms)
+        for (int i = 0; i < 4; ++i) times_ms[i] = tm[i];
+    return NA_OK;
+}
+
+void na_tune_clear(void) {
+    std::lock_guard<std::mutex> lock(g_cache_mu);
+    tiling_cache().clear();
 }
 
 na_status na_debug_windows(int rank, const int64_t* extents, const int32_t* kernel_size,

@@ -140,3 +140,93 @@ def test_debug_windows_rejects_before_launch(lib):
     assert lib.na_debug_windows(r, e, k, d, None, FAKE, FAKE, FAKE, None) == NA_ERR_WINDOW
     r, e, k, d = _args()
     assert lib.na_debug_windows(r, e, k, d, None, None, FAKE, FAKE, None) == NA_ERR_NULL
+
+
+# ---------------------------------------------------------------- tilings
+NA_ERR_TILING = 13
+
+
+def _tiling_type():
+    import paper_2403_04690_amd as na
+
+    return na._NaTiling  # the na_tiling struct the binding declared the entry points with
+
+
+TILING_PROBLEMS = [
+    # (extents, kernel, dilation, head_dim, dtype code)
+    ((56, 56), (7, 7), (1, 1), 32, 1),
+    ((16, 64, 64), (7, 7, 7), (1, 2, 2), 64, 1),
+    ((32768,), (1023,), (4,), 64, 1),
+    ((256,), (7,), (1,), 32, 0),
+    ((128, 128), (13, 13), (2, 2), 64, 2),
+    ((5, 9, 11), (5, 3, 3), (1, 3, 3), 32, 0),
+]
+
+
+def _pow2(x):
+    return x >= 1 and x & (x - 1) == 0
+
+
+@pytest.mark.parametrize("ext,ks,ds,D,dt", TILING_PROBLEMS)
+@pytest.mark.parametrize("fwd", [1, 0])
+def test_candidate_tilings_are_valid_and_start_with_the_heuristic(lib, ext, ks, ds, D, dt, fwd):
+    _Tiling = _tiling_type()
+    rank = len(ext)
+    r, e, k, d = _args(rank, ext, ks, ds)
+    n = lib.na_candidate_tilings(r, e, k, d, 2, 4, D, dt, fwd, None, 0)
+    assert 1 <= n <= 64
+    buf = (_Tiling * n)()
+    assert lib.na_candidate_tilings(r, e, k, d, 2, 4, D, dt, fwd, buf, n) == n
+    seen = set()
+    for t in buf:
+        wt, wg = tuple(t.wave_tile), tuple(t.waves)
+        assert t.blocks_per_wave in (1, 2)
+        assert all(_pow2(x) for x in wt + wg)
+        assert all(wt[a] == 1 and wg[a] == 1 for a in range(rank, 3))
+        assert wt[0] * wt[1] * wt[2] == 16 * t.blocks_per_wave
+        p = wg[0] * wg[1] * wg[2]
+        assert p == 4 or (p == 8 and fwd and rank == 1 and dt != 0)
+        key = (t.blocks_per_wave, wt, wg)
+        assert key not in seen
+        seen.add(key)
+    cur = _Tiling()
+    assert lib.na_current_tiling(r, e, k, d, None, 2, 4, D, dt, fwd, ctypes.byref(cur)) == NA_OK
+    assert (cur.blocks_per_wave, tuple(cur.wave_tile), tuple(cur.waves)) == \
+        (buf[0].blocks_per_wave, tuple(buf[0].wave_tile), tuple(buf[0].waves))
+
+
+def _tiling(m, wt, wg):
+    return _tiling_type()(m, (ctypes.c_int32 * 3)(*wt), (ctypes.c_int32 * 3)(*wg))
+
+
+@pytest.mark.parametrize("t,rank", [
+    ((3, (16, 1, 1), (4, 1, 1)), 1),    # blocks per wave
+    ((1, (8, 1, 1), (4, 1, 1)), 1),     # wave tile product != 16
+    ((1, (2, 8, 1), (2, 1, 1)), 2),     # waves product 2
+    ((1, (2, 8, 1), (8, 1, 1)), 2),     # 8 waves outside the 1-D forward
+    ((1, (3, 8, 1), (4, 1, 1)), 2),     # not a power of two
+    ((1, (2, 8, 2), (4, 1, 1)), 2),     # axis beyond the rank
+    ((1, (16, 1, 1), (8, 1, 1)), 1),    # 8 waves in fp32
+])
+def test_tiled_entry_points_reject_invalid_tilings(lib, t, rank):
+    ext, ks, ds = ((10, 12), (3, 5), (2, 1)) if rank == 2 else ((40,), (3,), (2,))
+    r, e, k, d = _args(rank, ext, ks, ds)
+    dt = 0 if t[2][0] == 8 and rank == 1 else 1
+    tl = _tiling(*t)
+    fake = ctypes.c_void_p(4096)  # never dereferenced: validation fails first
+    assert lib.na_forward_tiled(r, e, k, d, None, 2, 3, 64, dt, 0.125, ctypes.byref(tl),
+                                *([fake] * 5), None) == NA_ERR_TILING
+    if t[2][0] != 8:
+        assert lib.na_backward_tiled(r, e, k, d, None, 2, 3, 64, dt, 0.125, ctypes.byref(tl),
+                                     *([fake] * 9), None) == NA_ERR_TILING
+    assert lib.na_forward_tiled(r, e, k, d, None, 2, 3, 64, dt, 0.125, None,
+                                *([fake] * 5), None) == NA_ERR_NULL
+
+
+def test_tiling_status_string_and_cache_clear(lib):
+    assert b"tiling" in lib.na_status_string(NA_ERR_TILING)
+    lib.na_tune_clear()  # empty cache: the current tiling is the heuristic one
+    r, e, k, d = _args()
+    cur = _tiling_type()()
+    assert lib.na_current_tiling(r, e, k, d, None, 2, 3, 64, 1, 1, ctypes.byref(cur)) == NA_OK
+    assert cur.blocks_per_wave in (1, 2)

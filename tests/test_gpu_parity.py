@@ -431,3 +431,68 @@ def test_max_tokens_times_head_dim(na):
         assert max(e) <= TOL["fp16"]
     del q, k, v, g, out, lse, dq, dk, dv
     torch.cuda.empty_cache()
+
+
+# ---------------------------------------------------------------- tilings and the tuner
+TILING_CASES = [
+    # (extents, kernel, dilation, causal, head_dim, dtype, batch, heads)
+    ((37, 45), (7, 5), (2, 1), None, 32, "fp16", 2, 2),
+    ((6, 20, 22), (3, 7, 5), (1, 2, 2), None, 64, "fp16", 1, 2),
+    ((300,), (13,), (3,), None, 64, "bf16", 2, 2),
+    ((17, 33), (5, 9), (1, 2), (True, False), 64, "bf16", 1, 2),
+    ((5, 9, 11), (5, 3, 3), (1, 3, 3), None, 32, "fp32", 2, 1),
+]
+
+
+@pytest.mark.parametrize("ext,ks,ds,cs,D,dtype,B,H", TILING_CASES)
+def test_every_candidate_tiling_matches_the_oracle(na, ext, ks, ds, cs, D, dtype, B, H):
+    shape = (B, H) + ext + (D,)
+    q, k, v, g = _inputs(shape, dtype, 41, 4)
+    dq_, dk_, dv_, dg_ = _dev(q, k, v, g)
+    sc = 1.0 / math.sqrt(D)
+    ro, rl = oracle.forward(_f64(q), _f64(k), _f64(v), ks, ds, sc, causal=cs)
+    rq, rk, rv = oracle.backward(_f64(q), _f64(k), _f64(v), _f64(g), ks, ds, sc, causal=cs)
+    fwd_c = na.candidate_tilings(ext, ks, ds, B, H, D, TDT[dtype], forward=True)
+    bwd_c = na.candidate_tilings(ext, ks, ds, B, H, D, TDT[dtype], forward=False)
+    worst = 0.0
+    for t in fwd_c:
+        out, lse = na.forward(dq_, dk_, dv_, ks, ds, causal=cs, tiling=t)
+        e = max(_maxerr(out, ro), _maxerr(lse, rl))
+        assert e <= TOL[dtype], (t, e)
+        worst = max(worst, e)
+    out, lse = na.forward(dq_, dk_, dv_, ks, ds, causal=cs)
+    for t in bwd_c:
+        dq, dk, dv = na.backward(dq_, dk_, dv_, out, lse, dg_, ks, ds, causal=cs, tiling=t)
+        e = max(_maxerr(dq, rq), _maxerr(dk, rk), _maxerr(dv, rv))
+        assert e <= TOL[dtype], (t, e)
+        worst = max(worst, e)
+    _log(f"tilings {ext} k={ks} d={ds} c={cs} D={D} {dtype}: {len(fwd_c)} forward and "
+         f"{len(bwd_c)} backward tilings, worst max err {worst:.3g}")
+
+
+def test_tune_records_the_fastest_tilings_and_keeps_parity(na):
+    ext, ks, ds, D, dtype, B, H = (40, 48), (7, 7), (1, 1), 32, "fp16", 2, 4
+    shape = (B, H) + ext + (D,)
+    q, k, v, g = _inputs(shape, dtype, 43, 4)
+    dq_, dk_, dv_, dg_ = _dev(q, k, v, g)
+    sc = 1.0 / math.sqrt(D)
+    na.tune_clear()
+    heur_f = na.current_tiling(ext, ks, ds, B, H, D, TDT[dtype], forward=True)
+    bf, bb, times = na.tune(dq_, dk_, dv_, dg_, ks, ds, repeats=3)
+    try:
+        assert bf in na.candidate_tilings(ext, ks, ds, B, H, D, TDT[dtype], forward=True)
+        assert bb in na.candidate_tilings(ext, ks, ds, B, H, D, TDT[dtype], forward=False)
+        assert na.current_tiling(ext, ks, ds, B, H, D, TDT[dtype], forward=True) == bf
+        assert na.current_tiling(ext, ks, ds, B, H, D, TDT[dtype], forward=False) == bb
+        assert 0 < times[0] <= times[2] and 0 < times[1] <= times[3]
+        ro, rl = oracle.forward(_f64(q), _f64(k), _f64(v), ks, ds, sc)
+        rq, rk, rv = oracle.backward(_f64(q), _f64(k), _f64(v), _f64(g), ks, ds, sc)
+        out, lse = na.forward(dq_, dk_, dv_, ks, ds)  # the tuned tiling
+        dq, dk, dv = na.backward(dq_, dk_, dv_, out, lse, dg_, ks, ds)
+        e = [_maxerr(out, ro), _maxerr(lse, rl), _maxerr(dq, rq), _maxerr(dk, rk),
+             _maxerr(dv, rv)]
+        _log(f"tuned {bf} / {bb}, ms {times}: max err {e}")
+        assert max(e) <= TOL[dtype]
+    finally:
+        na.tune_clear()
+    assert na.current_tiling(ext, ks, ds, B, H, D, TDT[dtype], forward=True) == heur_f
