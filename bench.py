@@ -11,7 +11,9 @@ listed too).  The reported value is the forward's useful throughput,
 
 A "cold" forward figure is measured beside it: single launches, each after a
 512 MiB write that evicts the inputs from L2 and the MALL, timed one by one
-with events (which adds the event overhead of one launch).
+with events (which adds the event overhead of one launch).  So are the K
+forwards and K backwards replayed from HIP graphs (fwd_ms_graph,
+bwd_ms_graph), as a serving loop that captures its launches would run them.
 
 Prints one JSON line.  --gpus above 1 is refused: this build runs on one GPU.
 """
@@ -132,6 +134,8 @@ def main():
     ap.add_argument("--workload", default=WORKLOAD, choices=workloads.CONFIG_ORDER,
                     help="profiling aid: run the same step on another workload (the reported "
                          "line is defined on the default one)")
+    ap.add_argument("--no-graphs", dest="graphs", action="store_false",
+                    help="skip the HIP-graph replay side measurement")
     ap.add_argument("--tune", action="store_true",
                     help="run the library's tiling tuner (na_tune) on the workload before the "
                          "timed regions, so they use the tuned tilings")
@@ -246,6 +250,33 @@ def main():
         bwd_reps.append(timed(bwd))
     step_ms, fwd_ms, bwd_ms = median(step_reps), median(fwd_reps), median(bwd_reps)
 
+    # The same K forwards and K backwards replayed from HIP graphs (what a
+    # serving loop that captures its launches would see); context only.
+    def graph_ms(fn):
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.stream(side):
+            fn()
+            torch.cuda.synchronize()
+            with torch.cuda.graph(graph, stream=side):
+                for _ in range(K):
+                    fn()
+        torch.cuda.synchronize()
+        ts = []
+        for _ in range(reps):
+            g0, g1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            g0.record()
+            graph.replay()
+            g1.record()
+            torch.cuda.synchronize()
+            ts.append(g0.elapsed_time(g1) / K)
+        del graph
+        return median(ts)
+
+    fwd_graph_ms = graph_ms(fwd) if args.graphs else None
+    bwd_graph_ms = graph_ms(bwd) if args.graphs else None
+
     # Cold forward: each launch after a write of 512 MiB (beyond L2 and the
     # 256 MiB MALL), so Q, K and V come from HBM.
     cold_ms = None
@@ -301,6 +332,8 @@ def main():
         "bwd_ms_reps": [round(t, 5) for t in bwd_reps],
         "step_ms_reps": [round(t, 5) for t in step_reps],
         "fwd_ms_cold": None if cold_ms is None else round(cold_ms, 5),
+        "fwd_ms_graph": None if fwd_graph_ms is None else round(fwd_graph_ms, 5),
+        "bwd_ms_graph": None if bwd_graph_ms is None else round(bwd_graph_ms, 5),
         "tuned": tuning,
         "host_enqueue_ms_per_step": round(host_step_s * 1e3, 4),
         "mfma_peak_frac": round(fwd_tflops / PEAK_FP16_TFLOPS, 5),

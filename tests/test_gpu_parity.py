@@ -496,3 +496,39 @@ def test_tune_records_the_fastest_tilings_and_keeps_parity(na):
     finally:
         na.tune_clear()
     assert na.current_tiling(ext, ks, ds, B, H, D, TDT[dtype], forward=True) == heur_f
+
+
+def test_graph_capture_replays_match_eager(na):
+    """Forward and backward captured in one HIP graph replay the eager results bit for bit,
+    replay after replay, with eager work on the same buffers in between."""
+    ext, ks, ds, D, dtype, B, H = (24, 40), (7, 5), (1, 2), 32, "fp16", 2, 2
+    shape = (B, H) + ext + (D,)
+    q, k, v, g = _dev(*_inputs(shape, dtype, 47, 4))
+    out, lse = torch.empty_like(q), torch.empty(q.shape[:-1], dtype=torch.float32, device="cuda")
+    dq, dk, dv = torch.empty_like(q), torch.empty_like(q), torch.empty_like(q)
+
+    def step():
+        na.forward(q, k, v, ks, ds, out=out, lse=lse)
+        na.backward(q, k, v, out, lse, g, ks, ds, dq=dq, dk=dk, dv=dv)
+
+    step()
+    torch.cuda.synchronize()
+    want = [t.clone() for t in (out, lse, dq, dk, dv)]
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.stream(s):
+        step()  # warm-up on the capture stream
+        torch.cuda.synchronize()
+        with torch.cuda.graph(graph, stream=s):
+            step()
+    torch.cuda.synchronize()
+    for rep in range(3):
+        for t in (out, lse, dq, dk, dv):
+            t.zero_()
+        graph.replay()
+        torch.cuda.synchronize()
+        for name, got, ref in zip(("out", "lse", "dq", "dk", "dv"), (out, lse, dq, dk, dv), want):
+            assert torch.equal(got, ref), (rep, name)
+        step()  # eager work between replays
+        torch.cuda.synchronize()
