@@ -347,7 +347,9 @@ __global__ __launch_bounds__(W * kWave) void na_fwd_kernel(Geo g, const T* __res
                         const float ymax = group_max4(lmax);
                         const bool raise = ymax > thr[m];
                         const float dlt = raise ? ymax : 0.f;
-                        const float alpha = fast_exp2(-dlt);
+                        // a row without a reference has nothing to rescale (and its
+                        // first maximum may lie below -128: exp2(-dlt) = inf)
+                        const float alpha = thr[m] == -INFINITY ? 0.f : fast_exp2(-dlt);
                         mref[m] = raise ? dlt - negm[m] : mref[m];
                         const bool seen = mref[m] != -INFINITY;
                         negm[m] = seen ? -mref[m] : 0.f;

@@ -159,6 +159,51 @@ def test_forward_eight_wave_workgroups(na, monkeypatch, ext, ks, ds, cs, D, dtyp
     assert eo <= TOL[dtype] and el <= TOL[dtype]
 
 
+# Scores that grow (or shrink) steeply along the key order: each tile of keys
+# passes the running reference by far more than the lazy headroom, so the
+# reference is raised again and again.  fp16 with 0.4 per key (natural log
+# units, 12.8 per 32-key tile) overflows fp16 P before the raise; bf16 / fp32
+# with 4 per key jump by ~185 in base 2 between tiles, past the fp32 range of
+# exp2.  Logits stay within +-20 for fp16, whose prescaled Q carries a
+# relative rounding of 2^-11 into every score.
+GROWTH_CASES = [
+    # (extents, kernel, head_dim, dtype, growth per key step, blocks per wave)
+    ((96,), (47,), 64, "fp16", 0.4, 1),
+    ((96,), (47,), 64, "fp16", 0.4, 2),
+    ((96,), (47,), 64, "fp16", -0.4, 2),
+    ((96,), (47,), 64, "bf16", 4.0, 2),
+    ((96,), (47,), 32, "fp32", 4.0, 1),
+    ((96,), (47,), 32, "fp32", -4.0, 2),
+    ((12, 40), (5, 9), 32, "bf16", 40.0, 1),
+    ((12, 40), (5, 9), 64, "fp16", 2.0, 2),
+]
+
+
+@pytest.mark.parametrize("ext,ks,D,dtype,a,m", GROWTH_CASES)
+def test_forward_steep_scores_raise_the_reference(na, monkeypatch, ext, ks, D, dtype, a, m):
+    monkeypatch.setenv("NA_WAVE_BLOCKS", str(m))
+    B, H = 1, 2
+    shape = (B, H) + ext + (D,)
+    gen = torch.Generator().manual_seed(21)
+    scale = 1.0 / math.sqrt(D)
+    # q = (a / scale) e0 and k[..., 0] = centred index along the outermost axis
+    # (1-D: the key index; 2-D: the row), so q.k * scale = a * index
+    q = torch.zeros(shape, dtype=torch.float64)
+    q[..., 0] = a / scale
+    idx = torch.arange(ext[0], dtype=torch.float64) - ext[0] // 2
+    k = torch.randn(shape, generator=gen, dtype=torch.float64)
+    k[..., 0] = idx.view((ext[0],) + (1,) * (len(ext) - 1))
+    v = torch.randn(shape, generator=gen, dtype=torch.float64)
+    q, k, v = (t.to(TDT[dtype]) for t in (q, k, v))
+    ds = (1,) * len(ext)
+    out, lse = na.forward(*_dev(q, k, v), ks, ds)
+    ro, rl = oracle.forward(_f64(q), _f64(k), _f64(v), ks, ds, scale)
+    eo, el = _maxerr(out, ro), _maxerr(lse, rl)
+    _log(f"fwd steep {ext} k={ks} D={D} {dtype} a={a} m={m}: max|dO|={eo:.3g} max|dLSE|={el:.3g}")
+    assert np.isfinite(_f64(out)).all() and np.isfinite(_f64(lse)).all()
+    assert eo <= TOL[dtype] and el <= TOL[dtype]
+
+
 def test_forward_window_one_is_exact_copy(na):
     for dtype in ("fp16", "bf16", "fp32"):
         shape = (2, 2, 13, 17, 64)
