@@ -164,23 +164,31 @@ def test_forward_eight_wave_workgroups(na, monkeypatch, ext, ks, ds, cs, D, dtyp
 # reference is raised again and again.  fp16 with 0.4 per key (natural log
 # units, 12.8 per 32-key tile) overflows fp16 P before the raise; bf16 / fp32
 # with 4 per key jump by ~185 in base 2 between tiles, past the fp32 range of
-# exp2.  Logits stay within +-20 for fp16, whose prescaled Q carries a
-# relative rounding of 2^-11 into every score.
-GROWTH_CASES = [
-    # (extents, kernel, head_dim, dtype, growth per key step, blocks per wave)
-    ((96,), (47,), 64, "fp16", 0.4, 1),
-    ((96,), (47,), 64, "fp16", 0.4, 2),
-    ((96,), (47,), 64, "fp16", -0.4, 2),
-    ((96,), (47,), 64, "bf16", 4.0, 2),
-    ((96,), (47,), 32, "fp32", 4.0, 1),
-    ((96,), (47,), 32, "fp32", -4.0, 2),
-    ((12, 40), (5, 9), 32, "bf16", 40.0, 1),
-    ((12, 40), (5, 9), 64, "fp16", 2.0, 2),
+# exp2; the 2-D bf16 case starts rows at a first maximum below -128 in base 2.
+# Logits stay within +-20 for fp16, whose prescaled Q carries a relative
+# rounding of 2^-11 into every score.
+#
+# Gradients here reach |dK| = 320, so the backward is held to the tolerance
+# relative to each gradient's largest entry.  Not the bf16 case with 4 per
+# key: its rows are one-hot, dQ_i = scale * sum_j dS_ij k_j is a residual of
+# terms up to scale * |k| = 8.5, and the method's Delta_i = dO_i . O_i takes O
+# rounded to bf16 (relative 2^-9), which alone moves dQ by ~0.16 against a
+# largest |dQ| of 0.40.  The fp32 case on the same inputs checks that backward.
+STEEP_CASES = [
+    # (extents, kernel, head_dim, dtype, growth per key step, blocks per wave, check bwd)
+    ((96,), (47,), 64, "fp16", 0.4, 1, True),
+    ((96,), (47,), 64, "fp16", 0.4, 2, True),
+    ((96,), (47,), 64, "fp16", -0.4, 2, True),
+    ((96,), (47,), 64, "bf16", 4.0, 2, False),
+    ((96,), (47,), 32, "fp32", 4.0, 1, True),
+    ((96,), (47,), 32, "fp32", -4.0, 2, True),
+    ((12, 40), (5, 9), 32, "bf16", 40.0, 1, True),
+    ((12, 40), (5, 9), 64, "fp16", 2.0, 2, True),
 ]
 
 
-@pytest.mark.parametrize("ext,ks,D,dtype,a,m", GROWTH_CASES)
-def test_forward_steep_scores_raise_the_reference(na, monkeypatch, ext, ks, D, dtype, a, m):
+@pytest.mark.parametrize("ext,ks,D,dtype,a,m,check_bwd", STEEP_CASES)
+def test_steep_scores_raise_the_reference(na, monkeypatch, ext, ks, D, dtype, a, m, check_bwd):
     monkeypatch.setenv("NA_WAVE_BLOCKS", str(m))
     B, H = 1, 2
     shape = (B, H) + ext + (D,)
@@ -194,14 +202,26 @@ def test_forward_steep_scores_raise_the_reference(na, monkeypatch, ext, ks, D, d
     k = torch.randn(shape, generator=gen, dtype=torch.float64)
     k[..., 0] = idx.view((ext[0],) + (1,) * (len(ext) - 1))
     v = torch.randn(shape, generator=gen, dtype=torch.float64)
-    q, k, v = (t.to(TDT[dtype]) for t in (q, k, v))
+    g = torch.randn(shape, generator=gen, dtype=torch.float64)
+    q, k, v, g = (t.to(TDT[dtype]) for t in (q, k, v, g))
     ds = (1,) * len(ext)
-    out, lse = na.forward(*_dev(q, k, v), ks, ds)
+    qd, kd, vd, gd = _dev(q, k, v, g)
+    out, lse = na.forward(qd, kd, vd, ks, ds)
     ro, rl = oracle.forward(_f64(q), _f64(k), _f64(v), ks, ds, scale)
     eo, el = _maxerr(out, ro), _maxerr(lse, rl)
     _log(f"fwd steep {ext} k={ks} D={D} {dtype} a={a} m={m}: max|dO|={eo:.3g} max|dLSE|={el:.3g}")
     assert np.isfinite(_f64(out)).all() and np.isfinite(_f64(lse)).all()
     assert eo <= TOL[dtype] and el <= TOL[dtype]
+    # the backward recomputes P from these LSE values (nearly one-hot rows)
+    dq, dk, dv = na.backward(qd, kd, vd, out, lse, gd, ks, ds)
+    refs = oracle.backward(_f64(q), _f64(k), _f64(v), _f64(g), ks, ds, scale)
+    rel = [_maxerr(x, r) / max(1.0, float(np.max(np.abs(r)))) for x, r in zip((dq, dk, dv), refs)]
+    _log(f"bwd steep {ext} k={ks} D={D} {dtype} a={a} m={m}: max err / max(1, max|ref|) "
+         f"dq/dk/dv = {[f'{x:.3g}' for x in rel]}")
+    for x in (dq, dk, dv):
+        assert np.isfinite(_f64(x)).all()
+    if check_bwd:
+        assert max(rel) <= TOL[dtype]
 
 
 def test_forward_window_one_is_exact_copy(na):
