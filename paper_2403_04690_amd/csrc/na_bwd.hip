@@ -727,14 +727,18 @@ __device__ __forceinline__ void dkdv_role(const Geo& g, int braw, int nwk,
 // the kernel: workgroups [0, nwk) take the dK/dV role, the next g.nwg the dQ
 // role (dK/dV first: its workgroups carry more work and start earlier)
 // ---------------------------------------------------------------------------
-// 16-bit types with D <= 64 are held to 2 waves per SIMD (<= 256 registers).
-template <int D, typename T>
+// 16-bit types with D <= 64 are held to 2 waves per SIMD (<= 256 registers),
+// and to 3 (<= 168) for rank 1: there the few values that no longer fit are
+// spilled outside the tile loop (the dQ role's per-stage state), and the
+// third wave hides more of the tile loop's latency (1-D k = 1023 backward:
+// -7 %).  Ranks 2 and 3 would spill inside the loop.
+template <int R, int D, typename T>
 constexpr int bwd_min_waves() {
-    return sizeof(T) == 2 && D <= 64 ? 2 : 1;
+    return sizeof(T) == 2 && D <= 64 ? (R == 1 ? 3 : 2) : 1;
 }
 
 template <int R, int D, typename T, int QM, int KM, int SBQ, int SBK, int SHORT>
-__global__ __launch_bounds__(256, (bwd_min_waves<D, T>())) void na_bwd_kernel(Geo g, int nwk, const T* __restrict__ q,
+__global__ __launch_bounds__(256, (bwd_min_waves<R, D, T>())) void na_bwd_kernel(Geo g, int nwk, const T* __restrict__ q,
                                                      const T* __restrict__ k,
                                                      const T* __restrict__ v,
                                                      const T* __restrict__ o,
