@@ -173,6 +173,13 @@ __global__ __launch_bounds__(W * kWave) void na_fwd_kernel(Geo g, const T* __res
     x8 ones;
 #pragma unroll
     for (int j = 0; j < 8; ++j) ones[j] = (T)1.0f;
+    // kept in four registers for the whole loop: rebuilt from the constant
+    // it would cost three moves per tile
+    if constexpr (kMfmaSum) {
+        i32x4 u = __builtin_bit_cast(i32x4, ones);
+        asm volatile("" : "+v"(u));
+        ones = __builtin_bit_cast(x8, u);
+    }
     f32x4 oacc[QM][C::kDB], lsum[QM];
     float mref[QM], negm[QM], thr[QM], lrow[QM];
     // kFoldAdd: negm in all four slots, the accumulator seed of full tiles,
