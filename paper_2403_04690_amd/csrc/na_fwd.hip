@@ -345,9 +345,13 @@ __global__ __launch_bounds__(W * kWave) void na_fwd_kernel(Geo g, const T* __res
                     }
                     // this lane's share of the row; the row maximum exceeds the
                     // threshold exactly when some lane's share does
-                    const float lmax =
-                        fmaxf(fmaxf(fmaxf(y[0][0], y[0][1]), fmaxf(y[0][2], y[0][3])),
-                              fmaxf(fmaxf(y[1][0], y[1][1]), fmaxf(y[1][2], y[1][3])));
+                    // (a chain, so that it becomes three v_max3 and one v_max)
+                    const float lmax = fmaxf(
+                        fmaxf(fmaxf(fmaxf(fmaxf(fmaxf(fmaxf(y[0][0], y[0][1]), y[0][2]), y[0][3]),
+                                          y[1][0]),
+                                    y[1][1]),
+                              y[1][2]),
+                        y[1][3]);
                     // raise the reference on the first valid key of a row, or when
                     // the row grows by more than kLazy (rare, wave-uniform branch)
                     if (__builtin_amdgcn_ballot_w64(lmax > thr[m])) {
