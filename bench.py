@@ -15,7 +15,7 @@ with events (which adds the event overhead of one launch).  So are the K
 forwards and K backwards replayed from HIP graphs (fwd_ms_graph,
 bwd_ms_graph), as a serving loop that captures its launches would run them.
 
-Prints one JSON line.  --gpus above 1 is refused: this build runs on one GPU.
+Prints one JSON line.  --gpus above 1 is refused: the benchmark runs on one GPU.
 """
 import argparse
 import hashlib
@@ -155,7 +155,7 @@ def main():
         print(json.dumps({"copy_probe_bytes": n, "copies": 5}), flush=True)
         return
     if args.gpus != 1:
-        print(f"bench.py: this build runs on exactly one GPU; --gpus {args.gpus} is not supported",
+        print(f"bench.py: the benchmark runs on exactly one GPU; --gpus {args.gpus} is not supported",
               file=sys.stderr)
         sys.exit(2)
 
