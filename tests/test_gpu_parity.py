@@ -245,6 +245,38 @@ def test_forward_deterministic_and_empty(na):
     assert o.shape == z.shape
 
 
+# Dilation at its limits (Sec. 3.4): windows that fill their whole sub-lattice
+# (k * d = L), sub-lattices of unequal length (d does not divide L) whose
+# shorter groups are exactly k long, dilation larger than the window, and a
+# single group per axis of the other axis, in all dtypes, forward and backward.
+DILATION_EDGE_CASES = [
+    # (extents, kernel, dilation, causal, head_dim, dtype)
+    ((12, 15), (4, 5), (3, 3), None, 32, "fp16"),
+    ((10,), (3,), (3,), None, 64, "bf16"),
+    ((10, 11), (3, 2), (3, 5), None, 64, "fp32"),
+    ((7, 9, 10), (2, 3, 3), (3, 3, 3), None, 32, "fp16"),
+    ((31, 17), (3, 4), (10, 4), (True, False), 64, "bf16"),
+    ((64,), (2,), (32,), (True,), 32, "fp16"),
+    ((16, 16, 16), (16, 1, 4), (1, 16, 4), None, 64, "fp16"),
+]
+
+
+@pytest.mark.parametrize("ext,ks,ds,cs,D,dtype", DILATION_EDGE_CASES)
+def test_dilation_edge_cases(na, ext, ks, ds, cs, D, dtype):
+    shape = (1, 2) + ext + (D,)
+    q, k, v, g = _inputs(shape, dtype, 41, 4)
+    qd, kd, vd, gd = _dev(q, k, v, g)
+    scale = 1.0 / math.sqrt(D)
+    out, lse = na.forward(qd, kd, vd, ks, ds, causal=cs)
+    ro, rl = oracle.forward(_f64(q), _f64(k), _f64(v), ks, ds, scale, causal=cs)
+    dq, dk, dv = na.backward(qd, kd, vd, out, lse, gd, ks, ds, causal=cs)
+    rq, rk, rv = oracle.backward(_f64(q), _f64(k), _f64(v), _f64(g), ks, ds, scale, causal=cs)
+    e = [_maxerr(out, ro), _maxerr(lse, rl), _maxerr(dq, rq), _maxerr(dk, rk), _maxerr(dv, rv)]
+    _log(f"dilation edge {ext} k={ks} d={ds} c={cs} D={D} {dtype}: max err o/lse/dq/dk/dv = "
+         f"{[f'{x:.3g}' for x in e]}")
+    assert max(e) <= TOL[dtype]
+
+
 # ---------------------------------------------------------------- backward
 BWD_CASES = [
     ((200,), (7,), (1,), 32, "fp32", 1, 2),
