@@ -34,13 +34,21 @@ def test_golden_hand_derived_windows():
         assert [bf.axis_neighbours(x, L, k, d) for x in range(L)] == [rows[x] for x in range(L)]
 
 
-@pytest.mark.parametrize("L", [1, 2, 5, 7, 10, 13, 16])
-@pytest.mark.parametrize("d", [1, 2, 3])
-@pytest.mark.parametrize("k", [1, 2, 3, 4, 5])
+# every legal (L, k, d) of a small grid (k * d <= L)
+LEGAL_1D = [(L, k, d) for L in (1, 2, 5, 7, 10, 13, 16) for d in (1, 2, 3) for k in (1, 2, 3, 4, 5)
+            if k * d <= L]
+
+
+@pytest.mark.parametrize("L,k,d", LEGAL_1D)
 def test_1d_matches_bruteforce(L, k, d):
-    if k * d > L:
-        pytest.skip("illegal window")
     assert _sets(oracle.neighbors([L], [k], [d])) == bf.neighbours([L], [k], [d])
+
+
+def test_illegal_windows_are_refused():
+    # k * d > L has no window of k same-group neighbours: the oracle refuses it
+    for L, k, d in [(1, 2, 1), (5, 3, 2), (7, 4, 2), (10, 4, 3)]:
+        with pytest.raises(Exception):
+            oracle.neighbors([L], [k], [d])
 
 
 @pytest.mark.parametrize("case", [
