@@ -34,6 +34,7 @@
 //     would cost a wave of occupancy, so those sum with v_dot2).
 #include <algorithm>
 #include <cmath>
+#include <type_traits>
 
 #include "na_launch.h"
 #include "na_stage.h"
@@ -249,16 +250,17 @@ __global__ __launch_bounds__(W * kWave) void na_fwd_kernel(Geo g, const T* __res
             const uint64_t relm = __builtin_amdgcn_ballot_w64(lane < SB && lrel);
             const uint64_t fullm = __builtin_amdgcn_ballot_w64(lane < SB && lfull);
             uint64_t tiles = (relm | (relm >> 1)) & 0x5555555555555555ull;
-            while (tiles) {
-                const int tp = __builtin_ctzll(tiles) >> 1;
-                tiles &= tiles - 1;
+            // The body of one tile (block pair tp).  kFull: both blocks lie inside
+            // every window of the wave's queries, so no mask is evaluated.
+            auto tile = [&](int tp, auto full_pair) {
+                constexpr bool kFull = decltype(full_pair)::value;
                 bool rel[2], full[2];
                 int boc[2][kMaxRank], bin0[2];
 #pragma unroll
                 for (int bi = 0; bi < 2; ++bi) {
                     const int j = tp * 2 + bi;
-                    rel[bi] = (relm >> j) & 1;
-                    full[bi] = (fullm >> j) & 1;
+                    rel[bi] = kFull || ((relm >> j) & 1);
+                    full[bi] = kFull || ((fullm >> j) & 1);
                     bin0[bi] = __builtin_amdgcn_readlane(lin0, j);
 #pragma unroll
                     for (int a = 0; a < R - 1; ++a) boc[bi][a] = __builtin_amdgcn_readlane(loc[a], j);
@@ -399,6 +401,21 @@ __global__ __launch_bounds__(W * kWave) void na_fwd_kernel(Geo g, const T* __res
 #pragma unroll
                     for (int m = 0; m < QM; ++m) lsum[m] = Tr<T>::mma(ones, pf[m], lsum[m]);
                 }
+                        };
+            // Tiles of two full blocks (rows of more than two blocks only) are
+            // visited first, by a body with no mask and no per-block branch;
+            // the order of tiles is free in the online softmax.
+            uint64_t full_tiles = short_rows ? 0 : (fullm & (fullm >> 1)) & tiles;
+            tiles &= ~full_tiles;
+            while (full_tiles) {
+                const int tp = __builtin_ctzll(full_tiles) >> 1;
+                full_tiles &= full_tiles - 1;
+                tile(tp, std::true_type{});
+            }
+            while (tiles) {
+                const int tp = __builtin_ctzll(tiles) >> 1;
+                tiles &= tiles - 1;
+                tile(tp, std::false_type{});
             }
         }
 
