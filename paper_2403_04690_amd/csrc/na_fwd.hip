@@ -203,7 +203,7 @@ __global__ __launch_bounds__(W * kWave) void na_fwd_kernel(Geo g, const T* __res
     // -inf where not), refreshed only when the reference moves.  Block bi of
     // a tile has inner block index bi when rows hold two blocks, else 0.
     constexpr bool short_rows = SHORT != 0 && R > 1;
-    float ain[QM][2][4];
+    f32x4 ain[QM][2];
     auto refresh_addends = [&](int m) {
 #pragma unroll
         for (int bi = 0; bi < 2; ++bi)
@@ -245,21 +245,26 @@ __global__ __launch_bounds__(W * kWave) void na_fwd_kernel(Geo g, const T* __res
             // queries; the wave then visits only the tiles (block pairs) with
             // a relevant block, reading their coordinates back from the lanes
             int loc[kMaxRank], lin0;
-            bool lrel, lfull;
-            wr.test(halo, s * SB + (lane < SB ? lane : 0), loc, lin0, lrel, lfull);
+            bool lrel, lfull, lofull;
+            wr.test(halo, s * SB + (lane < SB ? lane : 0), loc, lin0, lrel, lfull, lofull);
             const uint64_t relm = __builtin_amdgcn_ballot_w64(lane < SB && lrel);
             const uint64_t fullm = __builtin_amdgcn_ballot_w64(lane < SB && lfull);
+            const uint64_t ofullm = __builtin_amdgcn_ballot_w64(lane < SB && lofull);
             uint64_t tiles = (relm | (relm >> 1)) & 0x5555555555555555ull;
-            // The body of one tile (block pair tp).  kFull: both blocks lie inside
-            // every window of the wave's queries, so no mask is evaluated.
-            auto tile = [&](int tp, auto full_pair) {
-                constexpr bool kFull = decltype(full_pair)::value;
+            // The body of one tile (block pair tp), by kind: 0 general; 1 both
+            // blocks inside every window of the wave's queries (no mask); 2 short
+            // rows, both blocks inside every window along the outer axes (the
+            // mask is the per-lane inner-axis addend alone, used in place).
+            auto tile = [&](int tp, auto tile_kind) {
+                constexpr int kKind = decltype(tile_kind)::value;
+                constexpr bool kFull = kKind == 1;
+                constexpr bool kOuterFull = kKind == 2;
                 bool rel[2], full[2];
                 int boc[2][kMaxRank], bin0[2];
 #pragma unroll
                 for (int bi = 0; bi < 2; ++bi) {
                     const int j = tp * 2 + bi;
-                    rel[bi] = kFull || ((relm >> j) & 1);
+                    rel[bi] = kFull || kOuterFull || ((relm >> j) & 1);
                     full[bi] = kFull || ((fullm >> j) & 1);
                     bin0[bi] = __builtin_amdgcn_readlane(lin0, j);
 #pragma unroll
@@ -297,10 +302,12 @@ __global__ __launch_bounds__(W * kWave) void na_fwd_kernel(Geo g, const T* __res
                         add = f32x4{negm[m], negm[m], negm[m], negm[m]};
                     } else {
                         bool outer_ok = rel[bi];
+                        if (!kOuterFull) {
 #pragma unroll
-                        for (int a = 0; a < R - 1; ++a)
-                            outer_ok =
-                                outer_ok && (unsigned)(boc[bi][a] - qs[m][a]) < (unsigned)g.k[a];
+                            for (int a = 0; a < R - 1; ++a)
+                                outer_ok = outer_ok &&
+                                           (unsigned)(boc[bi][a] - qs[m][a]) < (unsigned)g.k[a];
+                        }
                         // generic rows: slot r is valid when base + r lies in [0, lim),
                         // lim folding the outer axes in (0 fails every slot)
                         const int base = bin0[bi] + grp * 4 - qs[m][R - 1];
@@ -317,9 +324,12 @@ __global__ __launch_bounds__(W * kWave) void na_fwd_kernel(Geo g, const T* __res
                 for (int bi = 0; bi < 2; ++bi)
 #pragma unroll
                     for (int m = 0; m < QM; ++m) {
-                        // (the first product of a full tile reads negm4 in place)
+                        // (the first product of a full tile reads negm4 in place, of an
+                        // outer-full tile of short rows the inner addends)
                         if (kFoldAdd && !short_rows && full[bi])
                             sacc[m][bi] = Tr<T>::mma(kf[bi][0], qf[m][0], negm4[m]);
+                        else if (kFoldAdd && short_rows && kOuterFull)
+                            sacc[m][bi] = Tr<T>::mma(kf[bi][0], qf[m][0], ain[m][bi]);
                         else
                             sacc[m][bi] = Tr<T>::mma(kf[bi][0], qf[m][0],
                                                      kFoldAdd ? score_addend(m, bi)
@@ -402,20 +412,22 @@ __global__ __launch_bounds__(W * kWave) void na_fwd_kernel(Geo g, const T* __res
                     for (int m = 0; m < QM; ++m) lsum[m] = Tr<T>::mma(ones, pf[m], lsum[m]);
                 }
                         };
-            // Tiles of two full blocks (rows of more than two blocks only) are
-            // visited first, by a body with no mask and no per-block branch;
-            // the order of tiles is free in the online softmax.
-            uint64_t full_tiles = short_rows ? 0 : (fullm & (fullm >> 1)) & tiles;
-            tiles &= ~full_tiles;
-            while (full_tiles) {
-                const int tp = __builtin_ctzll(full_tiles) >> 1;
-                full_tiles &= full_tiles - 1;
-                tile(tp, std::true_type{});
+            // Tiles of two full blocks (kind 1, rows of more than two blocks) or
+            // of two outer-full blocks (kind 2, short rows) are visited first, by
+            // bodies without per-block branches; the order of tiles is free in
+            // the online softmax.
+            const uint64_t pairs = short_rows ? ofullm & (ofullm >> 1) : fullm & (fullm >> 1);
+            uint64_t fast_tiles = pairs & tiles;
+            tiles &= ~fast_tiles;
+            while (fast_tiles) {
+                const int tp = __builtin_ctzll(fast_tiles) >> 1;
+                fast_tiles &= fast_tiles - 1;
+                tile(tp, std::integral_constant<int, short_rows ? 2 : 1>{});
             }
             while (tiles) {
                 const int tp = __builtin_ctzll(tiles) >> 1;
                 tiles &= tiles - 1;
-                tile(tp, std::false_type{});
+                tile(tp, std::integral_constant<int, 0>{});
             }
         }
 

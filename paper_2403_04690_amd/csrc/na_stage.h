@@ -68,8 +68,11 @@ template <int R>
 struct WaveRange {
     int lo[kMaxRank], hi[kMaxRank], flo[kMaxRank], fhi[kMaxRank];
 
+    // rel: block b meets some window of the wave's queries; full: it lies
+    // inside all of them; outer_full: inside all of them along the outer axes
+    // (the innermost axis not tested).
     __device__ __forceinline__ void test(const Box<R>& box, int b, int* oc, int& inner0, bool& rel,
-                                         bool& full) const {
+                                         bool& full, bool& outer_full) const {
         box.block_coords(b, oc, inner0);
         bool r_ = b < box.nb, f_ = b < box.nb;
 #pragma unroll
@@ -77,10 +80,16 @@ struct WaveRange {
             r_ = r_ && oc[a] >= lo[a] && oc[a] < hi[a];
             f_ = f_ && oc[a] >= flo[a] && oc[a] < fhi[a];
         }
+        outer_full = f_;
         r_ = r_ && inner0 < hi[R - 1] && inner0 + 16 > lo[R - 1];
         f_ = f_ && inner0 >= flo[R - 1] && inner0 + 16 <= fhi[R - 1];
         rel = r_;
         full = f_;
+    }
+    __device__ __forceinline__ void test(const Box<R>& box, int b, int* oc, int& inner0, bool& rel,
+                                         bool& full) const {
+        bool outer_full;
+        test(box, b, oc, inner0, rel, full, outer_full);
     }
 };
 
