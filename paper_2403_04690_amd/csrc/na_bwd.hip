@@ -18,6 +18,7 @@
 // The roles are independent, so they share the GPU instead of running as
 // consecutive launches.
 #include <algorithm>
+#include <type_traits>
 
 #include "na_launch.h"
 #include "na_stage.h"
@@ -152,7 +153,7 @@ __device__ __forceinline__ void dq_role(const Geo& g, int braw, unsigned char* s
     // Score addends folded into the accumulators (not for D = 128 or bf16,
     // as in the forward)
     constexpr bool kFoldAdd = D <= 64 && !std::is_same_v<T, __bf16>;
-    float ain[QM][2][4];
+    f32x4 ain[QM][2];
 #pragma unroll
     for (int m = 0; m < QM; ++m)
 #pragma unroll
@@ -200,21 +201,26 @@ __device__ __forceinline__ void dq_role(const Geo& g, int braw, unsigned char* s
             // lane j < SB tests block s*SB + j; only tiles with a relevant
             // block are visited, their coordinates read back from the lanes
             int loc[kMaxRank], lin0;
-            bool lrel, lfull;
-            wr.test(halo, s * SB + (lane < SB ? lane : 0), loc, lin0, lrel, lfull);
+            bool lrel, lfull, lofull;
+            wr.test(halo, s * SB + (lane < SB ? lane : 0), loc, lin0, lrel, lfull, lofull);
             const uint64_t relm = __builtin_amdgcn_ballot_w64(lane < SB && lrel);
             const uint64_t fullm = __builtin_amdgcn_ballot_w64(lane < SB && lfull);
+            const uint64_t ofullm = __builtin_amdgcn_ballot_w64(lane < SB && lofull);
             uint64_t tiles = (relm | (relm >> 1)) & 0x5555555555555555ull;
-            while (tiles) {
-                const int tp = __builtin_ctzll(tiles) >> 1;
-                tiles &= tiles - 1;
+            // The body of one tile (block pair tp), by kind, as in the forward:
+            // 0 general; 1 both blocks inside every window of the wave's queries;
+            // 2 short rows, both blocks inside every window along the outer axes.
+            auto tile = [&](int tp, auto tile_kind) {
+                constexpr int kKind = decltype(tile_kind)::value;
+                constexpr bool kFull = kKind == 1;
+                constexpr bool kOuterFull = kKind == 2;
                 bool rel[2], full[2];
                 int boc[2][kMaxRank], bin0[2];
 #pragma unroll
                 for (int bi = 0; bi < 2; ++bi) {
                     const int j = tp * 2 + bi;
-                    rel[bi] = (relm >> j) & 1;
-                    full[bi] = (fullm >> j) & 1;
+                    rel[bi] = kFull || kOuterFull || ((relm >> j) & 1);
+                    full[bi] = kFull || ((fullm >> j) & 1);
                     bin0[bi] = __builtin_amdgcn_readlane(lin0, j);
 #pragma unroll
                     for (int a = 0; a < R - 1; ++a) boc[bi][a] = __builtin_amdgcn_readlane(loc[a], j);
@@ -229,10 +235,12 @@ __device__ __forceinline__ void dq_role(const Geo& g, int braw, unsigned char* s
                         add = f32x4{-lse2[m], -lse2[m], -lse2[m], -lse2[m]};
                     } else {
                         bool outer_ok = rel[bi];
+                        if (!kOuterFull) {
 #pragma unroll
-                        for (int a = 0; a < R - 1; ++a)
-                            outer_ok =
-                                outer_ok && (unsigned)(boc[bi][a] - qs[m][a]) < (unsigned)g.k[a];
+                            for (int a = 0; a < R - 1; ++a)
+                                outer_ok = outer_ok &&
+                                           (unsigned)(boc[bi][a] - qs[m][a]) < (unsigned)g.k[a];
+                        }
                         // generic rows: slot r is valid when base + r lies in [0, lim)
                         const int base = bin0[bi] + grp * 4 - qs[m][R - 1];
                         const unsigned lim = outer_ok ? (unsigned)g.k[R - 1] : 0u;
@@ -258,6 +266,8 @@ __device__ __forceinline__ void dq_role(const Geo& g, int braw, unsigned char* s
                                     sacc[m][bi] = Tr<T>::mma(kf, qf[m][st], sacc[m][bi]);
                                 else if (kFoldAdd && !short_rows && full[bi])
                                     sacc[m][bi] = Tr<T>::mma(kf, qf[m][0], nlse4[m]);  // in place
+                                else if (kFoldAdd && short_rows && kOuterFull)
+                                    sacc[m][bi] = Tr<T>::mma(kf, qf[m][0], ain[m][bi]);  // in place
                                 else
                                     sacc[m][bi] = Tr<T>::mma(kf, qf[m][0],
                                                              kFoldAdd ? score_addend(m, bi)
@@ -304,6 +314,20 @@ __device__ __forceinline__ void dq_role(const Geo& g, int braw, unsigned char* s
 #pragma unroll
                     for (int m = 0; m < QM; ++m) dqacc[m][db] = Tr<T>::mma(kf, dsf[m], dqacc[m][db]);
                 }
+                        };
+            // the specialised tiles first (the order of tiles does not matter)
+            const uint64_t pairs = short_rows ? ofullm & (ofullm >> 1) : fullm & (fullm >> 1);
+            uint64_t fast_tiles = pairs & tiles;
+            tiles &= ~fast_tiles;
+            while (fast_tiles) {
+                const int tp = __builtin_ctzll(fast_tiles) >> 1;
+                fast_tiles &= fast_tiles - 1;
+                tile(tp, std::integral_constant<int, short_rows ? 2 : 1>{});
+            }
+            while (tiles) {
+                const int tp = __builtin_ctzll(tiles) >> 1;
+                tiles &= tiles - 1;
+                tile(tp, std::integral_constant<int, 0>{});
             }
         }
 
