@@ -598,21 +598,26 @@ __device__ __forceinline__ void dkdv_role(const Geo& g, int braw, int nwk,
             // lane j < SB tests block s*SB + j; only tiles with a relevant
             // block are visited, their coordinates read back from the lanes
             int loc[kMaxRank], lin0;
-            bool lrel, lfull;
-            wr.test(ibox, s * SB + (lane < SB ? lane : 0), loc, lin0, lrel, lfull);
+            bool lrel, lfull, lofull;
+            wr.test(ibox, s * SB + (lane < SB ? lane : 0), loc, lin0, lrel, lfull, lofull);
             const uint64_t relm = __builtin_amdgcn_ballot_w64(lane < SB && lrel);
             const uint64_t fullm = __builtin_amdgcn_ballot_w64(lane < SB && lfull);
+            const uint64_t ofullm = __builtin_amdgcn_ballot_w64(lane < SB && lofull);
             uint64_t tiles = (relm | (relm >> 1)) & 0x5555555555555555ull;
-            while (tiles) {
-                const int tp = __builtin_ctzll(tiles) >> 1;
-                tiles &= tiles - 1;
+            // The body of one tile (block pair tp), by kind: 0 general; 1 both
+            // query blocks attend every key of the wave; 2 short rows, both
+            // blocks inside the wave's inverse ranges along the outer axes.
+            auto tile = [&](int tp, auto tile_kind) {
+                constexpr int kKind = decltype(tile_kind)::value;
+                constexpr bool kFull = kKind == 1;
+                constexpr bool kOuterFull = kKind == 2;
                 bool rel[2], full[2];
                 int boc[2][kMaxRank], bin0[2];
 #pragma unroll
                 for (int bi = 0; bi < 2; ++bi) {
                     const int j = tp * 2 + bi;
-                    rel[bi] = (relm >> j) & 1;
-                    full[bi] = (fullm >> j) & 1;
+                    rel[bi] = kFull || kOuterFull || ((relm >> j) & 1);
+                    full[bi] = kFull || ((fullm >> j) & 1);
                     bin0[bi] = __builtin_amdgcn_readlane(lin0, j);
 #pragma unroll
                     for (int a = 0; a < R - 1; ++a) boc[bi][a] = __builtin_amdgcn_readlane(loc[a], j);
@@ -637,10 +642,12 @@ __device__ __forceinline__ void dkdv_role(const Geo& g, int braw, int nwk,
                         add = nlse[bi];
                     } else {
                         bool outer_ok = rel[bi];
+                        if (!kOuterFull) {
 #pragma unroll
-                        for (int a = 0; a < R - 1; ++a)
-                            outer_ok = outer_ok && (unsigned)(boc[bi][a] - ilo[m][a]) <=
-                                                       (unsigned)ispan[m][a];
+                            for (int a = 0; a < R - 1; ++a)
+                                outer_ok = outer_ok && (unsigned)(boc[bi][a] - ilo[m][a]) <=
+                                                           (unsigned)ispan[m][a];
+                        }
                         // generic rows: slot r is valid when base + r lies in [0, lim)
                         const int base = bin0[bi] + grp * 4 - ilo[m][R - 1];
                         const unsigned lim = outer_ok ? (unsigned)ispan[m][R - 1] + 1u : 0u;
@@ -722,6 +729,24 @@ __device__ __forceinline__ void dkdv_role(const Geo& g, int braw, int nwk,
                         dkacc[m][d] = Tr<T>::mma(qa, dsf[m], dkacc[m][d]);
                     }
                 }
+                        };
+            // the specialised tiles first (the order of tiles does not matter);
+            // 16-bit types at D <= 64 only (the compiler fails on the others)
+            if constexpr (sizeof(T) == 2 && D <= 64) {
+                const uint64_t pairs =
+                    short_rows ? ofullm & (ofullm >> 1) : fullm & (fullm >> 1);
+                uint64_t fast_tiles = pairs & tiles;
+                tiles &= ~fast_tiles;
+                while (fast_tiles) {
+                    const int tp = __builtin_ctzll(fast_tiles) >> 1;
+                    fast_tiles &= fast_tiles - 1;
+                    tile(tp, std::integral_constant<int, short_rows ? 2 : 1>{});
+                }
+            }
+            while (tiles) {
+                const int tp = __builtin_ctzll(tiles) >> 1;
+                tiles &= tiles - 1;
+                tile(tp, std::integral_constant<int, 0>{});
             }
         }
 
