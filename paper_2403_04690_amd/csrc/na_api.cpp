@@ -232,9 +232,66 @@ bool valid_tiling(int rank, na_dtype dtype, bool forward, const na_tiling& t) {
     return pg == 8 && forward && rank == 1 && dtype != NA_FP32;
 }
 
+// Rank 2: the wave tile (h, w) of 16 * m queries that multiplies each query
+// with the fewest keys.  A wave visits h + k0 - 1 halo rows of
+// ceil((w + k1 - 1) / 16) 16-key blocks each (in group coordinates, clipped
+// to the group).  Two weights for what else a key costs: two blocks per wave
+// share every K/V fragment read (x 0.85), and 4-wide rows spread a 16-query
+// block over four rows (x 1.25).  Partly filled waves (a tile longer than
+// the group) count per useful query.  Two blocks per wave only where that
+// still leaves 1024 workgroups, as for the other ranks; NA_WAVE_BLOCKS=1|2
+// forces m.  The weights come from timing all five shapes of both m on
+// 2-D windows of 5 to 31 keys (head dims 32 and 64, fp16 and bf16), where
+// the choice is the fastest forward in every case measured.
+bool rank2_tiling(const int64_t* extents, const int32_t* ks, const int32_t* ds, int64_t BH,
+                  na_tiling& best) {
+    int glen[3];
+    group_lengths(2, extents, ds, glen);
+    int forced = 0;
+    if (const char* env = std::getenv("NA_WAVE_BLOCKS")) {
+        const int v = std::atoi(env);
+        if (v == 1 || v == 2) forced = v;
+    }
+    double best_cost = 0.0;
+    bool have = false;
+    for (int m = 1; m <= 2; ++m) {
+        if (forced && m != forced) continue;
+        for (int w = 4; w <= 16; w *= 2) {
+            const int h = 16 * m / w;
+            if (w > 4 && w > pow2ceil(glen[1])) continue;
+            if (h > pow2ceil(glen[0])) continue;
+            na_tiling t;
+            t.blocks_per_wave = m;
+            t.wave_tile[0] = h;
+            t.wave_tile[1] = w;
+            t.wave_tile[2] = 1;
+            t.waves[0] = 4;
+            t.waves[1] = t.waves[2] = 1;
+            if (m == 2 && !forced) {
+                na::Geo g;
+                if (!geo_from_tiling(2, extents, ks, ds, nullptr, BH, t, g) || g.nwg < 1024)
+                    continue;
+            }
+            const int rows = std::min(h + ks[0] - 1, glen[0]);
+            const int cols = std::min(w + ks[1] - 1, glen[1]);
+            const int useful = std::min(h, glen[0]) * std::min(w, glen[1]);
+            const double cost = double(rows) * ((cols + 15) / 16) * (m == 2 ? 0.85 : 1.0) *
+                                (w == 4 ? 1.25 : 1.0) * (16.0 * m / useful);
+            if (!have || cost < best_cost) {
+                best = t;
+                best_cost = cost;
+                have = true;
+            }
+        }
+    }
+    return have;
+}
+
 // Heuristic tilings of na_forward / na_backward.
 na_tiling default_forward_tiling(int rank, const int64_t* extents, const int32_t* ks,
                                  const int32_t* ds, int64_t BH, na_dtype dtype) {
+    na_tiling t2;
+    if (rank == 2 && rank2_tiling(extents, ks, ds, BH, t2)) return t2;
     const int m = choose_m(rank, extents, ks, ds, BH);
     na::Geo g4;
     int waves = 4;
@@ -244,6 +301,8 @@ na_tiling default_forward_tiling(int rank, const int64_t* extents, const int32_t
 
 na_tiling default_backward_tiling(int rank, const int64_t* extents, const int32_t* ks,
                                   const int32_t* ds, int64_t BH) {
+    na_tiling t2;
+    if (rank == 2 && rank2_tiling(extents, ks, ds, BH, t2)) return t2;
     return heuristic_tiling(rank, extents, ks, ds, choose_m(rank, extents, ks, ds, BH), 4);
 }
 

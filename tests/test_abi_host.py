@@ -195,6 +195,36 @@ def test_candidate_tilings_are_valid_and_start_with_the_heuristic(lib, ext, ks, 
         (buf[0].blocks_per_wave, tuple(buf[0].wave_tile), tuple(buf[0].waves))
 
 
+# 2-D problems whose tilings were all timed on the MI355X (forward and
+# backward, every wave-tile shape of both blocks-per-wave values): the
+# heuristic must pick the fastest forward tiling measured.
+RANK2_FASTEST = [
+    # (extents, kernel, dilation, batch, heads, head dim, dtype code, fastest tiling)
+    ((56, 56), (7, 7), (1, 1), 4, 4, 32, 1, (1, (2, 8, 1))),
+    ((56, 56), (7, 7), (1, 1), 16, 4, 32, 1, (1, (2, 8, 1))),
+    ((56, 56), (7, 7), (1, 1), 8, 8, 64, 1, (1, (2, 8, 1))),
+    ((64, 64), (5, 5), (1, 1), 8, 8, 32, 1, (1, (2, 8, 1))),
+    ((96, 96), (9, 9), (1, 1), 4, 8, 64, 1, (1, (2, 8, 1))),
+    ((128, 128), (7, 7), (2, 2), 2, 8, 64, 1, (1, (2, 8, 1))),
+    ((128, 128), (13, 13), (2, 2), 2, 8, 64, 2, (1, (4, 4, 1))),
+    ((128, 128), (15, 15), (1, 1), 1, 8, 64, 1, (2, (2, 16, 1))),
+    ((128, 128), (21, 21), (1, 1), 1, 8, 64, 1, (2, (4, 8, 1))),
+    ((128, 128), (31, 31), (1, 1), 1, 8, 64, 1, (2, (2, 16, 1))),
+]
+
+
+@pytest.mark.parametrize("ext,ks,ds,B,H,D,dt,best", RANK2_FASTEST)
+def test_rank2_heuristic_picks_the_fastest_measured_tiling(lib, monkeypatch, ext, ks, ds, B, H, D,
+                                                           dt, best):
+    monkeypatch.delenv("NA_WAVE_BLOCKS", raising=False)
+    lib.na_tune_clear()
+    r, e, k, d = _args(2, ext, ks, ds)
+    for fwd in (1, 0):
+        cur = _tiling_type()()
+        assert lib.na_current_tiling(r, e, k, d, None, B, H, D, dt, fwd, ctypes.byref(cur)) == NA_OK
+        assert (cur.blocks_per_wave, tuple(cur.wave_tile), tuple(cur.waves)) == best + ((4, 1, 1),)
+
+
 def _tiling(m, wt, wg):
     return _tiling_type()(m, (ctypes.c_int32 * 3)(*wt), (ctypes.c_int32 * 3)(*wg))
 
