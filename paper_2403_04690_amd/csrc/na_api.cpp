@@ -44,53 +44,6 @@ int64_t token_count(int rank, const int64_t* extents) {
     return n;
 }
 
-// Wave tile (queries or keys owned by one wave, 16 * m of them) along each
-// axis, sized from the innermost axis outwards and never longer than the
-// longest dilation group of an axis (rounded up to a power of two).
-// An inner window of 10 to 13 keys: a 4-wide wave tile keeps the union of its
-// windows along the inner axis inside one 16-key block, so each halo row is
-// one block instead of two (mask density 0.66 instead of 0.41 at k = 13).
-bool narrow_inner_tile(int rank, int k_inner) { return rank > 1 && k_inner >= 10 && k_inner <= 13; }
-
-void wave_tile(int rank, const int* glen, int m, int waves, int k_inner, int* wt, int* wgd) {
-    const int q = 16 * m;
-    for (int a = 0; a < 3; ++a) wt[a] = wgd[a] = 1;
-    if (rank == 1) {
-        wt[0] = q;
-        wgd[0] = waves;
-        return;
-    }
-    const int inner = rank - 1;
-    const int cap = narrow_inner_tile(rank, k_inner) ? 4 : rank == 2 ? (m == 1 ? 8 : 16) : 8;
-    wt[inner] = std::min(cap, pow2ceil(glen[inner]));
-    int rem = q / wt[inner];
-    // hand out the remaining factor 2 at a time over the outer axes, outermost first
-    int a = 0;
-    while (rem > 1) {
-        bool placed = false;
-        for (int t = 0; t < inner && rem > 1; ++t) {
-            const int ax = (a + t) % inner;
-            if (wt[ax] < pow2ceil(glen[ax]) || t == inner - 1) {
-                wt[ax] *= 2;
-                rem /= 2;
-                a = (ax + 1) % inner;
-                placed = true;
-                break;
-            }
-        }
-        if (!placed) {
-            wt[0] *= rem;
-            rem = 1;
-        }
-    }
-    if (rank == 2) {
-        wgd[0] = 4;
-    } else {
-        wgd[0] = 2;
-        wgd[1] = 2;
-    }
-}
-
 // Longest dilation group along each axis (inert axes: 1).
 void group_lengths(int rank, const int64_t* extents, const int32_t* ds, int* glen) {
     for (int a = 0; a < 3; ++a)
@@ -144,50 +97,6 @@ bool geo_from_tiling(int rank, const int64_t* extents, const int32_t* ks, const 
     return true;
 }
 
-// The heuristic tiling for wave tiles of 16 * m tokens and `waves` waves
-// (waves != 4 only for rank 1).
-na_tiling heuristic_tiling(int rank, const int64_t* extents, const int32_t* ks,
-                          const int32_t* ds, int m, int waves) {
-    int glen[3];
-    group_lengths(rank, extents, ds, glen);
-    na_tiling t;
-    t.blocks_per_wave = m;
-    wave_tile(rank, glen, m, rank == 1 ? waves : 4, ks[rank - 1], t.wave_tile, t.waves);
-    return t;
-}
-
-bool make_geo(int rank, const int64_t* extents, const int32_t* ks, const int32_t* ds,
-              const int32_t* causal, int64_t BH, int m, na::Geo& g, int waves = 4) {
-    return geo_from_tiling(rank, extents, ks, ds, causal, BH,
-                           heuristic_tiling(rank, extents, ks, ds, m, waves), g);
-}
-
-// Wave size multiplier: two 16-token blocks per wave unless that leaves the
-// GPU (256 CUs) with too few workgroups.  NA_WAVE_BLOCKS=1|2 overrides.
-int choose_m(int rank, const int64_t* extents, const int32_t* ks, const int32_t* ds, int64_t BH) {
-    if (const char* env = std::getenv("NA_WAVE_BLOCKS")) {
-        const int v = std::atoi(env);
-        if (v == 1 || v == 2) return v;
-    }
-    // 4 x 4 wave tiles of narrow inner windows: two of them would share few rows
-    if (narrow_inner_tile(rank, ks[rank - 1])) return 1;
-    na::Geo g;
-    if (!make_geo(rank, extents, ks, ds, nullptr, BH, 2, g)) return 1;
-    return g.nwg < 1024 ? 1 : 2;
-}
-
-// Forward workgroup size: 1-D problems of 16-bit types with plenty of
-// 4-wave workgroups run 8-wave ones instead (each stage of K/V rows then
-// serves twice the queries).  NA_FWD_WAVES=4|8 overrides.
-int forward_waves(int rank, na_dtype dtype, const na::Geo& g4) {
-    if (rank != 1 || dtype == NA_FP32) return 4;
-    if (const char* env = std::getenv("NA_FWD_WAVES")) {
-        const int v = std::atoi(env);
-        if (v == 4 || v == 8) return v;
-    }
-    return g4.nwg >= 2048 ? 8 : 4;
-}
-
 na_status check_problem(int rank, const int64_t* extents, const int32_t* ks, const int32_t* ds,
                         int64_t batch, int64_t heads, int64_t head_dim, na_dtype dtype,
                         float scale) {
@@ -232,78 +141,116 @@ bool valid_tiling(int rank, na_dtype dtype, bool forward, const na_tiling& t) {
     return pg == 8 && forward && rank == 1 && dtype != NA_FP32;
 }
 
-// Rank 2: the wave tile (h, w) of 16 * m queries that multiplies each query
-// with the fewest keys.  A wave visits h + k0 - 1 halo rows of
-// ceil((w + k1 - 1) / 16) 16-key blocks each (in group coordinates, clipped
-// to the group).  Two weights for what else a key costs: two blocks per wave
-// share every K/V fragment read (x 0.85), and 4-wide rows spread a 16-query
-// block over four rows (x 1.25).  Partly filled waves (a tile longer than
-// the group) count per useful query.  Two blocks per wave only where that
-// still leaves 1024 workgroups, as for the other ranks; NA_WAVE_BLOCKS=1|2
-// forces m.  The weights come from timing all five shapes of both m on
-// 2-D windows of 5 to 31 keys (head dims 32 and 64, fp16 and bf16), where
-// the choice is the fastest forward, or within 1 % of it, in every case.
-bool rank2_tiling(const int64_t* extents, const int32_t* ks, const int32_t* ds, int64_t BH,
-                  na_tiling& best) {
-    int glen[3];
-    group_lengths(2, extents, ds, glen);
-    int forced = 0;
-    if (const char* env = std::getenv("NA_WAVE_BLOCKS")) {
+int env_choice(const char* name, int a, int b) {
+    if (const char* env = std::getenv(name)) {
         const int v = std::atoi(env);
-        if (v == 1 || v == 2) forced = v;
+        if (v == a || v == b) return v;
     }
+    return 0;
+}
+
+// The heuristic tiling: the wave tile of 16 * m queries that multiplies each
+// query with the fewest keys.  Along each outer axis a wave visits
+// h + k - 1 halo rows, and along the inner axis ceil((w + k - 1) / 16)
+// 16-key blocks (group coordinates, clipped to the group).  Two weights for
+// what else a key costs: two blocks per wave share every K/V fragment read
+// (x 0.85, and x 0.8 in 1-D), and a 4-wide inner tile spreads a 16-query
+// block over four rows (x 1.25).  Partly filled waves count per useful query.
+//
+// m = 2 only where that still leaves 1024 workgroups, and not in the
+// backward at head dim 128, whose two-block kernels hold one wave per SIMD.
+// Workgroups are 4 waves along the outermost axis (1-D, 2-D) or 2 x 2 over
+// the two outer axes (3-D).  The 1-D forward of a 16-bit type with a window
+// of at least 512 keys and 2048 such workgroups runs 8-wave workgroups
+// instead: each stage of K/V rows then serves twice the queries.  With
+// smaller windows the larger halo stage costs more than it saves (up to
+// +38 % at 63 keys).  NA_WAVE_BLOCKS=1|2 and NA_FWD_WAVES=4|8 force m and
+// the workgroup size.
+//
+// The weights come from timing every candidate tiling (na_tune, or all five
+// 2-D wave tiles of both m) on 1-D windows of 7 to 1023 keys, 2-D windows
+// of 5 to 31 and 3-D windows of 3 x 7 x 7 to 7 x 7 x 7.  In the forward the
+// choice is the fastest measured, or within 2 % of it, in every case.
+na_tiling model_tiling(int rank, const int64_t* extents, const int32_t* ks, const int32_t* ds,
+                       int64_t BH, int64_t head_dim, na_dtype dtype, bool forward) {
+    int glen[3];
+    group_lengths(rank, extents, ds, glen);
+    const int inner = rank - 1;
+    const int forced = env_choice("NA_WAVE_BLOCKS", 1, 2);
+    na_tiling best{};
     double best_cost = 0.0;
     bool have = false;
     for (int m = 1; m <= 2; ++m) {
         if (forced && m != forced) continue;
-        for (int w = 4; w <= 16; w *= 2) {
-            const int h = 16 * m / w;
-            if (w > 4 && w > pow2ceil(glen[1])) continue;
-            if (h > pow2ceil(glen[0])) continue;
-            na_tiling t;
-            t.blocks_per_wave = m;
-            t.wave_tile[0] = h;
-            t.wave_tile[1] = w;
-            t.wave_tile[2] = 1;
-            t.waves[0] = 4;
-            t.waves[1] = t.waves[2] = 1;
-            if (m == 2 && !forced) {
-                na::Geo g;
-                if (!geo_from_tiling(2, extents, ks, ds, nullptr, BH, t, g) || g.nwg < 1024)
-                    continue;
-            }
-            const int rows = std::min(h + ks[0] - 1, glen[0]);
-            const int cols = std::min(w + ks[1] - 1, glen[1]);
-            const int useful = std::min(h, glen[0]) * std::min(w, glen[1]);
-            const double cost = double(rows) * ((cols + 15) / 16) * (m == 2 ? 0.85 : 1.0) *
-                                (w == 4 ? 1.25 : 1.0) * (16.0 * m / useful);
-            if (!have || cost < best_cost) {
-                best = t;
-                best_cost = cost;
-                have = true;
+        if (!forced && m == 2 && !forward && head_dim == 128) continue;
+        for (int w = rank == 1 ? 16 * m : 4; w <= (rank == 1 ? 16 * m : 16); w *= 2) {
+            const int outer = 16 * m / w;  // product of the outer wave-tile lengths
+            for (int t0 = 1; t0 <= (rank == 3 ? outer : 1); t0 *= 2) {
+                na_tiling t;
+                t.blocks_per_wave = m;
+                for (int a = 0; a < 3; ++a) t.wave_tile[a] = t.waves[a] = 1;
+                t.wave_tile[inner] = w;
+                if (rank == 2) t.wave_tile[0] = outer;
+                if (rank == 3) {
+                    t.wave_tile[0] = t0;
+                    t.wave_tile[1] = outer / t0;
+                }
+                if (rank == 3) {
+                    t.waves[0] = t.waves[1] = 2;
+                } else {
+                    t.waves[0] = 4;
+                }
+                bool fits = rank == 1 || w == 4 || w <= pow2ceil(glen[inner]);
+                for (int a = 0; a < inner; ++a) fits = fits && t.wave_tile[a] <= pow2ceil(glen[a]);
+                if (!fits) continue;
+                if (m == 2 && !forced) {
+                    na::Geo g;
+                    if (!geo_from_tiling(rank, extents, ks, ds, nullptr, BH, t, g) || g.nwg < 1024)
+                        continue;
+                }
+                double keys = 16.0 * ((std::min(w + ks[inner] - 1, glen[inner]) + 15) / 16);
+                double useful = std::min(w, glen[inner]);
+                for (int a = 0; a < inner; ++a) {
+                    keys *= std::min(t.wave_tile[a] + ks[a] - 1, glen[a]);
+                    useful *= std::min(t.wave_tile[a], glen[a]);
+                }
+                const double share = rank == 1 ? 0.8 : 0.85;
+                const double cost = keys * (m == 2 ? share : 1.0) *
+                                    (rank > 1 && w == 4 ? 1.25 : 1.0) * (16.0 * m / useful);
+                if (!have || cost < best_cost) {
+                    best = t;
+                    best_cost = cost;
+                    have = true;
+                }
             }
         }
     }
-    return have;
+    if (!have) {  // no wave tile fits the groups: one block per wave along the inner axis
+        for (int a = 0; a < 3; ++a) best.wave_tile[a] = best.waves[a] = 1;
+        best.blocks_per_wave = 1;
+        best.wave_tile[inner] = 16;
+        if (rank == 3) best.waves[0] = best.waves[1] = 2;
+        else best.waves[0] = 4;
+    }
+    if (forward && rank == 1 && dtype != NA_FP32) {
+        const int fw = env_choice("NA_FWD_WAVES", 4, 8);
+        na::Geo g4;
+        if (fw == 8 || (fw == 0 && ks[0] >= 512 &&
+                        geo_from_tiling(1, extents, ks, ds, nullptr, BH, best, g4) && g4.nwg >= 2048))
+            best.waves[0] = 8;
+    }
+    return best;
 }
 
 // Heuristic tilings of na_forward / na_backward.
 na_tiling default_forward_tiling(int rank, const int64_t* extents, const int32_t* ks,
-                                 const int32_t* ds, int64_t BH, na_dtype dtype) {
-    na_tiling t2;
-    if (rank == 2 && rank2_tiling(extents, ks, ds, BH, t2)) return t2;
-    const int m = choose_m(rank, extents, ks, ds, BH);
-    na::Geo g4;
-    int waves = 4;
-    if (make_geo(rank, extents, ks, ds, nullptr, BH, m, g4)) waves = forward_waves(rank, dtype, g4);
-    return heuristic_tiling(rank, extents, ks, ds, m, waves);
+                                 const int32_t* ds, int64_t BH, int64_t head_dim, na_dtype dtype) {
+    return model_tiling(rank, extents, ks, ds, BH, head_dim, dtype, true);
 }
 
 na_tiling default_backward_tiling(int rank, const int64_t* extents, const int32_t* ks,
-                                  const int32_t* ds, int64_t BH) {
-    na_tiling t2;
-    if (rank == 2 && rank2_tiling(extents, ks, ds, BH, t2)) return t2;
-    return heuristic_tiling(rank, extents, ks, ds, choose_m(rank, extents, ks, ds, BH), 4);
+                                  const int32_t* ds, int64_t BH, int64_t head_dim, na_dtype dtype) {
+    return model_tiling(rank, extents, ks, ds, BH, head_dim, dtype, false);
 }
 
 // ---- tiling cache (filled by na_tune) ----
@@ -342,8 +289,8 @@ na_tiling current_tiling(int rank, const int64_t* extents, const int32_t* ks, co
             if (!forward && it->second.has_bwd) return it->second.bwd;
         }
     }
-    return forward ? default_forward_tiling(rank, extents, ks, ds, BH, dtype)
-                   : default_backward_tiling(rank, extents, ks, ds, BH);
+    return forward ? default_forward_tiling(rank, extents, ks, ds, BH, head_dim, dtype)
+                   : default_backward_tiling(rank, extents, ks, ds, BH, head_dim, dtype);
 }
 
 bool same_tiling(const na_tiling& a, const na_tiling& b) {
@@ -359,10 +306,11 @@ bool same_tiling(const na_tiling& a, const na_tiling& b) {
 // axis is at least 4 (2-D, 3-D), at most kMaxCandidates in all.
 constexpr int kMaxCandidates = 64;
 std::vector<na_tiling> candidates(int rank, const int64_t* extents, const int32_t* ks,
-                                  const int32_t* ds, int64_t BH, na_dtype dtype, bool forward) {
+                                  const int32_t* ds, int64_t BH, int64_t head_dim, na_dtype dtype,
+                                  bool forward) {
     std::vector<na_tiling> out;
-    out.push_back(forward ? default_forward_tiling(rank, extents, ks, ds, BH, dtype)
-                          : default_backward_tiling(rank, extents, ks, ds, BH));
+    out.push_back(forward ? default_forward_tiling(rank, extents, ks, ds, BH, head_dim, dtype)
+                          : default_backward_tiling(rank, extents, ks, ds, BH, head_dim, dtype));
     int glen[3];
     group_lengths(rank, extents, ds, glen);
     const int maxwg = forward && rank == 1 && dtype != NA_FP32 ? 8 : 4;
@@ -525,7 +473,7 @@ int na_candidate_tilings(int rank, const int64_t* extents, const int32_t* kernel
     na_status st = check_problem(rank, extents, kernel_size, dilation, batch, heads, head_dim,
                                  dtype, 1.0f);
     if (st != NA_OK) return -(int)st;
-    const auto c = candidates(rank, extents, kernel_size, dilation, batch * heads, dtype,
+    const auto c = candidates(rank, extents, kernel_size, dilation, batch * heads, head_dim, dtype,
                               forward != 0);
     for (int i = 0; i < (int)c.size() && i < max && out; ++i) out[i] = c[i];
     return (int)c.size();
@@ -591,8 +539,8 @@ na_status na_tune(int rank, const int64_t* extents, const int32_t* kernel_size,
                                  dtype, scale);
     if (st != NA_OK) return st;
     const int64_t BH = batch * heads;
-    na_tiling bf = default_forward_tiling(rank, extents, kernel_size, dilation, BH, dtype);
-    na_tiling bb = default_backward_tiling(rank, extents, kernel_size, dilation, BH);
+    na_tiling bf = default_forward_tiling(rank, extents, kernel_size, dilation, BH, head_dim, dtype);
+    na_tiling bb = default_backward_tiling(rank, extents, kernel_size, dilation, BH, head_dim, dtype);
     float tm[4] = {0.f, 0.f, 0.f, 0.f};
     if (!empty_problem(rank, extents, batch, heads)) {
         st = backward_pointers(q, k, v, out, logsumexp, dout, dq, dk, dv);
@@ -654,7 +602,7 @@ na_status na_tune(int rank, const int64_t* extents, const int32_t* kernel_size,
             t_best = tb;
             return NA_OK;
         };
-        const auto fc = candidates(rank, extents, kernel_size, dilation, BH, dtype, true);
+        const auto fc = candidates(rank, extents, kernel_size, dilation, BH, head_dim, dtype, true);
         st = pick(
             fc,
             [&](const na_tiling& t) {
@@ -666,7 +614,7 @@ na_status na_tune(int rank, const int64_t* extents, const int32_t* kernel_size,
         if (st == NA_OK)
             st = run_forward(rank, extents, kernel_size, dilation, causal, BH, head_dim, dtype,
                              scale, bf, q, k, v, out, logsumexp, s);
-        const auto bc = candidates(rank, extents, kernel_size, dilation, BH, dtype, false);
+        const auto bc = candidates(rank, extents, kernel_size, dilation, BH, head_dim, dtype, false);
         if (st == NA_OK)
             st = pick(
                 bc,

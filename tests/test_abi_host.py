@@ -195,34 +195,53 @@ def test_candidate_tilings_are_valid_and_start_with_the_heuristic(lib, ext, ks, 
         (buf[0].blocks_per_wave, tuple(buf[0].wave_tile), tuple(buf[0].waves))
 
 
-# 2-D problems whose tilings were all timed on the MI355X (forward and
-# backward, every wave-tile shape of both blocks-per-wave values): the
-# heuristic must pick the fastest forward tiling measured.
-RANK2_FASTEST = [
-    # (extents, kernel, dilation, batch, heads, head dim, dtype code, fastest tiling)
-    ((56, 56), (7, 7), (1, 1), 4, 4, 32, 1, (1, (2, 8, 1))),
-    ((56, 56), (7, 7), (1, 1), 16, 4, 32, 1, (1, (2, 8, 1))),
-    ((56, 56), (7, 7), (1, 1), 8, 8, 64, 1, (1, (2, 8, 1))),
-    ((64, 64), (5, 5), (1, 1), 8, 8, 32, 1, (1, (2, 8, 1))),
-    ((96, 96), (9, 9), (1, 1), 4, 8, 64, 1, (1, (2, 8, 1))),
-    ((128, 128), (7, 7), (2, 2), 2, 8, 64, 1, (1, (2, 8, 1))),
-    ((128, 128), (13, 13), (2, 2), 2, 8, 64, 2, (1, (4, 4, 1))),
-    ((128, 128), (15, 15), (1, 1), 1, 8, 64, 1, (2, (2, 16, 1))),
-    ((128, 128), (21, 21), (1, 1), 1, 8, 64, 1, (2, (4, 8, 1))),
-    ((128, 128), (31, 31), (1, 1), 1, 8, 64, 1, (2, (2, 16, 1))),
+# Problems whose candidate tilings were all timed on the MI355X (the tuner,
+# and every 2-D wave-tile shape of both blocks-per-wave values): the
+# heuristic forward tiling must be the fastest measured, or within 2 % of it.
+# The backward takes the same tiling, except one block per wave at head
+# dim 128.
+FASTEST_FORWARD = [
+    # (extents, kernel, dilation, batch, heads, head dim, dtype code, fastest forward tiling)
+    ((56, 56), (7, 7), (1, 1), 4, 4, 32, 1, (1, (2, 8, 1), (4, 1, 1))),
+    ((56, 56), (7, 7), (1, 1), 16, 4, 32, 1, (1, (2, 8, 1), (4, 1, 1))),
+    ((56, 56), (7, 7), (1, 1), 8, 8, 64, 1, (1, (2, 8, 1), (4, 1, 1))),
+    ((64, 64), (5, 5), (1, 1), 8, 8, 32, 1, (1, (2, 8, 1), (4, 1, 1))),
+    ((96, 96), (9, 9), (1, 1), 4, 8, 64, 1, (1, (2, 8, 1), (4, 1, 1))),
+    ((128, 128), (7, 7), (2, 2), 2, 8, 64, 1, (1, (2, 8, 1), (4, 1, 1))),
+    ((128, 128), (13, 13), (2, 2), 2, 8, 64, 2, (1, (4, 4, 1), (4, 1, 1))),
+    ((128, 128), (15, 15), (1, 1), 1, 8, 64, 1, (2, (2, 16, 1), (4, 1, 1))),
+    ((128, 128), (21, 21), (1, 1), 1, 8, 64, 1, (2, (4, 8, 1), (4, 1, 1))),
+    ((128, 128), (31, 31), (1, 1), 1, 8, 64, 1, (2, (2, 16, 1), (4, 1, 1))),
+    ((8192,), (7,), (1,), 4, 8, 64, 1, (1, (16, 1, 1), (4, 1, 1))),
+    ((16384,), (31,), (1,), 2, 8, 64, 1, (1, (16, 1, 1), (4, 1, 1))),
+    ((32768,), (63,), (1,), 2, 8, 32, 1, (2, (32, 1, 1), (4, 1, 1))),
+    ((32768,), (127,), (1,), 1, 16, 64, 1, (2, (32, 1, 1), (4, 1, 1))),
+    ((4096,), (255,), (1,), 4, 8, 128, 2, (2, (32, 1, 1), (4, 1, 1))),
+    ((65536,), (1023,), (1,), 1, 8, 64, 1, (2, (32, 1, 1), (8, 1, 1))),
+    ((16, 64, 64), (7, 7, 7), (1, 2, 2), 1, 8, 64, 1, (2, (2, 2, 8), (2, 2, 1))),
+    ((32, 32, 32), (7, 7, 7), (1, 1, 1), 1, 8, 64, 1, (2, (2, 2, 8), (2, 2, 1))),
+    ((8, 56, 56), (3, 7, 7), (1, 1, 1), 1, 8, 64, 1, (1, (1, 2, 8), (2, 2, 1))),
+    ((16, 48, 48), (5, 9, 9), (1, 1, 1), 1, 8, 64, 2, (1, (1, 2, 8), (2, 2, 1))),
 ]
 
 
-@pytest.mark.parametrize("ext,ks,ds,B,H,D,dt,best", RANK2_FASTEST)
-def test_rank2_heuristic_picks_the_fastest_measured_tiling(lib, monkeypatch, ext, ks, ds, B, H, D,
-                                                           dt, best):
+@pytest.mark.parametrize("ext,ks,ds,B,H,D,dt,best", FASTEST_FORWARD)
+def test_heuristic_picks_the_fastest_measured_tiling(lib, monkeypatch, ext, ks, ds, B, H, D, dt,
+                                                     best):
     monkeypatch.delenv("NA_WAVE_BLOCKS", raising=False)
+    monkeypatch.delenv("NA_FWD_WAVES", raising=False)
     lib.na_tune_clear()
-    r, e, k, d = _args(2, ext, ks, ds)
+    r, e, k, d = _args(len(ext), ext, ks, ds)
+    got = []
     for fwd in (1, 0):
         cur = _tiling_type()()
         assert lib.na_current_tiling(r, e, k, d, None, B, H, D, dt, fwd, ctypes.byref(cur)) == NA_OK
-        assert (cur.blocks_per_wave, tuple(cur.wave_tile), tuple(cur.waves)) == best + ((4, 1, 1),)
+        got.append((cur.blocks_per_wave, tuple(cur.wave_tile), tuple(cur.waves)))
+    assert got[0] == best
+    if D == 128:
+        assert got[1][0] == 1
+    else:
+        assert got[1] == (best[0], best[1], (4, 1, 1) if len(ext) < 3 else (2, 2, 1))
 
 
 def _tiling(m, wt, wg):
