@@ -157,8 +157,10 @@ int env_choice(const char* name, int a, int b) {
 // (x 0.85, and x 0.8 in 1-D), and a 4-wide inner tile spreads a 16-query
 // block over four rows (x 1.25).  Partly filled waves count per useful query.
 //
-// m = 2 only where that still leaves 1024 workgroups, and not in the
-// backward at head dim 128, whose two-block kernels hold one wave per SIMD.
+// m = 2 only where that still leaves 1024 workgroups, and neither for fp32
+// nor in the backward at head dim 128: those two-block kernels hold half the
+// waves per SIMD of the one-block ones, or fewer (one-block tilings were
+// 18-31 % faster wherever measured).
 // Workgroups are 4 waves along the outermost axis (1-D, 2-D) or 2 x 2 over
 // the two outer axes (3-D).  The 1-D forward of a 16-bit type with a window
 // of at least 512 keys and 2048 such workgroups runs 8-wave workgroups
@@ -182,7 +184,7 @@ na_tiling model_tiling(int rank, const int64_t* extents, const int32_t* ks, cons
     bool have = false;
     for (int m = 1; m <= 2; ++m) {
         if (forced && m != forced) continue;
-        if (!forced && m == 2 && !forward && head_dim == 128) continue;
+        if (!forced && m == 2 && (dtype == NA_FP32 || (!forward && head_dim == 128))) continue;
         for (int w = rank == 1 ? 16 * m : 4; w <= (rank == 1 ? 16 * m : 16); w *= 2) {
             const int outer = 16 * m / w;  // product of the outer wave-tile lengths
             for (int t0 = 1; t0 <= (rank == 3 ? outer : 1); t0 *= 2) {

@@ -222,6 +222,12 @@ FASTEST_FORWARD = [
     ((32, 32, 32), (7, 7, 7), (1, 1, 1), 1, 8, 64, 1, (2, (2, 2, 8), (2, 2, 1))),
     ((8, 56, 56), (3, 7, 7), (1, 1, 1), 1, 8, 64, 1, (1, (1, 2, 8), (2, 2, 1))),
     ((16, 48, 48), (5, 9, 9), (1, 1, 1), 1, 8, 64, 2, (1, (1, 2, 8), (2, 2, 1))),
+    ((16384,), (127,), (1,), 2, 8, 64, 0, (1, (16, 1, 1), (4, 1, 1))),
+    ((8192,), (255,), (1,), 2, 8, 128, 0, (1, (16, 1, 1), (4, 1, 1))),
+    ((32, 32, 32), (7, 7, 7), (1, 1, 1), 1, 4, 64, 0, (1, (1, 2, 8), (2, 2, 1))),
+    ((128, 128), (31, 31), (1, 1), 1, 8, 128, 1, (2, (2, 16, 1), (4, 1, 1))),
+    ((32768,), (511,), (1,), 1, 8, 128, 1, (2, (32, 1, 1), (4, 1, 1))),
+    ((32, 32, 32), (7, 7, 7), (1, 1, 1), 1, 4, 128, 2, (2, (2, 2, 8), (2, 2, 1))),
 ]
 
 
