@@ -192,16 +192,16 @@ na_tiling model_tiling(int rank, const int64_t* extents, const int32_t* ks, cons
                 t.blocks_per_wave = m;
                 for (int a = 0; a < 3; ++a) t.wave_tile[a] = t.waves[a] = 1;
                 t.wave_tile[inner] = w;
-                if (rank == 2) t.wave_tile[0] = outer;
-                if (rank == 3) {
+                if (rank == 2) {
+                    t.wave_tile[0] = outer;
+                } else if (rank == 3) {
                     t.wave_tile[0] = t0;
                     t.wave_tile[1] = outer / t0;
                 }
-                if (rank == 3) {
+                if (rank == 3)
                     t.waves[0] = t.waves[1] = 2;
-                } else {
+                else
                     t.waves[0] = 4;
-                }
                 bool fits = rank == 1 || w == 4 || w <= pow2ceil(glen[inner]);
                 for (int a = 0; a < inner; ++a) fits = fits && t.wave_tile[a] <= pow2ceil(glen[a]);
                 if (!fits) continue;
