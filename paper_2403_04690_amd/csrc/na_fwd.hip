@@ -166,10 +166,10 @@ __global__ __launch_bounds__(W * kWave) void na_fwd_kernel(Geo g, const T* __res
     // Row sums: with kMfmaSum, lsum[m] accumulates ones^T P^T on the matrix
     // cores (every entry is the row sum); otherwise each lane sums its share
     // of P in lrow[m], reduced across the four lane groups at the end.
-    // Two blocks per wave: the matrix cores in 1-D at D <= 64, where the two
-    // extra accumulators leave the occupancy as it is (elsewhere they cost a
-    // wave per SIMD).
-    constexpr bool kMfmaSum = sizeof(T) == 2 && (QM == 1 || (R == 1 && D <= 64));
+    // Two blocks per wave: the matrix cores at D = 32, and in 1-D at D = 64,
+    // where the two extra accumulators leave the occupancy as it is
+    // (elsewhere they cost a wave per SIMD).
+    constexpr bool kMfmaSum = sizeof(T) == 2 && (QM == 1 || D <= 32 || (R == 1 && D <= 64));
     // Score addends folded into the accumulators.  Not for D = 128 (the
     // addend vectors would cost it occupancy) nor bf16 (rounding c*Q to 8
     // mantissa bits would add an error comparable to that of P itself).
