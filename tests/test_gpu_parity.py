@@ -132,8 +132,8 @@ def test_forward_small(na, ext, ks, ds, D, dtype, B, H):
     assert eo <= TOL[dtype] and el <= TOL[dtype]
 
 
-# 1-D forwards run on 8-wave workgroups when the problem is large; the
-# environment forces that launch shape (and the query blocks per wave) on
+# 1-D forwards of 16-bit types run on 8-wave workgroups when the window and
+# the problem are large; the environment forces that launch shape (and the query blocks per wave) on
 # small ragged, dilated and causal problems too.
 EIGHT_WAVE_CASES = [
     # (extents, kernel, dilation, causal, head_dim, dtype, batch, heads, blocks per wave)
