@@ -59,10 +59,12 @@ def _load():
     lib.na_ref_forward.argtypes = prob + [_f64p] * 5
     lib.na_ref_forward_rows.argtypes = prob + [_f64p] * 3 + [ctypes.c_int64, _i64p, _f64p, _f64p]
     lib.na_ref_backward.argtypes = prob + [_f64p] * 7
+    lib.na_ref_backward_given.argtypes = prob + [_f64p] * 12
     lib.na_ref_backward_rows.argtypes = prob + [_f64p] * 4 + [
         ctypes.c_int64, _i64p, _f64p, ctypes.c_int64, _i64p, _f64p, _f64p]
     for name in ("na_ref_neighbors", "na_ref_axis_relation", "na_ref_forward",
-                 "na_ref_forward_rows", "na_ref_backward", "na_ref_backward_rows"):
+                 "na_ref_forward_rows", "na_ref_backward", "na_ref_backward_given",
+                 "na_ref_backward_rows"):
         getattr(lib, name).restype = ctypes.c_int
     _lib = lib
     return lib
@@ -170,6 +172,27 @@ def backward(q, k, v, dout, kernel_size, dilation, scale, causal=None):
                                _ptr(dout, _f64p), _ptr(dq, _f64p), _ptr(dk, _f64p),
                                _ptr(dv, _f64p)))
     return dq, dk, dv
+
+
+def backward_given(q, k, v, out, lse, dout, kernel_size, dilation, scale, causal=None,
+                   abs_sums=False):
+    """The backward operator from stored forward results: P rebuilt from ``lse``, Delta from
+    ``out`` (as the library's na_backward takes them).  Returns (dq, dk, dv) in fp64, and with
+    ``abs_sums`` also (dq_abs, dk_abs, dv_abs): the same sums over absolute values of their
+    terms, the magnitude a rounding of the terms is relative to."""
+    lib = _load()
+    q, k, v, out, lse, dout = (_f64(a) for a in (q, k, v, out, lse, dout))
+    B, H, D = q.shape[0], q.shape[1], q.shape[-1]
+    rank, L, K, Dl, C = _problem(q.shape[2:-1], kernel_size, dilation, causal)
+    if out.shape != q.shape or dout.shape != q.shape or lse.shape != q.shape[:-1]:
+        raise ValueError("oracle: out and dout must be shaped like q, lse like q[..., 0]")
+    res = [np.zeros_like(q) for _ in range(6 if abs_sums else 3)]
+    ptrs = [_ptr(r, _f64p) for r in res] + ([None] * 3 if not abs_sums else [])
+    _check(lib.na_ref_backward_given(rank, _ptr(L, _i64p), _ptr(K, _i32p), _ptr(Dl, _i32p),
+                                     _ptr(C, _i32p), B, H, D, float(scale), _ptr(q, _f64p),
+                                     _ptr(k, _f64p), _ptr(v, _f64p), _ptr(out, _f64p),
+                                     _ptr(lse, _f64p), _ptr(dout, _f64p), *ptrs))
+    return tuple(res)
 
 
 def backward_rows(q, k, v, dout, kernel_size, dilation, scale, qrows, krows, causal=None):

@@ -512,3 +512,98 @@ int na_ref_backward_rows(int rank, const int64_t* L, const int32_t* ks, const in
     }
     return fail ? REF_ERR_ALLOC : REF_OK;
 }
+
+/*
+ * The backward operator as the library's boundary defines it: gradients from
+ * the stored forward results `out` and `lse` instead of recomputing them.
+ * The probabilities come back from the logsumexp, Delta from the stored
+ * output (the operators of Sec. 3.1 with P rebuilt from LSE):
+ *   P[x,j]  = exp(scale * q[x].k[j] - lse[x])
+ *   Delta   = sum_c dO[x,c] * out[x,c]
+ *   dA[x,j] = P[x,j] * (dO[x].v[j] - Delta)
+ *   dQ[x]   = scale * sum_j dA[x,j] k[j];  dK[j] += scale * dA[x,j] q[x];
+ *   dV[j]  += P[x,j] dO[x].
+ * When out and lse are the exact forward results this is na_ref_backward.
+ *
+ * dq_abs, dk_abs, dv_abs (each NULL or shaped like dq) receive the same sums
+ * taken over absolute values of their terms:
+ *   dq_abs[x] = scale * sum_j |dA[x,j]| |k[j]|,  dk_abs[j] = scale * sum_x |dA[x,j]| |q[x]|,
+ *   dv_abs[j] = sum_x P[x,j] |dO[x]|
+ * -- the magnitude a rounding of the terms (dA or P to a 16-bit type) is
+ * relative to, used to bound low-precision results (standard error analysis
+ * of a sum, not part of the method).
+ */
+int na_ref_backward_given(int rank, const int64_t* L, const int32_t* ks, const int32_t* dil,
+                          const int32_t* causal, int64_t B, int64_t H, int64_t D, double scale,
+                          const double* q, const double* k, const double* v, const double* out,
+                          const double* lse, const double* dout, double* dq, double* dk,
+                          double* dv, double* dq_abs, double* dk_abs, double* dv_abs) {
+    int st = check_problem(rank, L, ks, dil);
+    if (st) return st;
+    for (int a = 0; a < rank; ++a)
+        if (ks[a] > 4096) return REF_ERR_KERNEL_SIZE;
+    int64_t N = tokens_of(rank, L), ell = window_size(rank, ks);
+    int64_t slices = B * H;
+    const size_t bytes = sizeof(double) * (size_t)(slices * N * D);
+    memset(dk, 0, bytes);
+    memset(dv, 0, bytes);
+    if (dk_abs) memset(dk_abs, 0, bytes);
+    if (dv_abs) memset(dv_abs, 0, bytes);
+    int fail = 0;
+#pragma omp parallel
+    {
+        int64_t* nb = (int64_t*)malloc(sizeof(int64_t) * (size_t)ell);
+        if (!nb) {
+#pragma omp atomic write
+            fail = 1;
+        } else {
+#pragma omp for schedule(dynamic, 1)
+            for (int64_t sl = 0; sl < slices; ++sl) {
+                const int64_t base = sl * N * D;
+                for (int64_t t = 0; t < N; ++t) {
+                    const double* qr = q + base + t * D;
+                    const double* g = dout + base + t * D;
+                    const double* orow = out + base + t * D;
+                    const double l = lse[sl * N + t];
+                    int64_t cnt = neighbours_of(rank, L, ks, dil, causal, t, nb);
+                    double delta = 0.0;
+                    for (int64_t c = 0; c < D; ++c) delta += g[c] * orow[c];
+                    double* dqr = dq + base + t * D;
+                    for (int64_t c = 0; c < D; ++c) dqr[c] = 0.0;
+                    if (dq_abs)
+                        for (int64_t c = 0; c < D; ++c) dq_abs[base + t * D + c] = 0.0;
+                    for (int64_t e = 0; e < cnt; ++e) {
+                        const int64_t j = nb[e];
+                        const double* kr = k + base + j * D;
+                        const double* vr = v + base + j * D;
+                        double s = 0.0, dp = 0.0;
+                        for (int64_t c = 0; c < D; ++c) {
+                            s += qr[c] * kr[c];
+                            dp += g[c] * vr[c];
+                        }
+                        const double p = exp(scale * s - l);
+                        const double da = p * (dp - delta);
+                        double* dkr = dk + base + j * D;
+                        double* dvr = dv + base + j * D;
+                        for (int64_t c = 0; c < D; ++c) {
+                            dqr[c] += scale * da * kr[c];
+                            dkr[c] += scale * da * qr[c];
+                            dvr[c] += p * g[c];
+                        }
+                        if (dq_abs)
+                            for (int64_t c = 0; c < D; ++c)
+                                dq_abs[base + t * D + c] += scale * fabs(da) * fabs(kr[c]);
+                        if (dk_abs)
+                            for (int64_t c = 0; c < D; ++c)
+                                dk_abs[base + j * D + c] += scale * fabs(da) * fabs(qr[c]);
+                        if (dv_abs)
+                            for (int64_t c = 0; c < D; ++c)
+                                dv_abs[base + j * D + c] += p * fabs(g[c]);
+                    }
+                }
+            }
+        }
+        free(nb);
+    }
+    return fail ? REF_ERR_ALLOC : REF_OK;
+}
