@@ -28,8 +28,8 @@
  *   - Every device pointer must be 16-byte aligned.
  *   - The caller owns all memory; the library never allocates or frees
  *     device memory and needs no workspace.  Its only global state is the
- *     tiling cache that na_tune fills (guarded by a mutex); every entry point
- *     is re-entrant.
+ *     tiling cache that na_tune (or tuning on first use) fills, guarded by a
+ *     mutex, and the tune-on-first-use mode; every entry point is re-entrant.
  *   - Calls are asynchronous and stream-ordered on `stream` (a hipStream_t;
  *     NULL means the legacy default stream).  Problem validation is
  *     synchronous and happens before any launch: a non-NA_OK status means
@@ -39,7 +39,14 @@
  *   - B * H * N == 0 (empty batch or heads) is a no-op returning NA_OK.
  *   - Supported: rank 1..3, head_dim in {32, 64, 128}, any k_a >= 1 and
  *     d_a >= 1 with k_a * d_a <= X_a, fp32 / fp16 / bf16.  N * D must stay
- *     below 2^31 and B * H below 2^31.
+ *     below 2^31 and B * H below 2^31, and a launch must stay below 2^32
+ *     threads: nwg * 64 * (waves per workgroup) for the forward and
+ *     (nwg + nwg rounded up to a multiple of 8) * 256 for the backward, nwg
+ *     being the number of query tiles over every (batch, head, dilation
+ *     group); for 1-D problems of at most 64 tokens per group that means
+ *     B * H * prod(d) < 2^23.  Larger problems are rejected with NA_ERR_SHAPE
+ *     before any launch (na_validate checks the heuristic tilings, the
+ *     tiled entry points their own).
  */
 #ifndef NA_H_
 #define NA_H_
@@ -104,6 +111,12 @@ int na_version(void);
  * Host-only check of the problem description used by every entry point
  * (rank, extents, kernel_size, dilation, causal, batch, heads, head_dim,
  * dtype, scale).  Touches no device and no pointer other than the arrays.
+ * The paper leaves the legal parameters implicit: a window is never
+ * truncated (Sec. 1-2, caption of Fig. "neighborhoodattention"), and a
+ * dilated window lives in one sub-lattice of an axis (Sec. 3.4), so each axis
+ * needs k_a * d_a <= X_a (NA_ERR_WINDOW_EXCEEDS_EXTENT otherwise); the
+ * softmax scale of Eq. 1 must be finite.  Returns NA_OK or the status of
+ * the first check that fails.
  */
 na_status na_validate(int rank, const int64_t* extents, const int32_t* kernel_size,
                       const int32_t* dilation, const int32_t* causal, int64_t batch, int64_t heads,
@@ -144,11 +157,12 @@ na_status na_backward(int rank, const int64_t* extents, const int32_t* kernel_si
  * of the cache is (rank, extents, kernel_size, dilation, causal, batch * heads,
  * head_dim, dtype); the scale does not matter.
  *
- * na_candidate_tilings (host only): writes up to `max` tilings that na_tune
- * considers for the forward (forward != 0) or the backward of the problem,
- * the heuristic one first, and returns how many there are in all (so a
- * return value above `max` means the list was cut), or a negative na_status
- * for an invalid problem.
+ * na_candidate_tilings (host only): writes up to `max` of the candidate
+ * tilings for the forward (forward != 0) or the backward of the problem, the
+ * heuristic one first, and returns how many candidates there are in all (so
+ * a return value above `max` means the list was cut; out may be NULL to count
+ * them), or a negative na_status for an invalid problem.  na_tune times the
+ * first NA_TUNE_DEFAULT_CANDIDATES of them, or all with NA_TUNE_THOROUGH.
  *
  * na_current_tiling (host only): the tiling na_forward (forward != 0) or
  * na_backward would use now for the problem.
@@ -158,20 +172,35 @@ na_status na_backward(int rank, const int64_t* extents, const int32_t* kernel_si
  * Every valid tiling gives the same result up to summation order.
  *
  * na_tune (auto-tuner over the query-tile factorisations, App. A): after a
- * warm-up, times every candidate tiling of the forward and of the backward,
- * each over `repeats` launches (>= 1) after one warm-up launch, then times the
- * three fastest and the heuristic tiling again; the heuristic one is kept
- * unless a finalist beats it by more than 2 %.  Runs on the caller's buffers,
- * which end up holding the results of the chosen tilings (out and logsumexp
- * of the forward of q, k, v; dq, dk, dv of the backward with dout).  Records
- * the chosen forward and backward tilings in the cache.  Synchronises
- * `stream`; must not run concurrently with other work on these buffers.
- * Optional outputs (NULL to skip): best_forward, best_backward, and
- * times_ms[4] = {best forward, best backward, heuristic forward, heuristic
- * backward} in milliseconds per launch.
+ * warm-up, times the candidate tilings of the forward and, separately, of the
+ * backward (the first NA_TUNE_DEFAULT_CANDIDATES, or every one when flags has
+ * NA_TUNE_THOROUGH), each over `repeats` launches (>= 1) after one warm-up
+ * launch, then times the three fastest and the heuristic tiling again; the
+ * heuristic one is kept unless a finalist beats it by more than 2 %.  Runs on
+ * the caller's buffers, which end up holding the results of the chosen
+ * tilings (out and logsumexp of the forward of q, k, v; dq, dk, dv of the
+ * backward with dout).  Records the chosen forward and backward tilings in
+ * the cache.  Synchronises `stream`; must not run concurrently with other
+ * work on these buffers.  Unknown flags give NA_ERR_TILING.  Optional outputs
+ * (NULL to skip): best_forward, best_backward, and times_ms[4] = {best
+ * forward, best backward, heuristic forward, heuristic backward} in
+ * milliseconds per launch.
  *
  * na_tune_clear: empties the cache.
+ *
+ * na_set_autotune (tune on first use, App. A): mode 1 makes na_forward and
+ * na_backward tune a problem whose tiling is not cached yet (forward and
+ * backward each by its own timing, as na_tune does, with 3 launches per
+ * candidate) on the call's own buffers, record the choice and return its
+ * result; mode 2 does the same over every candidate (NA_TUNE_THOROUGH); 0
+ * turns it off.  Such a first call synchronises its stream and takes as long
+ * as timing every candidate; later calls on the problem run the cached
+ * tiling.  A call on a stream that is being captured into a graph never
+ * tunes.  The initial mode comes from the environment variable NA_AUTOTUNE
+ * (0, 1 or 2; unset: 0).  na_autotune returns the mode in force.
  */
+#define NA_TUNE_THOROUGH 1
+#define NA_TUNE_DEFAULT_CANDIDATES 64
 int na_candidate_tilings(int rank, const int64_t* extents, const int32_t* kernel_size,
                          const int32_t* dilation, int64_t batch, int64_t heads, int64_t head_dim,
                          na_dtype dtype, int forward, na_tiling* out, int max);
@@ -194,17 +223,26 @@ na_status na_tune(int rank, const int64_t* extents, const int32_t* kernel_size,
                   const int32_t* dilation, const int32_t* causal, int64_t batch, int64_t heads,
                   int64_t head_dim, na_dtype dtype, float scale, const void* q, const void* k,
                   const void* v, void* out, float* logsumexp, const void* dout, void* dq, void* dk,
-                  void* dv, int repeats, na_stream_t stream, na_tiling* best_forward,
+                  void* dv, int repeats, int flags, na_stream_t stream, na_tiling* best_forward,
                   na_tiling* best_backward, float* times_ms);
 void na_tune_clear(void);
+void na_set_autotune(int mode);
+int na_autotune(void);
 
 /*
  * Test hook: evaluates on the device, with the same index functions the
- * kernels use, the per-axis neighbourhood summary of the problem.  Each output
- * is a device int32 array of sum_a extents[a] entries, axis 0 first:
+ * kernels use, the per-axis neighbourhood summary of the problem: the window
+ * of each query coordinate (Sec. 1-2 and the caption of Fig.
+ * "neighborhoodattention": k nearest same-group neighbours, shifted at
+ * borders; Sec. 3.4: dilation groups and causal axes) and the inverse
+ * neighbourhood of each key coordinate (the queries attending to it, which
+ * the IN operator of Sec. 3.1 sums over).  Each output is a device int32
+ * array of sum_a extents[a] entries, axis 0 first:
  *   start[x]  = first (smallest) neighbour coordinate of query coordinate x,
  *   inv_lo[j] = smallest query coordinate whose window contains key j,
  *   inv_hi[j] = largest query coordinate whose window contains key j.
+ * Only the problem arguments are validated (batch, heads, head_dim and dtype
+ * play no part).  Asynchronous on `stream`.
  */
 na_status na_debug_windows(int rank, const int64_t* extents, const int32_t* kernel_size,
                            const int32_t* dilation, const int32_t* causal, int32_t* start,

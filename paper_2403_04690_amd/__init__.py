@@ -20,7 +20,7 @@ import torch
 
 __all__ = ["NAError", "forward", "backward", "na_attention", "debug_windows", "validate",
            "library_path", "load_library", "DTYPES", "Tiling", "candidate_tilings",
-           "current_tiling", "tune", "tune_clear"]
+           "current_tiling", "tune", "tune_clear", "set_autotune", "autotune"]
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
 # NA_LIBRARY may point at another build of the same library (A/B comparisons
@@ -105,11 +105,15 @@ def load_library():
     lib.na_forward_tiled.restype = ctypes.c_int
     lib.na_backward_tiled.argtypes = prob + [tp] + [_vp] * 10
     lib.na_backward_tiled.restype = ctypes.c_int
-    lib.na_tune.argtypes = prob + [_vp] * 9 + [ctypes.c_int, _vp, tp, tp,
+    lib.na_tune.argtypes = prob + [_vp] * 9 + [ctypes.c_int, ctypes.c_int, _vp, tp, tp,
                                                ctypes.POINTER(ctypes.c_float)]
     lib.na_tune.restype = ctypes.c_int
     lib.na_tune_clear.argtypes = []
     lib.na_tune_clear.restype = None
+    lib.na_set_autotune.argtypes = [ctypes.c_int]
+    lib.na_set_autotune.restype = None
+    lib.na_autotune.argtypes = []
+    lib.na_autotune.restype = ctypes.c_int
     _lib = lib
     return lib
 
@@ -165,7 +169,8 @@ def validate(extents, kernel_size, dilation, batch, heads, head_dim, dtype, scal
 
 def candidate_tilings(extents, kernel_size, dilation, batch, heads, head_dim, dtype,
                       forward=True):
-    """The tilings na_tune considers (the heuristic one first), host only."""
+    """Every candidate tiling (the heuristic one first), host only; na_tune times the first
+    NA_TUNE_DEFAULT_CANDIDATES (64) of them, or all when thorough."""
     lib = load_library()
     rank, ext, ks, ds, _ = _problem_arrays(extents, kernel_size, dilation)
     n = lib.na_candidate_tilings(rank, ext, ks, ds, batch, heads, head_dim, DTYPES[dtype],
@@ -190,11 +195,11 @@ def current_tiling(extents, kernel_size, dilation, batch, heads, head_dim, dtype
 
 
 def tune(q, k, v, dout, kernel_size, dilation=1, scale=None, causal=None, repeats=5,
-         out=None, lse=None, dq=None, dk=None, dv=None):
-    """Auto-tune the tilings of this problem (na_tune): times every candidate forward and
-    backward tiling, caches the fastest for later calls and returns
-    (best_forward, best_backward, times_ms) with times_ms = [best fwd, best bwd,
-    heuristic fwd, heuristic bwd].  Synchronises the current stream."""
+         out=None, lse=None, dq=None, dk=None, dv=None, thorough=False):
+    """Auto-tune the tilings of this problem (na_tune): times the candidate forward and
+    backward tilings (the first 64, or all with thorough=True), caches the fastest for later
+    calls and returns (best_forward, best_backward, times_ms) with times_ms = [best fwd,
+    best bwd, heuristic fwd, heuristic bwd].  Synchronises the current stream."""
     lib = load_library()
     _check_tensors(q, k, v, dout)
     B, H, D = q.shape[0], q.shape[1], q.shape[-1]
@@ -212,14 +217,26 @@ def tune(q, k, v, dout, kernel_size, dilation=1, scale=None, causal=None, repeat
     _check(lib.na_tune(rank, ext, ks, ds, cs, B, H, D, DTYPES[q.dtype], float(scale),
                        q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(), lse.data_ptr(),
                        dout.data_ptr(), dq.data_ptr(), dk.data_ptr(), dv.data_ptr(),
-                       int(repeats), _stream(q.device), ctypes.byref(bf), ctypes.byref(bb),
-                       times))
+                       int(repeats), 1 if thorough else 0, _stream(q.device), ctypes.byref(bf),
+                       ctypes.byref(bb), times))
     return Tiling._from_c(bf), Tiling._from_c(bb), list(times)
 
 
 def tune_clear():
     """Forget every tiling na_tune recorded."""
     load_library().na_tune_clear()
+
+
+def set_autotune(mode):
+    """Tune on first use (na_set_autotune): 1 makes forward/backward tune a problem whose
+    tiling is not cached yet on the call's own buffers (3 launches per candidate), 2 does so
+    over every candidate, 0 turns it off."""
+    load_library().na_set_autotune(int(mode))
+
+
+def autotune():
+    """The tune-on-first-use mode in force (0, 1 or 2)."""
+    return int(load_library().na_autotune())
 
 
 def forward(q, k, v, kernel_size, dilation=1, scale=None, out=None, lse=None, causal=None,

@@ -9,6 +9,7 @@
 #include <cstdint>
 #include <cstdlib>
 #include <cstring>
+#include <atomic>
 #include <map>
 #include <mutex>
 #include <vector>
@@ -18,7 +19,7 @@
 
 namespace {
 
-constexpr int kVersion = 300;  // 0.3.0
+constexpr int kVersion = 400;  // 0.4.0
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
@@ -50,9 +51,24 @@ void group_lengths(int rank, const int64_t* extents, const int32_t* ds, int* gle
         glen[a] = a < rank ? na::group_len((int)extents[a], ds[a], 0) : 1;
 }
 
-// Fills the geometry of a problem for a tiling (validated by the caller).
+// Threads in the x dimension of a launch must stay below 2^32.  The forward
+// runs nwg workgroups of 64 * (waves per workgroup) threads; the backward runs
+// nwk + nwg workgroups of 256 threads, nwk being nwg rounded up to a multiple
+// of the 8 XCDs.
+bool grid_fits(int64_t nwg, const na_tiling& t, bool forward) {
+    const int64_t limit = int64_t(1) << 32;
+    if (forward) {
+        const int64_t waves = int64_t(t.waves[0]) * t.waves[1] * t.waves[2];
+        return nwg * waves * 64 < limit;
+    }
+    return (((nwg + 7) & ~int64_t(7)) + nwg) * 256 < limit;
+}
+
+// Fills the geometry of a problem for a tiling (validated by the caller);
+// false if the launch it needs would be too large (grid_fits).
 bool geo_from_tiling(int rank, const int64_t* extents, const int32_t* ks, const int32_t* ds,
-                     const int32_t* causal, int64_t BH, const na_tiling& t, na::Geo& g) {
+                     const int32_t* causal, int64_t BH, const na_tiling& t, na::Geo& g,
+                     bool forward) {
     std::memset(&g, 0, sizeof(g));
     int glen[3];
     group_lengths(rank, extents, ds, glen);
@@ -83,7 +99,7 @@ bool geo_from_tiling(int rank, const int64_t* extents, const int32_t* ks, const 
         ntiles *= g.nt[a];
     }
     const int64_t nwg = ntiles * g.ngroups * BH;
-    if (nwg >= (int64_t(1) << 31)) return false;
+    if (!grid_fits(nwg, t, forward)) return false;
     g.ntiles = (int)ntiles;
     g.nwg = (int)nwg;
     for (int a = 0; a < 3; ++a) {
@@ -207,7 +223,8 @@ na_tiling model_tiling(int rank, const int64_t* extents, const int32_t* ks, cons
                 if (!fits) continue;
                 if (m == 2 && !forced) {
                     na::Geo g;
-                    if (!geo_from_tiling(rank, extents, ks, ds, nullptr, BH, t, g) || g.nwg < 1024)
+                    if (!geo_from_tiling(rank, extents, ks, ds, nullptr, BH, t, g, forward) ||
+                        g.nwg < 1024)
                         continue;
                 }
                 double keys = 16.0 * ((std::min(w + ks[inner] - 1, glen[inner]) + 15) / 16);
@@ -238,7 +255,8 @@ na_tiling model_tiling(int rank, const int64_t* extents, const int32_t* ks, cons
         const int fw = env_choice("NA_FWD_WAVES", 4, 8);
         na::Geo g4;
         if (fw == 8 || (fw == 0 && ks[0] >= 512 &&
-                        geo_from_tiling(1, extents, ks, ds, nullptr, BH, best, g4) && g4.nwg >= 2048))
+                        geo_from_tiling(1, extents, ks, ds, nullptr, BH, best, g4, true) &&
+                        g4.nwg >= 2048))
             best.waves[0] = 8;
     }
     return best;
@@ -304,9 +322,8 @@ bool same_tiling(const na_tiling& a, const na_tiling& b) {
 
 // Candidate tilings: the heuristic one, then every valid factorisation
 // whose workgroup tile is no longer than twice an axis's longest group
-// (rounded up to a power of two) and whose wave tile along the innermost
-// axis is at least 4 (2-D, 3-D), at most kMaxCandidates in all.
-constexpr int kMaxCandidates = 64;
+// (rounded up to a power of two), whose wave tile along the innermost axis is
+// at least 4 (2-D, 3-D) and whose launch fits (grid_fits).
 std::vector<na_tiling> candidates(int rank, const int64_t* extents, const int32_t* ks,
                                   const int32_t* ds, int64_t BH, int64_t head_dim, na_dtype dtype,
                                   bool forward) {
@@ -341,14 +358,249 @@ std::vector<na_tiling> candidates(int rank, const int64_t* extents, const int32_
                                             ok = false;
                                     }
                                     if (!ok || !valid_tiling(rank, dtype, forward, t)) continue;
+                                    na::Geo g;
+                                    if (!geo_from_tiling(rank, extents, ks, ds, nullptr, BH, t, g,
+                                                         forward))
+                                        continue;
                                     bool dup = false;
                                     for (const auto& c : out) dup = dup || same_tiling(c, t);
-                                    if (!dup && (int)out.size() < kMaxCandidates) out.push_back(t);
+                                    if (!dup) out.push_back(t);
                                 }
                 }
     }
     return out;
 }
+
+// The heuristic forward and backward launches of a valid problem fit
+// (grid_fits); NA_ERR_SHAPE otherwise.
+na_status check_launchable(int rank, const int64_t* extents, const int32_t* ks, const int32_t* ds,
+                           int64_t batch, int64_t heads, int64_t head_dim, na_dtype dtype) {
+    const int64_t BH = batch * heads;
+    na::Geo g;
+    if (!geo_from_tiling(rank, extents, ks, ds, nullptr, BH,
+                         default_forward_tiling(rank, extents, ks, ds, BH, head_dim, dtype), g,
+                         true) ||
+        !geo_from_tiling(rank, extents, ks, ds, nullptr, BH,
+                         default_backward_tiling(rank, extents, ks, ds, BH, head_dim, dtype), g,
+                         false))
+        return NA_ERR_SHAPE;
+    return NA_OK;
+}
+
+na_status check_all(int rank, const int64_t* extents, const int32_t* ks, const int32_t* ds,
+                    int64_t batch, int64_t heads, int64_t head_dim, na_dtype dtype, float scale) {
+    na_status st = check_problem(rank, extents, ks, ds, batch, heads, head_dim, dtype, scale);
+    if (st != NA_OK) return st;
+    return check_launchable(rank, extents, ks, ds, batch, heads, head_dim, dtype);
+}
+
+// Launchers for a validated, non-empty problem with checked pointers.
+na_status run_forward(int rank, const int64_t* extents, const int32_t* ks, const int32_t* ds,
+                      const int32_t* causal, int64_t BH, int64_t head_dim, na_dtype dtype,
+                      float scale, const na_tiling& t, const void* q, const void* k,
+                      const void* v, void* out, float* lse, hipStream_t s) {
+    na::Geo g;
+    if (!geo_from_tiling(rank, extents, ks, ds, causal, BH, t, g, true)) return NA_ERR_SHAPE;
+    hipError_t e = na::launch_forward(g, rank, (int)head_dim, (int)dtype, t.blocks_per_wave, q, k,
+                                      v, out, lse, scale, s);
+    return e == hipSuccess ? NA_OK : NA_ERR_HIP;
+}
+
+na_status run_backward(int rank, const int64_t* extents, const int32_t* ks, const int32_t* ds,
+                       const int32_t* causal, int64_t BH, int64_t head_dim, na_dtype dtype,
+                       float scale, const na_tiling& t, const void* q, const void* k,
+                       const void* v, const void* out, const float* lse, const void* dout,
+                       void* dq, void* dk, void* dv, hipStream_t s) {
+    na::Geo g;
+    if (!geo_from_tiling(rank, extents, ks, ds, causal, BH, t, g, false)) return NA_ERR_SHAPE;
+    hipError_t e = na::launch_backward(g, rank, (int)head_dim, (int)dtype, t.blocks_per_wave, q,
+                                       k, v, out, lse, dout, dq, dk, dv, scale, s);
+    return e == hipSuccess ? NA_OK : NA_ERR_HIP;
+}
+
+na_status forward_pointers(const void* q, const void* k, const void* v, const void* out,
+                           const float* lse) {
+    if (!q || !k || !v || !out || !lse) return NA_ERR_NULL;
+    if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(out) || !aligned16(lse))
+        return NA_ERR_ALIGNMENT;
+    return NA_OK;
+}
+
+na_status backward_pointers(const void* q, const void* k, const void* v, const void* out,
+                            const float* lse, const void* dout, const void* dq, const void* dk,
+                            const void* dv) {
+    if (!q || !k || !v || !out || !lse || !dout || !dq || !dk || !dv) return NA_ERR_NULL;
+    const void* ptrs[] = {q, k, v, out, lse, dout, dq, dk, dv};
+    for (const void* p : ptrs)
+        if (!aligned16(p)) return NA_ERR_ALIGNMENT;
+    return NA_OK;
+}
+
+// ---- the auto-tuner (App. A): time candidate tilings on the caller's buffers ----
+// Candidates timed by default (the heuristic one and the next ones in
+// enumeration order); NA_TUNE_THOROUGH times every candidate.
+constexpr int kDefaultCandidates = 64;
+
+// Times launches of a candidate list on one stream and picks one: after a
+// warm-up of the heuristic (candidate 0), every candidate is timed once over
+// `reps` launches (after one launch of its own); the three fastest and the
+// heuristic are then timed again back to back, and the heuristic stays
+// unless another finalist beats it by more than 2 %.
+class Tuner {
+  public:
+    Tuner(hipStream_t s, int reps) : s_(s), reps_(reps < 1 ? 1 : reps) {
+        ok_ = hipEventCreate(&e0_) == hipSuccess && hipEventCreate(&e1_) == hipSuccess;
+    }
+    ~Tuner() {
+        if (e0_) (void)hipEventDestroy(e0_);
+        if (e1_) (void)hipEventDestroy(e1_);
+    }
+    bool ok() const { return ok_; }
+
+    template <class Launch>
+    na_status pick(std::vector<na_tiling> c, bool thorough, Launch launch, na_tiling& chosen,
+                   float& t_best, float& t_heur) {
+        if (!thorough && (int)c.size() > kDefaultCandidates) c.resize(kDefaultCandidates);
+        for (int r = 0; r < 3 * reps_; ++r)
+            if (launch(c[0]) != NA_OK) return NA_ERR_HIP;
+        std::vector<float> t1(c.size());
+        for (size_t i = 0; i < c.size(); ++i) {
+            t1[i] = time_it([&] { return launch(c[i]); });
+            if (t1[i] < 0.f) return NA_ERR_HIP;
+        }
+        std::vector<size_t> order(c.size());
+        for (size_t i = 0; i < c.size(); ++i) order[i] = i;
+        std::sort(order.begin(), order.end(), [&](size_t a, size_t b) { return t1[a] < t1[b]; });
+        std::vector<size_t> fin = {0};
+        for (size_t j = 0; j < order.size() && fin.size() < 4; ++j)
+            if (order[j] != 0) fin.push_back(order[j]);
+        size_t best = 0;
+        float tb = -1.f;
+        for (size_t i : fin) {
+            const float t = time_it([&] { return launch(c[i]); });
+            if (t < 0.f) return NA_ERR_HIP;
+            if (i == 0) t_heur = t;
+            if (tb < 0.f || t < tb) {
+                tb = t;
+                best = i;
+            }
+        }
+        if (best != 0 && tb > 0.98f * t_heur) {
+            best = 0;
+            tb = t_heur;
+        }
+        chosen = c[best];
+        t_best = tb;
+        return NA_OK;
+    }
+
+  private:
+    // ms per launch of `launch` (one launch first, untimed), or < 0 on failure
+    template <class Launch>
+    float time_it(Launch launch) {
+        if (launch() != NA_OK) return -1.f;
+        if (hipEventRecord(e0_, s_) != hipSuccess) return -1.f;
+        for (int r = 0; r < reps_; ++r)
+            if (launch() != NA_OK) return -1.f;
+        float ms = 0.f;
+        if (hipEventRecord(e1_, s_) != hipSuccess || hipEventSynchronize(e1_) != hipSuccess ||
+            hipEventElapsedTime(&ms, e0_, e1_) != hipSuccess)
+            return -1.f;
+        return ms / reps_;
+    }
+    hipStream_t s_;
+    int reps_;
+    bool ok_ = false;
+    hipEvent_t e0_ = nullptr, e1_ = nullptr;
+};
+
+// Tunes the forward tiling of a valid, non-empty problem; the buffers end up
+// holding the result of the chosen tiling.
+na_status tune_forward(int rank, const int64_t* extents, const int32_t* ks, const int32_t* ds,
+                       const int32_t* causal, int64_t BH, int64_t head_dim, na_dtype dtype,
+                       float scale, const void* q, const void* k, const void* v, void* out,
+                       float* lse, int reps, bool thorough, hipStream_t s, na_tiling& chosen,
+                       float& t_best, float& t_heur) {
+    Tuner tuner(s, reps);
+    if (!tuner.ok()) return NA_ERR_HIP;
+    na_status st = tuner.pick(
+        candidates(rank, extents, ks, ds, BH, head_dim, dtype, true), thorough,
+        [&](const na_tiling& t) {
+            return run_forward(rank, extents, ks, ds, causal, BH, head_dim, dtype, scale, t, q, k,
+                               v, out, lse, s);
+        },
+        chosen, t_best, t_heur);
+    if (st != NA_OK) return st;
+    return run_forward(rank, extents, ks, ds, causal, BH, head_dim, dtype, scale, chosen, q, k, v,
+                       out, lse, s);
+}
+
+na_status tune_backward(int rank, const int64_t* extents, const int32_t* ks, const int32_t* ds,
+                        const int32_t* causal, int64_t BH, int64_t head_dim, na_dtype dtype,
+                        float scale, const void* q, const void* k, const void* v, const void* out,
+                        const float* lse, const void* dout, void* dq, void* dk, void* dv,
+                        int reps, bool thorough, hipStream_t s, na_tiling& chosen, float& t_best,
+                        float& t_heur) {
+    Tuner tuner(s, reps);
+    if (!tuner.ok()) return NA_ERR_HIP;
+    na_status st = tuner.pick(
+        candidates(rank, extents, ks, ds, BH, head_dim, dtype, false), thorough,
+        [&](const na_tiling& t) {
+            return run_backward(rank, extents, ks, ds, causal, BH, head_dim, dtype, scale, t, q, k,
+                                v, out, lse, dout, dq, dk, dv, s);
+        },
+        chosen, t_best, t_heur);
+    if (st != NA_OK) return st;
+    return run_backward(rank, extents, ks, ds, causal, BH, head_dim, dtype, scale, chosen, q, k, v,
+                        out, lse, dout, dq, dk, dv, s);
+}
+
+void cache_store(const std::vector<int64_t>& key, const na_tiling* fwd, const na_tiling* bwd) {
+    std::lock_guard<std::mutex> lock(g_cache_mu);
+    Tuned& e = tiling_cache()[key];
+    if (fwd) {
+        e.has_fwd = true;
+        e.fwd = *fwd;
+    }
+    if (bwd) {
+        e.has_bwd = true;
+        e.bwd = *bwd;
+    }
+}
+
+bool cache_has(const std::vector<int64_t>& key, bool forward) {
+    std::lock_guard<std::mutex> lock(g_cache_mu);
+    auto& cache = tiling_cache();
+    auto it = cache.find(key);
+    return it != cache.end() && (forward ? it->second.has_fwd : it->second.has_bwd);
+}
+
+// Tune-on-miss mode: -1 until first read (then from NA_AUTOTUNE: 0 off,
+// 1 on, 2 on and thorough), or as set by na_set_autotune.
+std::atomic<int> g_autotune{-1};
+
+int autotune_mode() {
+    int m = g_autotune.load();
+    if (m < 0) {
+        const char* env = std::getenv("NA_AUTOTUNE");
+        const int v = env ? std::atoi(env) : 0;
+        m = (v == 1 || v == 2) ? v : 0;
+        int expected = -1;
+        g_autotune.compare_exchange_strong(expected, m);
+        m = g_autotune.load();
+    }
+    return m;
+}
+
+// Tuning synchronises the stream, which a stream being captured into a graph
+// does not allow: such calls use the cached or heuristic tiling.
+bool stream_capturing(hipStream_t s) {
+    hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+    if (hipStreamIsCapturing(s, &cs) != hipSuccess) return true;
+    return cs != hipStreamCaptureStatusNone;
+}
+
+constexpr int kAutotuneRepeats = 3;
 
 }  // namespace
 
@@ -379,75 +631,39 @@ na_status na_validate(int rank, const int64_t* extents, const int32_t* kernel_si
                       const int32_t* dilation, const int32_t* causal, int64_t batch, int64_t heads,
                       int64_t head_dim, na_dtype dtype, float scale) {
     (void)causal;  // any value is legal (NULL: no causal axis)
-    return check_problem(rank, extents, kernel_size, dilation, batch, heads, head_dim, dtype,
-                         scale);
+    return check_all(rank, extents, kernel_size, dilation, batch, heads, head_dim, dtype, scale);
 }
-
-}  // extern "C"
-
-namespace {
-
-// Launchers for a validated, non-empty problem with checked pointers.
-na_status run_forward(int rank, const int64_t* extents, const int32_t* ks, const int32_t* ds,
-                      const int32_t* causal, int64_t BH, int64_t head_dim, na_dtype dtype,
-                      float scale, const na_tiling& t, const void* q, const void* k,
-                      const void* v, void* out, float* lse, hipStream_t s) {
-    na::Geo g;
-    if (!geo_from_tiling(rank, extents, ks, ds, causal, BH, t, g)) return NA_ERR_SHAPE;
-    hipError_t e = na::launch_forward(g, rank, (int)head_dim, (int)dtype, t.blocks_per_wave, q, k,
-                                      v, out, lse, scale, s);
-    return e == hipSuccess ? NA_OK : NA_ERR_HIP;
-}
-
-na_status run_backward(int rank, const int64_t* extents, const int32_t* ks, const int32_t* ds,
-                       const int32_t* causal, int64_t BH, int64_t head_dim, na_dtype dtype,
-                       float scale, const na_tiling& t, const void* q, const void* k,
-                       const void* v, const void* out, const float* lse, const void* dout,
-                       void* dq, void* dk, void* dv, hipStream_t s) {
-    na::Geo g;
-    if (!geo_from_tiling(rank, extents, ks, ds, causal, BH, t, g)) return NA_ERR_SHAPE;
-    hipError_t e = na::launch_backward(g, rank, (int)head_dim, (int)dtype, t.blocks_per_wave, q,
-                                       k, v, out, lse, dout, dq, dk, dv, scale, s);
-    return e == hipSuccess ? NA_OK : NA_ERR_HIP;
-}
-
-na_status forward_pointers(const void* q, const void* k, const void* v, const void* out,
-                           const float* lse) {
-    if (!q || !k || !v || !out || !lse) return NA_ERR_NULL;
-    if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(out) || !aligned16(lse))
-        return NA_ERR_ALIGNMENT;
-    return NA_OK;
-}
-
-na_status backward_pointers(const void* q, const void* k, const void* v, const void* out,
-                            const float* lse, const void* dout, const void* dq, const void* dk,
-                            const void* dv) {
-    if (!q || !k || !v || !out || !lse || !dout || !dq || !dk || !dv) return NA_ERR_NULL;
-    const void* ptrs[] = {q, k, v, out, lse, dout, dq, dk, dv};
-    for (const void* p : ptrs)
-        if (!aligned16(p)) return NA_ERR_ALIGNMENT;
-    return NA_OK;
-}
-
-}  // namespace
-
-extern "C" {
 
 na_status na_forward(int rank, const int64_t* extents, const int32_t* kernel_size,
                      const int32_t* dilation, const int32_t* causal, int64_t batch, int64_t heads,
                      int64_t head_dim, na_dtype dtype, float scale, const void* q, const void* k,
                      const void* v, void* out, float* logsumexp, na_stream_t stream) {
-    na_status st = check_problem(rank, extents, kernel_size, dilation, batch, heads, head_dim,
-                                 dtype, scale);
+    na_status st = check_all(rank, extents, kernel_size, dilation, batch, heads, head_dim, dtype,
+                             scale);
     if (st != NA_OK) return st;
     if (empty_problem(rank, extents, batch, heads)) return NA_OK;
     st = forward_pointers(q, k, v, out, logsumexp);
     if (st != NA_OK) return st;
     const int64_t BH = batch * heads;
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    const int mode = autotune_mode();
+    if (mode) {
+        const auto key = problem_key(rank, extents, kernel_size, dilation, causal, BH, head_dim,
+                                     dtype);
+        if (!cache_has(key, true) && !stream_capturing(s)) {
+            na_tiling t;
+            float tb = 0.f, th = 0.f;
+            st = tune_forward(rank, extents, kernel_size, dilation, causal, BH, head_dim, dtype,
+                              scale, q, k, v, out, logsumexp, kAutotuneRepeats, mode == 2, s, t,
+                              tb, th);
+            if (st == NA_OK) cache_store(key, &t, nullptr);
+            return st;
+        }
+    }
     const na_tiling t = current_tiling(rank, extents, kernel_size, dilation, causal, BH, head_dim,
                                        dtype, true);
     return run_forward(rank, extents, kernel_size, dilation, causal, BH, head_dim, dtype, scale, t,
-                       q, k, v, out, logsumexp, reinterpret_cast<hipStream_t>(stream));
+                       q, k, v, out, logsumexp, s);
 }
 
 na_status na_backward(int rank, const int64_t* extents, const int32_t* kernel_size,
@@ -455,25 +671,39 @@ na_status na_backward(int rank, const int64_t* extents, const int32_t* kernel_si
                       int64_t head_dim, na_dtype dtype, float scale, const void* q, const void* k,
                       const void* v, const void* out, const float* logsumexp, const void* dout,
                       void* dq, void* dk, void* dv, na_stream_t stream) {
-    na_status st = check_problem(rank, extents, kernel_size, dilation, batch, heads, head_dim,
-                                 dtype, scale);
+    na_status st = check_all(rank, extents, kernel_size, dilation, batch, heads, head_dim, dtype,
+                             scale);
     if (st != NA_OK) return st;
     if (empty_problem(rank, extents, batch, heads)) return NA_OK;
     st = backward_pointers(q, k, v, out, logsumexp, dout, dq, dk, dv);
     if (st != NA_OK) return st;
     const int64_t BH = batch * heads;
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    const int mode = autotune_mode();
+    if (mode) {
+        const auto key = problem_key(rank, extents, kernel_size, dilation, causal, BH, head_dim,
+                                     dtype);
+        if (!cache_has(key, false) && !stream_capturing(s)) {
+            na_tiling t;
+            float tb = 0.f, th = 0.f;
+            st = tune_backward(rank, extents, kernel_size, dilation, causal, BH, head_dim, dtype,
+                               scale, q, k, v, out, logsumexp, dout, dq, dk, dv, kAutotuneRepeats,
+                               mode == 2, s, t, tb, th);
+            if (st == NA_OK) cache_store(key, nullptr, &t);
+            return st;
+        }
+    }
     const na_tiling t = current_tiling(rank, extents, kernel_size, dilation, causal, BH, head_dim,
                                        dtype, false);
     return run_backward(rank, extents, kernel_size, dilation, causal, BH, head_dim, dtype, scale,
-                        t, q, k, v, out, logsumexp, dout, dq, dk, dv,
-                        reinterpret_cast<hipStream_t>(stream));
+                        t, q, k, v, out, logsumexp, dout, dq, dk, dv, s);
 }
 
 int na_candidate_tilings(int rank, const int64_t* extents, const int32_t* kernel_size,
                          const int32_t* dilation, int64_t batch, int64_t heads, int64_t head_dim,
                          na_dtype dtype, int forward, na_tiling* out, int max) {
-    na_status st = check_problem(rank, extents, kernel_size, dilation, batch, heads, head_dim,
-                                 dtype, 1.0f);
+    na_status st = check_all(rank, extents, kernel_size, dilation, batch, heads, head_dim, dtype,
+                             1.0f);
     if (st != NA_OK) return -(int)st;
     const auto c = candidates(rank, extents, kernel_size, dilation, batch * heads, head_dim, dtype,
                               forward != 0);
@@ -485,8 +715,8 @@ na_status na_current_tiling(int rank, const int64_t* extents, const int32_t* ker
                             const int32_t* dilation, const int32_t* causal, int64_t batch,
                             int64_t heads, int64_t head_dim, na_dtype dtype, int forward,
                             na_tiling* out) {
-    na_status st = check_problem(rank, extents, kernel_size, dilation, batch, heads, head_dim,
-                                 dtype, 1.0f);
+    na_status st = check_all(rank, extents, kernel_size, dilation, batch, heads, head_dim, dtype,
+                             1.0f);
     if (st != NA_OK) return st;
     if (!out) return NA_ERR_NULL;
     *out = current_tiling(rank, extents, kernel_size, dilation, causal, batch * heads, head_dim,
@@ -499,8 +729,8 @@ na_status na_forward_tiled(int rank, const int64_t* extents, const int32_t* kern
                            int64_t heads, int64_t head_dim, na_dtype dtype, float scale,
                            const na_tiling* tiling, const void* q, const void* k, const void* v,
                            void* out, float* logsumexp, na_stream_t stream) {
-    na_status st = check_problem(rank, extents, kernel_size, dilation, batch, heads, head_dim,
-                                 dtype, scale);
+    na_status st = check_all(rank, extents, kernel_size, dilation, batch, heads, head_dim, dtype,
+                             scale);
     if (st != NA_OK) return st;
     if (!tiling) return NA_ERR_NULL;
     if (!valid_tiling(rank, dtype, true, *tiling)) return NA_ERR_TILING;
@@ -518,8 +748,8 @@ na_status na_backward_tiled(int rank, const int64_t* extents, const int32_t* ker
                             const na_tiling* tiling, const void* q, const void* k, const void* v,
                             const void* out, const float* logsumexp, const void* dout, void* dq,
                             void* dk, void* dv, na_stream_t stream) {
-    na_status st = check_problem(rank, extents, kernel_size, dilation, batch, heads, head_dim,
-                                 dtype, scale);
+    na_status st = check_all(rank, extents, kernel_size, dilation, batch, heads, head_dim, dtype,
+                             scale);
     if (st != NA_OK) return st;
     if (!tiling) return NA_ERR_NULL;
     if (!valid_tiling(rank, dtype, false, *tiling)) return NA_ERR_TILING;
@@ -535,11 +765,13 @@ na_status na_tune(int rank, const int64_t* extents, const int32_t* kernel_size,
                   const int32_t* dilation, const int32_t* causal, int64_t batch, int64_t heads,
                   int64_t head_dim, na_dtype dtype, float scale, const void* q, const void* k,
                   const void* v, void* out, float* logsumexp, const void* dout, void* dq, void* dk,
-                  void* dv, int repeats, na_stream_t stream, na_tiling* best_forward,
+                  void* dv, int repeats, int flags, na_stream_t stream, na_tiling* best_forward,
                   na_tiling* best_backward, float* times_ms) {
-    na_status st = check_problem(rank, extents, kernel_size, dilation, batch, heads, head_dim,
-                                 dtype, scale);
+    na_status st = check_all(rank, extents, kernel_size, dilation, batch, heads, head_dim, dtype,
+                             scale);
     if (st != NA_OK) return st;
+    if (flags & ~NA_TUNE_THOROUGH) return NA_ERR_TILING;
+    const bool thorough = (flags & NA_TUNE_THOROUGH) != 0;
     const int64_t BH = batch * heads;
     na_tiling bf = default_forward_tiling(rank, extents, kernel_size, dilation, BH, head_dim, dtype);
     na_tiling bb = default_backward_tiling(rank, extents, kernel_size, dilation, BH, head_dim, dtype);
@@ -547,98 +779,18 @@ na_status na_tune(int rank, const int64_t* extents, const int32_t* kernel_size,
     if (!empty_problem(rank, extents, batch, heads)) {
         st = backward_pointers(q, k, v, out, logsumexp, dout, dq, dk, dv);
         if (st != NA_OK) return st;
-        const int reps = repeats < 1 ? 1 : repeats;
         hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-        hipEvent_t e0 = nullptr, e1 = nullptr;
-        if (hipEventCreate(&e0) != hipSuccess || hipEventCreate(&e1) != hipSuccess) {
-            if (e0) (void)hipEventDestroy(e0);
-            return NA_ERR_HIP;
-        }
-        // ms per launch of `launch` (one warm-up launch first), or < 0 on failure
-        auto time_it = [&](auto launch) -> float {
-            if (launch() != NA_OK) return -1.f;
-            if (hipEventRecord(e0, s) != hipSuccess) return -1.f;
-            for (int r = 0; r < reps; ++r)
-                if (launch() != NA_OK) return -1.f;
-            float ms = 0.f;
-            if (hipEventRecord(e1, s) != hipSuccess || hipEventSynchronize(e1) != hipSuccess ||
-                hipEventElapsedTime(&ms, e0, e1) != hipSuccess)
-                return -1.f;
-            return ms / reps;
-        };
-        // Picks a tiling: every candidate timed once, then the three fastest and
-        // the heuristic (candidate 0) timed again back to back; the heuristic
-        // stays unless another finalist beats it by more than 2 %.  A warm-up
-        // of the heuristic comes first, so no candidate pays for a cold GPU.
-        auto pick = [&](const std::vector<na_tiling>& c, auto launch, na_tiling& chosen,
-                        float& t_best, float& t_heur) -> na_status {
-            for (int r = 0; r < 3 * reps; ++r)
-                if (launch(c[0]) != NA_OK) return NA_ERR_HIP;
-            std::vector<float> t1(c.size());
-            for (size_t i = 0; i < c.size(); ++i) {
-                t1[i] = time_it([&] { return launch(c[i]); });
-                if (t1[i] < 0.f) return NA_ERR_HIP;
-            }
-            std::vector<size_t> order(c.size());
-            for (size_t i = 0; i < c.size(); ++i) order[i] = i;
-            std::sort(order.begin(), order.end(), [&](size_t a, size_t b) { return t1[a] < t1[b]; });
-            std::vector<size_t> fin = {0};
-            for (size_t j = 0; j < order.size() && fin.size() < 4; ++j)
-                if (order[j] != 0) fin.push_back(order[j]);
-            size_t best = 0;
-            float tb = -1.f;
-            for (size_t i : fin) {
-                const float t = time_it([&] { return launch(c[i]); });
-                if (t < 0.f) return NA_ERR_HIP;
-                if (i == 0) t_heur = t;
-                if (tb < 0.f || t < tb) {
-                    tb = t;
-                    best = i;
-                }
-            }
-            if (best != 0 && tb > 0.98f * t_heur) {
-                best = 0;
-                tb = t_heur;
-            }
-            chosen = c[best];
-            t_best = tb;
-            return NA_OK;
-        };
-        const auto fc = candidates(rank, extents, kernel_size, dilation, BH, head_dim, dtype, true);
-        st = pick(
-            fc,
-            [&](const na_tiling& t) {
-                return run_forward(rank, extents, kernel_size, dilation, causal, BH, head_dim,
-                                   dtype, scale, t, q, k, v, out, logsumexp, s);
-            },
-            bf, tm[0], tm[2]);
-        // out and logsumexp from the chosen forward, then the backward tilings
+        // out and logsumexp from the chosen forward feed the backward's tuning
+        st = tune_forward(rank, extents, kernel_size, dilation, causal, BH, head_dim, dtype, scale,
+                          q, k, v, out, logsumexp, repeats, thorough, s, bf, tm[0], tm[2]);
         if (st == NA_OK)
-            st = run_forward(rank, extents, kernel_size, dilation, causal, BH, head_dim, dtype,
-                             scale, bf, q, k, v, out, logsumexp, s);
-        const auto bc = candidates(rank, extents, kernel_size, dilation, BH, head_dim, dtype, false);
-        if (st == NA_OK)
-            st = pick(
-                bc,
-                [&](const na_tiling& t) {
-                    return run_backward(rank, extents, kernel_size, dilation, causal, BH,
-                                        head_dim, dtype, scale, t, q, k, v, out, logsumexp, dout,
-                                        dq, dk, dv, s);
-                },
-                bb, tm[1], tm[3]);
-        if (st == NA_OK)
-            st = run_backward(rank, extents, kernel_size, dilation, causal, BH, head_dim, dtype,
-                              scale, bb, q, k, v, out, logsumexp, dout, dq, dk, dv, s);
+            st = tune_backward(rank, extents, kernel_size, dilation, causal, BH, head_dim, dtype,
+                               scale, q, k, v, out, logsumexp, dout, dq, dk, dv, repeats, thorough,
+                               s, bb, tm[1], tm[3]);
         if (st == NA_OK && hipStreamSynchronize(s) != hipSuccess) st = NA_ERR_HIP;
-        (void)hipEventDestroy(e0);
-        (void)hipEventDestroy(e1);
         if (st != NA_OK) return st;
-        std::lock_guard<std::mutex> lock(g_cache_mu);
-        Tuned& e = tiling_cache()[problem_key(rank, extents, kernel_size, dilation, causal, BH,
-                                              head_dim, dtype)];
-        e.has_fwd = e.has_bwd = true;
-        e.fwd = bf;
-        e.bwd = bb;
+        cache_store(problem_key(rank, extents, kernel_size, dilation, causal, BH, head_dim, dtype),
+                    &bf, &bb);
     }
     if (best_forward) *best_forward = bf;
     if (best_backward) *best_backward = bb;
@@ -651,6 +803,10 @@ void na_tune_clear(void) {
     std::lock_guard<std::mutex> lock(g_cache_mu);
     tiling_cache().clear();
 }
+
+void na_set_autotune(int mode) { g_autotune.store(mode == 1 || mode == 2 ? mode : 0); }
+
+int na_autotune(void) { return autotune_mode(); }
 
 na_status na_debug_windows(int rank, const int64_t* extents, const int32_t* kernel_size,
                            const int32_t* dilation, const int32_t* causal, int32_t* start,

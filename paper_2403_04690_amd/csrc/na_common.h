@@ -15,6 +15,7 @@
 
 #include <type_traits>
 
+#include "na_fastdiv.h"
 #include "na_index.h"
 
 namespace na {
@@ -196,36 +197,6 @@ __device__ __forceinline__ float dot8(typename Tr<T>::x8 a, typename Tr<T>::x8 b
 }
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
-
-// Division by a divisor that stays fixed for a whole launch or workgroup:
-// q = (umulhi(n, mul) + n) >> shr, exact for 0 <= n < 2^31 and d >= 1.
-// The multiplier is floor(2^32 (2^s - d) / d) + 1 with s = ceil(log2 d); on
-// the device it is formed with one double division (exact for d < 2^20,
-// since 2^32 (2^s - d) < 2^52 and the quotient's fractional part exceeds the
-// rounding error), on the host in 64-bit integers.
-struct FastDiv {
-    uint32_t mul, shr;
-    NA_HD void init(int d) {
-        uint32_t s = 0;
-        while ((1u << s) < (uint32_t)d) ++s;
-        shr = s;
-        const uint64_t a = ((uint64_t)1 << s) - (uint64_t)d;
-#if defined(__HIP_DEVICE_COMPILE__)
-        if (d < (1 << 20)) {
-            mul = (uint32_t)((uint64_t)__builtin_floor((double)a * 4294967296.0 / (double)d) + 1);
-            return;
-        }
-#endif
-        mul = (uint32_t)((a << 32) / (uint64_t)d + 1);
-    }
-    NA_HD int div(int n) const {
-#if defined(__HIP_DEVICE_COMPILE__)
-        return (int)((__umulhi((uint32_t)n, mul) + (uint32_t)n) >> shr);
-#else
-        return (int)((((uint64_t)(uint32_t)n * mul >> 32) + (uint32_t)n) >> shr);
-#endif
-    }
-};
 
 // Problem geometry shared by all kernels (filled on the host).  Axes beyond
 // the problem's rank are inert (extent 1, window 1, dilation 1).

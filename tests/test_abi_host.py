@@ -174,9 +174,15 @@ def test_candidate_tilings_are_valid_and_start_with_the_heuristic(lib, ext, ks, 
     rank = len(ext)
     r, e, k, d = _args(rank, ext, ks, ds)
     n = lib.na_candidate_tilings(r, e, k, d, 2, 4, D, dt, fwd, None, 0)
-    assert 1 <= n <= 64
+    assert n >= 1
     buf = (_Tiling * n)()
     assert lib.na_candidate_tilings(r, e, k, d, 2, 4, D, dt, fwd, buf, n) == n
+    # a short buffer gets the first entries and the call still returns the total
+    short = (_Tiling * 2)()
+    assert lib.na_candidate_tilings(r, e, k, d, 2, 4, D, dt, fwd, short, 1) == n
+    assert short[1].blocks_per_wave == 0
+    assert (short[0].blocks_per_wave, tuple(short[0].wave_tile)) == \
+        (buf[0].blocks_per_wave, tuple(buf[0].wave_tile))
     seen = set()
     for t in buf:
         wt, wg = tuple(t.wave_tile), tuple(t.waves)
@@ -285,3 +291,50 @@ def test_tiling_status_string_and_cache_clear(lib):
     cur = _tiling_type()()
     assert lib.na_current_tiling(r, e, k, d, None, 2, 3, 64, 1, 1, ctypes.byref(cur)) == NA_OK
     assert cur.blocks_per_wave in (1, 2)
+
+
+def test_candidate_count_is_the_total_beyond_the_tuner_default(lib):
+    """3-D 7x7x7 with dilation (1, 2, 2): more admissible tilings than na_tune times by
+    default (64); na_candidate_tilings counts them all."""
+    r, e, k, d = _args(3, (16, 64, 64), (7, 7, 7), (1, 2, 2))
+    n = lib.na_candidate_tilings(r, e, k, d, 1, 8, 64, 1, 1, None, 0)
+    assert n > 64
+    buf = (_tiling_type() * n)()
+    assert lib.na_candidate_tilings(r, e, k, d, 1, 8, 64, 1, 1, buf, n) == n
+    keys = {(t.blocks_per_wave, tuple(t.wave_tile), tuple(t.waves)) for t in buf}
+    assert len(keys) == n
+    assert any(t.blocks_per_wave == 2 for t in buf[64:])
+
+
+def test_tune_rejects_unknown_flags_before_any_launch(lib):
+    r, e, k, d = _args()
+    fake = ctypes.c_void_p(4096)  # never dereferenced: the flags are checked first
+    st = lib.na_tune(r, e, k, d, None, 2, 3, 64, 1, 0.125, *([fake] * 9), 3, 4, None, None,
+                     None, None)
+    assert st == NA_ERR_TILING
+
+
+def test_autotune_mode_set_and_read(lib):
+    before = lib.na_autotune()
+    try:
+        for m in (1, 2, 0):
+            lib.na_set_autotune(m)
+            assert lib.na_autotune() == m
+        lib.na_set_autotune(7)  # unknown modes turn it off
+        assert lib.na_autotune() == 0
+    finally:
+        lib.na_set_autotune(before)
+
+
+@pytest.mark.parametrize("B,H,ok", [(1 << 22, 1, True), (1 << 23, 1, False), (1 << 12, 1 << 10, True),
+                                    (1 << 12, 1 << 11, False)])
+def test_launches_beyond_the_grid_limit_are_rejected(lib, B, H, ok):
+    """1-D L = 16 (one 64-query tile per slice): the backward launches 2 * B * H workgroups of
+    256 threads, which must stay below 2^32 threads, so B * H < 2^23."""
+    r, e, k, d = _args(1, (16,), (3,), (1,))
+    want = NA_OK if ok else NA_ERR_SHAPE
+    assert lib.na_validate(r, e, k, d, None, B, H, 32, 1, 0.125) == want
+    fake = ctypes.c_void_p(4096)
+    if not ok:  # refused before any pointer is read
+        assert lib.na_forward(r, e, k, d, None, B, H, 32, 1, 0.125, *([fake] * 5), None) == want
+        assert lib.na_backward(r, e, k, d, None, B, H, 32, 1, 0.125, *([fake] * 9), None) == want
