@@ -248,6 +248,66 @@ na_status na_debug_windows(int rank, const int64_t* extents, const int32_t* kern
                            const int32_t* dilation, const int32_t* causal, int32_t* start,
                            int32_t* inv_lo, int32_t* inv_hi, na_stream_t stream);
 
+/*
+ * Unfused operators: the baseline the fused kernels are measured against.
+ * The paper builds NA from separate operators (Sec. 3.1) that each read or
+ * write the l-wide attention weights (l = prod_a kernel_size[a] per query) in
+ * global memory; its naive and GEMM-based kernels (Sec. 3.1-3.2, Tables
+ * "runtime_breakdown" and "runtime_breakdown_backward") work that way.  These
+ * entry points are that design on this GPU, one launch per operator:
+ *   forward   W = PN(q, k) * scale;  P = softmax(W);  out = NN(P, v)
+ *   backward  dP = PN(dout, v);  dA = softmax_backward(P, dP);
+ *             dq = NN(dA, k) * scale;  dk = IN(dA, q) * scale;  dv = IN(P, dout)
+ * They give the same results as na_forward / na_backward up to rounding (the
+ * weights are stored in the inputs' type), but move l-wide rows through
+ * memory instead of keeping them in registers.
+ *
+ * Weights: contiguous [B, H, N, l] arrays of `dtype` (N = prod extents), row
+ * i holding query i's neighbours in the row-major order of the per-axis
+ * window offsets t_a (axis 0 outermost): entry e = sum_a t_a prod_{b>a} k_b
+ * is the token whose coordinate along axis a is g_a + d_a (s_a + t_a), s_a
+ * being the start of the query's window in its dilation group g_a.  Along a
+ * causal axis the window of group position p has min(k_a, p + 1) positions;
+ * entries of offsets beyond them are not neighbours (PN writes -inf, the
+ * softmax 0, the others ignore them).  The caller allocates the weights
+ * (B * H * N * l elements).
+ *
+ * Problem arguments and conventions as for na_forward (head_dim and dtype
+ * describe a, b, out and the weights; scale multiplies the result of PN, NN
+ * and IN).  All pointers 16-byte aligned; the weights are overwritten in
+ * place by na_unfused_softmax (probabilities, and the natural-log logsumexp
+ * per row in logsumexp [B, H, N] fp32) and by na_unfused_softmax_backward
+ * (grad: in dP, out dA = P * (dP - sum_e P dP) per row).  Errors as for
+ * na_forward; NA_ERR_SHAPE also when the weight tensor would exceed 2^62
+ * elements or a row 2^31 - 1.
+ *
+ * na_unfused_pn:  weights[i, e] = scale * a_i . b_j(i,e)   (PN; a, b [B, H, N, D])
+ * na_unfused_nn:  out_i = scale * sum_e weights[i, e] b_j(i,e)   (NN)
+ * na_unfused_in:  out_j = scale * sum over the queries i whose window holds j
+ *                 of weights[i, e(i, j)] b_i   (IN, the inverse neighbourhood)
+ */
+na_status na_unfused_pn(int rank, const int64_t* extents, const int32_t* kernel_size,
+                        const int32_t* dilation, const int32_t* causal, int64_t batch,
+                        int64_t heads, int64_t head_dim, na_dtype dtype, float scale,
+                        const void* a, const void* b, void* weights, na_stream_t stream);
+na_status na_unfused_softmax(int rank, const int64_t* extents, const int32_t* kernel_size,
+                             const int32_t* dilation, const int32_t* causal, int64_t batch,
+                             int64_t heads, int64_t head_dim, na_dtype dtype, void* weights,
+                             float* logsumexp, na_stream_t stream);
+na_status na_unfused_nn(int rank, const int64_t* extents, const int32_t* kernel_size,
+                        const int32_t* dilation, const int32_t* causal, int64_t batch,
+                        int64_t heads, int64_t head_dim, na_dtype dtype, float scale,
+                        const void* weights, const void* b, void* out, na_stream_t stream);
+na_status na_unfused_in(int rank, const int64_t* extents, const int32_t* kernel_size,
+                        const int32_t* dilation, const int32_t* causal, int64_t batch,
+                        int64_t heads, int64_t head_dim, na_dtype dtype, float scale,
+                        const void* weights, const void* b, void* out, na_stream_t stream);
+na_status na_unfused_softmax_backward(int rank, const int64_t* extents,
+                                      const int32_t* kernel_size, const int32_t* dilation,
+                                      const int32_t* causal, int64_t batch, int64_t heads,
+                                      int64_t head_dim, na_dtype dtype, const void* probs,
+                                      void* grad, na_stream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -20,7 +20,9 @@ import torch
 
 __all__ = ["NAError", "forward", "backward", "na_attention", "debug_windows", "validate",
            "library_path", "load_library", "DTYPES", "Tiling", "candidate_tilings",
-           "current_tiling", "tune", "tune_clear", "set_autotune", "autotune"]
+           "current_tiling", "tune", "tune_clear", "set_autotune", "autotune", "unfused_pn",
+           "unfused_softmax", "unfused_nn", "unfused_in", "unfused_softmax_backward",
+           "unfused_forward", "unfused_backward"]
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
 # NA_LIBRARY may point at another build of the same library (A/B comparisons
@@ -114,6 +116,12 @@ def load_library():
     lib.na_set_autotune.restype = None
     lib.na_autotune.argtypes = []
     lib.na_autotune.restype = ctypes.c_int
+    for name in ("na_unfused_pn", "na_unfused_nn", "na_unfused_in"):
+        getattr(lib, name).argtypes = prob + [_vp] * 4
+        getattr(lib, name).restype = ctypes.c_int
+    for name in ("na_unfused_softmax", "na_unfused_softmax_backward"):
+        getattr(lib, name).argtypes = prob[:-1] + [_vp] * 3
+        getattr(lib, name).restype = ctypes.c_int
     _lib = lib
     return lib
 
@@ -328,3 +336,117 @@ class _NAFunction(torch.autograd.Function):
 def na_attention(q, k, v, kernel_size, dilation=1, scale=None, causal=None):
     """Autograd-aware fused neighborhood attention on [B, H, X_1..X_r, D] tensors."""
     return _NAFunction.apply(q, k, v, kernel_size, dilation, scale, causal)
+
+
+# ---------------------------------------------------------------- unfused operators
+# The baseline of separate PN / softmax / NN / IN launches (na_unfused_* in na.h) that
+# read and write the l-wide attention weights [B, H, X.., l] in global memory.
+
+def _window(kernel_size, rank):
+    return int(math.prod(_per_axis(kernel_size, rank, "kernel_size")))
+
+
+def _weights_like(x, kernel_size):
+    return torch.empty(tuple(x.shape[:-1]) + (_window(kernel_size, x.dim() - 3),), dtype=x.dtype,
+                       device=x.device)
+
+
+def _check_weights(w, ref, kernel_size):
+    want = tuple(ref.shape[:-1]) + (_window(kernel_size, ref.dim() - 3),)
+    if tuple(w.shape) != want or w.dtype != ref.dtype or not w.is_contiguous() or not w.is_cuda:
+        raise ValueError(f"weights must be a contiguous {ref.dtype} GPU tensor of shape {want}")
+
+
+def _uargs(ref, kernel_size, dilation, causal):
+    B, H, D = ref.shape[0], ref.shape[1], ref.shape[-1]
+    rank, ext, ks, ds, cs = _problem_arrays(tuple(ref.shape[2:-1]), kernel_size, dilation, causal)
+    return (rank, ext, ks, ds, cs, B, H, D, DTYPES[ref.dtype])
+
+
+def unfused_pn(a, b, kernel_size, dilation=1, scale=1.0, causal=None, weights=None):
+    """PN: weights[i, e] = scale * a_i . b_j(i,e) (-inf where e is not a neighbour)."""
+    lib = load_library()
+    _check_tensors(a, b)
+    w = _weights_like(a, kernel_size) if weights is None else weights
+    _check_weights(w, a, kernel_size)
+    _check(lib.na_unfused_pn(*_uargs(a, kernel_size, dilation, causal), float(scale),
+                             a.data_ptr(), b.data_ptr(), w.data_ptr(), _stream(a.device)))
+    return w
+
+
+def unfused_softmax(weights, head_dim, kernel_size, dilation=1, causal=None, lse=None):
+    """Row softmax of the weights in place; returns (probs, logsumexp [B, H, X..] fp32)."""
+    lib = load_library()
+    ref = torch.empty(tuple(weights.shape[:-1]) + (head_dim,), dtype=weights.dtype, device="meta")
+    _check_weights(weights, ref, kernel_size)
+    if lse is None:
+        lse = torch.empty(weights.shape[:-1], dtype=torch.float32, device=weights.device)
+    rank, ext, ks, ds, cs = _problem_arrays(tuple(weights.shape[2:-1]), kernel_size, dilation,
+                                            causal)
+    _check(lib.na_unfused_softmax(rank, ext, ks, ds, cs, weights.shape[0], weights.shape[1],
+                                  head_dim, DTYPES[weights.dtype], weights.data_ptr(),
+                                  lse.data_ptr(), _stream(weights.device)))
+    return weights, lse
+
+
+def unfused_nn(weights, b, kernel_size, dilation=1, scale=1.0, causal=None, out=None):
+    """NN: out_i = scale * sum_e weights[i, e] b_j(i,e)."""
+    lib = load_library()
+    _check_tensors(b)
+    _check_weights(weights, b, kernel_size)
+    out = torch.empty_like(b) if out is None else out
+    _check_tensors(b, out)
+    _check(lib.na_unfused_nn(*_uargs(b, kernel_size, dilation, causal), float(scale),
+                             weights.data_ptr(), b.data_ptr(), out.data_ptr(), _stream(b.device)))
+    return out
+
+
+def unfused_in(weights, b, kernel_size, dilation=1, scale=1.0, causal=None, out=None):
+    """IN: out_j = scale * sum over the queries i whose window holds j of weights[i, e(i,j)] b_i."""
+    lib = load_library()
+    _check_tensors(b)
+    _check_weights(weights, b, kernel_size)
+    out = torch.empty_like(b) if out is None else out
+    _check_tensors(b, out)
+    _check(lib.na_unfused_in(*_uargs(b, kernel_size, dilation, causal), float(scale),
+                             weights.data_ptr(), b.data_ptr(), out.data_ptr(), _stream(b.device)))
+    return out
+
+
+def unfused_softmax_backward(probs, grad, head_dim, kernel_size, dilation=1, causal=None):
+    """In place on grad (dP in, dA out): dA = P * (dP - sum_e P dP) per row."""
+    lib = load_library()
+    if grad.shape != probs.shape or grad.dtype != probs.dtype or not grad.is_contiguous():
+        raise ValueError("probs and grad must be contiguous tensors of one shape and dtype")
+    rank, ext, ks, ds, cs = _problem_arrays(tuple(probs.shape[2:-1]), kernel_size, dilation,
+                                            causal)
+    if probs.shape[-1] != _window(kernel_size, rank):
+        raise ValueError("the last axis of probs must hold prod(kernel_size) weights")
+    _check(lib.na_unfused_softmax_backward(rank, ext, ks, ds, cs, probs.shape[0], probs.shape[1],
+                                           head_dim, DTYPES[probs.dtype], probs.data_ptr(),
+                                           grad.data_ptr(), _stream(probs.device)))
+    return grad
+
+
+def unfused_forward(q, k, v, kernel_size, dilation=1, scale=None, causal=None, weights=None):
+    """Unfused NA forward: PN, softmax, NN as three launches.  Returns (out, lse, probs)."""
+    D = q.shape[-1]
+    scale = 1.0 / math.sqrt(D) if scale is None else scale
+    w = unfused_pn(q, k, kernel_size, dilation, scale, causal, weights)
+    p, lse = unfused_softmax(w, D, kernel_size, dilation, causal)
+    out = unfused_nn(p, v, kernel_size, dilation, 1.0, causal)
+    return out, lse, p
+
+
+def unfused_backward(q, k, v, probs, dout, kernel_size, dilation=1, scale=None, causal=None,
+                     grad_weights=None):
+    """Unfused NA backward from the forward's probabilities: PN, softmax backward, NN and two
+    IN launches.  Returns (dq, dk, dv)."""
+    D = q.shape[-1]
+    scale = 1.0 / math.sqrt(D) if scale is None else scale
+    dp = unfused_pn(dout, v, kernel_size, dilation, 1.0, causal, grad_weights)
+    da = unfused_softmax_backward(probs, dp, D, kernel_size, dilation, causal)
+    dq = unfused_nn(da, k, kernel_size, dilation, scale, causal)
+    dk = unfused_in(da, q, kernel_size, dilation, scale, causal)
+    dv = unfused_in(probs, dout, kernel_size, dilation, 1.0, causal)
+    return dq, dk, dv

@@ -11,7 +11,7 @@ INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libna.so")
 
-SOURCES = ["na_fwd.hip", "na_bwd.hip", "na_debug.hip", "na_api.cpp"]
+SOURCES = ["na_fwd.hip", "na_bwd.hip", "na_unfused.hip", "na_debug.hip", "na_api.cpp"]
 ARCH = os.environ.get("NA_OFFLOAD_ARCH", "gfx950")
 # Packed fp32 instructions stay off: the compiler must not form v_pk_*_f32.
 FLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", "-Wall",

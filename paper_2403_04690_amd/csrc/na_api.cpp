@@ -602,6 +602,63 @@ bool stream_capturing(hipStream_t s) {
 
 constexpr int kAutotuneRepeats = 3;
 
+// ---- the unfused operators (Sec. 3.1) ----
+// Geometry of a valid problem; false if its weight tensor cannot be indexed
+// (more than 2^31 - 1 weights per row or 2^62 in all).
+bool ugeo_from_problem(int rank, const int64_t* extents, const int32_t* ks, const int32_t* ds,
+                       const int32_t* causal, int64_t BH, na::UGeo& u) {
+    std::memset(&u, 0, sizeof(u));
+    int64_t ell = 1;
+    for (int a = 0; a < 3; ++a) {
+        u.L[a] = a < rank ? (int)extents[a] : 1;
+        u.k[a] = a < rank ? ks[a] : 1;
+        u.d[a] = a < rank ? ds[a] : 1;
+        u.causal[a] = a < rank && causal && causal[a] ? 1 : 0;
+        ell *= u.k[a];
+    }
+    if (ell >= (int64_t(1) << 31)) return false;
+    int s = 1, ks_ = 1;
+    for (int a = 2; a >= 0; --a) {
+        u.ts[a] = a < rank ? s : 0;
+        s *= u.L[a];
+        u.kst[a] = ks_;
+        ks_ *= u.k[a];
+    }
+    u.N = (int)token_count(rank, extents);
+    u.ell = (int)ell;
+    u.rows = BH * u.N;
+    if (u.rows > 0 && ell > (int64_t(1) << 62) / u.rows) return false;
+    for (int a = 0; a < 3; ++a) {
+        u.fd_L[a].init(u.L[a]);
+        u.fd_d[a].init(u.d[a]);
+        u.fd_k[a].init(u.k[a]);
+    }
+    return true;
+}
+
+// Validation, pointer checks and launch of one unfused operator.  need[] marks
+// which of x, y, z (and lse) the operator reads or writes.
+na_status run_unfused(int rank, const int64_t* extents, const int32_t* ks, const int32_t* ds,
+                      const int32_t* causal, int64_t batch, int64_t heads, int64_t head_dim,
+                      na_dtype dtype, float scale, int op, const void* x, const void* y, void* z,
+                      float* lse, na_stream_t stream) {
+    na_status st = check_problem(rank, extents, ks, ds, batch, heads, head_dim, dtype, scale);
+    if (st != NA_OK) return st;
+    if (empty_problem(rank, extents, batch, heads)) return NA_OK;
+    const bool use_x = op != na::kUnfusedSoftmax;
+    const bool use_y = op == na::kUnfusedPN || op == na::kUnfusedNN || op == na::kUnfusedIN;
+    const bool use_lse = op == na::kUnfusedSoftmax;
+    if ((use_x && !x) || (use_y && !y) || !z || (use_lse && !lse)) return NA_ERR_NULL;
+    if ((use_x && !aligned16(x)) || (use_y && !aligned16(y)) || !aligned16(z) ||
+        (use_lse && !aligned16(lse)))
+        return NA_ERR_ALIGNMENT;
+    na::UGeo u;
+    if (!ugeo_from_problem(rank, extents, ks, ds, causal, batch * heads, u)) return NA_ERR_SHAPE;
+    hipError_t e = na::launch_unfused(u, (int)head_dim, (int)dtype, op, x, y, z, lse, scale,
+                                      reinterpret_cast<hipStream_t>(stream));
+    return e == hipSuccess ? NA_OK : NA_ERR_HIP;
+}
+
 }  // namespace
 
 extern "C" {
@@ -802,6 +859,47 @@ na_status na_tune(int rank, const int64_t* extents, const int32_t* kernel_size,
 void na_tune_clear(void) {
     std::lock_guard<std::mutex> lock(g_cache_mu);
     tiling_cache().clear();
+}
+
+na_status na_unfused_pn(int rank, const int64_t* extents, const int32_t* kernel_size,
+                        const int32_t* dilation, const int32_t* causal, int64_t batch,
+                        int64_t heads, int64_t head_dim, na_dtype dtype, float scale,
+                        const void* a, const void* b, void* weights, na_stream_t stream) {
+    return run_unfused(rank, extents, kernel_size, dilation, causal, batch, heads, head_dim, dtype,
+                       scale, na::kUnfusedPN, a, b, weights, nullptr, stream);
+}
+
+na_status na_unfused_softmax(int rank, const int64_t* extents, const int32_t* kernel_size,
+                             const int32_t* dilation, const int32_t* causal, int64_t batch,
+                             int64_t heads, int64_t head_dim, na_dtype dtype, void* weights,
+                             float* logsumexp, na_stream_t stream) {
+    return run_unfused(rank, extents, kernel_size, dilation, causal, batch, heads, head_dim, dtype,
+                       1.0f, na::kUnfusedSoftmax, nullptr, nullptr, weights, logsumexp, stream);
+}
+
+na_status na_unfused_nn(int rank, const int64_t* extents, const int32_t* kernel_size,
+                        const int32_t* dilation, const int32_t* causal, int64_t batch,
+                        int64_t heads, int64_t head_dim, na_dtype dtype, float scale,
+                        const void* weights, const void* b, void* out, na_stream_t stream) {
+    return run_unfused(rank, extents, kernel_size, dilation, causal, batch, heads, head_dim, dtype,
+                       scale, na::kUnfusedNN, weights, b, out, nullptr, stream);
+}
+
+na_status na_unfused_in(int rank, const int64_t* extents, const int32_t* kernel_size,
+                        const int32_t* dilation, const int32_t* causal, int64_t batch,
+                        int64_t heads, int64_t head_dim, na_dtype dtype, float scale,
+                        const void* weights, const void* b, void* out, na_stream_t stream) {
+    return run_unfused(rank, extents, kernel_size, dilation, causal, batch, heads, head_dim, dtype,
+                       scale, na::kUnfusedIN, weights, b, out, nullptr, stream);
+}
+
+na_status na_unfused_softmax_backward(int rank, const int64_t* extents,
+                                      const int32_t* kernel_size, const int32_t* dilation,
+                                      const int32_t* causal, int64_t batch, int64_t heads,
+                                      int64_t head_dim, na_dtype dtype, const void* probs,
+                                      void* grad, na_stream_t stream) {
+    return run_unfused(rank, extents, kernel_size, dilation, causal, batch, heads, head_dim, dtype,
+                       1.0f, na::kUnfusedSoftmaxBwd, probs, nullptr, grad, nullptr, stream);
 }
 
 void na_set_autotune(int mode) { g_autotune.store(mode == 1 || mode == 2 ? mode : 0); }

@@ -423,7 +423,8 @@ def test_autograd_function_matches_explicit_calls(na):
 
 # ---------------------------------------------------------------- full-size workloads
 # Every workload at full size, in the launch configuration bench.py times, compared element by
-# element against the oracle on the whole tensors (O, LSE, dQ, dK, dV).
+# element against the oracle on the whole tensors (O, LSE, dQ, dK, dV); the unfused baseline
+# (na_unfused_*) is compared against the same oracle results.
 @pytest.mark.parametrize("name", workloads.CONFIG_ORDER)
 def test_full_workload_forward(na, name):
     p = workloads.CONFIGS[name]
@@ -433,12 +434,18 @@ def test_full_workload_forward(na, name):
     out, lse = na.forward(*_dev(x["q"], x["k"], x["v"]), p.kernel_size, p.dilation,
                           p.softmax_scale, causal=cz)
     torch.cuda.synchronize()
+    # the unfused baseline (separate PN, softmax and NN launches) on the same inputs
+    uo, ul, _ = na.unfused_forward(*_dev(x["q"], x["k"], x["v"]), p.kernel_size, p.dilation,
+                                   p.softmax_scale, causal=cz)
+    torch.cuda.synchronize()
     qd, kd, vd = (_f64(x[n]) for n in ("q", "k", "v"))
     ro, rl = oracle.forward(qd, kd, vd, p.kernel_size, p.dilation, p.softmax_scale, causal=cz)
     eo, el = _maxerr(out, ro), _maxerr(lse, rl)
+    uo_e, ul_e = _maxerr(uo, ro), _maxerr(ul, rl)
     _log(f"[full fwd] {name}: {ro.size} outputs, {rl.size} logsumexps: max|dO|={eo:.3g} "
-         f"max|dLSE|={el:.3g}")
+         f"max|dLSE|={el:.3g}; unfused max|dO|={uo_e:.3g} max|dLSE|={ul_e:.3g}")
     assert eo <= TOL[p.dtype] and el <= TOL[p.dtype]
+    assert uo_e <= TOL[p.dtype] and ul_e <= TOL[p.dtype]
 
 
 @pytest.mark.parametrize("name", workloads.CONFIG_ORDER)
@@ -452,14 +459,21 @@ def test_full_workload_backward(na, name):
     out, lse = na.forward(q, k, v, p.kernel_size, p.dilation, p.softmax_scale, causal=cz)
     dq, dk, dv = na.backward(q, k, v, out, lse, g, p.kernel_size, p.dilation, p.softmax_scale,
                              causal=cz)
+    # the unfused baseline: PN, softmax backward, NN and two IN launches
+    _, _, probs = na.unfused_forward(q, k, v, p.kernel_size, p.dilation, p.softmax_scale,
+                                     causal=cz)
+    ug = na.unfused_backward(q, k, v, probs, g, p.kernel_size, p.dilation, p.softmax_scale,
+                             causal=cz)
     torch.cuda.synchronize()
-    del q, k, v, g, out, lse
+    del q, k, v, g, out, lse, probs
     refs = oracle.backward(*(_f64(x[n]) for n in ("q", "k", "v", "dout")), p.kernel_size,
                            p.dilation, p.softmax_scale, causal=cz)
     e = [_maxerr(a, r) for a, r in zip((dq, dk, dv), refs)]
+    ue = [_maxerr(a, r) for a, r in zip(ug, refs)]
     _log(f"[full bwd] {name}: 3 x {refs[0].size} gradients: max err dq/dk/dv = "
-         f"{[f'{x:.3g}' for x in e]}")
+         f"{[f'{x:.3g}' for x in e]}; unfused {[f'{x:.3g}' for x in ue]}")
     assert max(e) <= TOL[p.dtype]
+    assert max(ue) <= TOL[p.dtype]
 
 
 # ---------------------------------------------------------------- causal axes
