@@ -18,6 +18,7 @@
 // The roles are independent, so they share the GPU instead of running as
 // consecutive launches.
 #include <algorithm>
+#include <cstdlib>
 #include <type_traits>
 
 #include "na_launch.h"
@@ -347,16 +348,18 @@ __device__ __forceinline__ void dq_role(const Geo& g, int braw, unsigned char* s
 // ---------------------------------------------------------------------------
 // dK, dV: key-major, over the union of the key tile's inverse neighbourhoods.
 // ---------------------------------------------------------------------------
-template <int R, int D, typename T, int KM, int SB>
+// DIN: -Delta of every query comes from memory (written by a pre-pass), so
+// neither O rows nor a Delta pass are needed.
+template <int R, int D, typename T, int KM, int SB, bool DIN = false>
 struct DkvCfg {
     static constexpr int kThreads = 4 * kWave;
     static constexpr int kRows = SB * 16;  // queries per stage
     static constexpr int kTileBytes = kRows * Rows<T, D>::kRowBytes;
-    // One staged query per thread (the whole box in one stage): each thread
-    // forms Delta of its query from its O row in registers, and no O tile is
-    // staged.  Otherwise O rows are staged beside Q and dO.
-    static constexpr bool kRegDelta = kRows == kThreads;
-    static constexpr int kTiles = kRegDelta ? 2 : 3;
+    // Without DIN, one staged query per thread (the whole box in one stage):
+    // each thread forms Delta of its query from its O row in registers, and
+    // no O tile is staged.  Otherwise O rows are staged beside Q and dO.
+    static constexpr bool kRegDelta = !DIN && kRows == kThreads;
+    static constexpr int kTiles = (DIN || kRegDelta) ? 2 : 3;
     // Q rows, dO rows, [O rows,] then fp32 -lse2 and -Delta per query
     static constexpr size_t kFloatOff = (size_t)kTiles * kTileBytes;
     static constexpr size_t kBufBytes = kFloatOff + 2 * kRows * sizeof(float);
@@ -368,14 +371,16 @@ struct DkvCfg {
 // SHORT = 1: every query-box row holds at most two 16-query blocks (rank >= 2).
 // braw: the workgroup's index among the nwk dK/dV-role workgroups (nwk is
 // g.nwg rounded up to a multiple of the 8 XCDs; the surplus ones exit).
-template <int R, int D, typename T, int KM, int SB, int SHORT>
+// DIN: ndg holds -Delta of every query ([B * H * N] fp32, from the pre-pass).
+template <int R, int D, typename T, int KM, int SB, int SHORT, bool DIN>
 __device__ __forceinline__ void dkdv_role(const Geo& g, int braw, int nwk,
                                           unsigned char* smem_raw, const T* __restrict__ qg,
                                           const T* __restrict__ kg, const T* __restrict__ vg,
                                           const T* __restrict__ og, const T* __restrict__ dog,
-                                          const float* __restrict__ lseg, T* __restrict__ dkg,
+                                          const float* __restrict__ lseg,
+                                          const float* __restrict__ ndg, T* __restrict__ dkg,
                                           T* __restrict__ dvg, float scale_log2, float scale) {
-    using C = DkvCfg<R, D, T, KM, SB>;
+    using C = DkvCfg<R, D, T, KM, SB, DIN>;
     using x8 = typename Tr<T>::x8;
 
     const int tid = threadIdx.x;
@@ -407,6 +412,7 @@ __device__ __forceinline__ void dkdv_role(const Geo& g, int braw, int nwk,
     const T* gb = dog + slice;
     const T* ob = og + slice;
     const float* lb = lseg + (size_t)bh * g.N;
+    const float* nb_ = DIN ? ndg + (size_t)bh * g.N : nullptr;
 
     // this wave's key sub-box: the queries that attend to any / all of its keys
     int wc[kMaxRank], wo[kMaxRank];
@@ -492,14 +498,14 @@ __device__ __forceinline__ void dkdv_role(const Geo& g, int braw, int nwk,
     const int tstep = g.d[R - 1];
     typename C::Ld ld;
     using L = Rows<T, D>;
-    float lse_reg = 0.f;
+    float lse_reg = 0.f, ndl_reg = 0.f;
     i32x4 orow[L::kSegs];  // kRegDelta: this thread's O row
     auto issue_stage = [&](int s, int buf) {
         ld.compute(ibox, g, gc, s * SB, tstep, wave, lane);
         unsigned char* tile = smem_raw + buf * C::kBufBytes;
         ld.issue(qb, tile, wave);
         ld.issue(gb, tile + C::kTileBytes, wave);
-        if constexpr (!C::kRegDelta) ld.issue(ob, tile + 2 * C::kTileBytes, wave);
+        if constexpr (!DIN && !C::kRegDelta) ld.issue(ob, tile + 2 * C::kTileBytes, wave);
         if (tid < C::kRows) {
             int valid;
             const int tok0 = ibox.block_token(g, gc, s * SB + (tid >> 4), valid);
@@ -507,6 +513,7 @@ __device__ __forceinline__ void dkdv_role(const Geo& g, int braw, int nwk,
             const int tk = ok ? tok0 + (tid & 15) * tstep : 0;  // token 0: safe stand-in
             const float lv = lb[tk];
             lse_reg = ok ? -lv * kLog2e : 0.f;  // staged negated: -lse2
+            if constexpr (DIN) ndl_reg = ok ? nb_[tk] : 0.f;  // already -Delta
             if constexpr (C::kRegDelta) {
 #pragma unroll
                 for (int sg = 0; sg < L::kSegs; ++sg)
@@ -532,7 +539,9 @@ __device__ __forceinline__ void dkdv_role(const Geo& g, int braw, int nwk,
     // and -Delta per staged query
     auto delta_pass = [&](int buf) {
         const unsigned char* gt = smem_raw + buf * C::kBufBytes + C::kTileBytes;
-        if constexpr (C::kRegDelta) {
+        if constexpr (DIN) {
+            (void)gt;
+        } else if constexpr (C::kRegDelta) {
             float acc = 0.f;
 #pragma unroll
             for (int sg = 0; sg < L::kSegs; ++sg) acc = dot16(lds16(gt + L::off(tid, sg)), orow[sg], acc);
@@ -572,8 +581,15 @@ __device__ __forceinline__ void dkdv_role(const Geo& g, int braw, int nwk,
         }
 
     const int nst = (ibox.nb + SB - 1) / SB;
+    // the per-query floats of a stage: -lse2, and -Delta when it comes from memory
+    auto put_floats = [&](int buf) {
+        if (tid < C::kRows) {
+            floats(buf)[tid] = lse_reg;
+            if constexpr (DIN) floats(buf)[C::kRows + tid] = ndl_reg;
+        }
+    };
     issue_stage(0, 0);
-    if (tid < C::kRows) floats(0)[tid] = lse_reg;
+    put_floats(0);
     wait_vmem();
     __syncthreads();
     delta_pass(0);
@@ -751,11 +767,11 @@ __device__ __forceinline__ void dkdv_role(const Geo& g, int braw, int nwk,
         }
 
         if (s + 1 < nst) {
-            if (tid < C::kRows) floats((s + 1) & 1)[tid] = lse_reg;
+            put_floats((s + 1) & 1);
             wait_vmem();
         }
         __syncthreads();
-        if (s + 1 < nst) {
+        if (!DIN && s + 1 < nst) {
             delta_pass((s + 1) & 1);
             __syncthreads();
         }
@@ -781,29 +797,42 @@ __device__ __forceinline__ void dkdv_role(const Geo& g, int braw, int nwk,
 // spilled outside the tile loop (the dQ role's per-stage state), and the
 // third wave hides more of the tile loop's latency (1-D k = 1023 backward:
 // -7 %).  Ranks 2 and 3 would spill inside the loop.
-template <int R, int D, typename T>
+// ROLE 0 runs both roles in one grid; ROLE 1 only the dK/dV role (nwk
+// workgroups) and ROLE 2 only the dQ role (g.nwg workgroups), each as a
+// launch of its own with its own register budget.
+template <int R, int D, typename T, int QM, int ROLE>
 constexpr int bwd_min_waves() {
+    if constexpr (ROLE == 2) return sizeof(T) == 2 && D <= 64 ? (QM == 1 ? 5 : 3) : 2;
     return sizeof(T) == 2 && D <= 64 ? (R == 1 ? 3 : 2) : 1;
 }
 
-template <int R, int D, typename T, int QM, int KM, int SBQ, int SBK, int SHORT>
-__global__ __launch_bounds__(256, (bwd_min_waves<R, D, T>())) void na_bwd_kernel(Geo g, int nwk, const T* __restrict__ q,
+template <int R, int D, typename T, int QM, int KM, int SBQ, int SBK, int SHORT, int ROLE>
+__global__ __launch_bounds__(256, (bwd_min_waves<R, D, T, QM, ROLE>())) void na_bwd_kernel(Geo g, int nwk, const T* __restrict__ q,
                                                      const T* __restrict__ k,
                                                      const T* __restrict__ v,
                                                      const T* __restrict__ o,
                                                      const T* __restrict__ dout,
                                                      const float* __restrict__ lse,
+                                                     const float* __restrict__ ndelta,
                                                      T* __restrict__ dq, T* __restrict__ dk,
                                                      T* __restrict__ dv, float scale_log2,
                                                      float scale) {
     extern __shared__ __align__(16) unsigned char smem_raw[];
     const int b = blockIdx.x;
-    if (b < nwk)
-        dkdv_role<R, D, T, KM, SBK, SHORT>(g, b, nwk, smem_raw, q, k, v, o, dout, lse, dk, dv,
-                                           scale_log2, scale);
-    else
-        dq_role<R, D, T, QM, SBQ, SHORT>(g, b - nwk, smem_raw, q, k, v, o, dout, lse, dq,
-                                         scale_log2, scale);
+    if constexpr (ROLE == 1) {
+        dkdv_role<R, D, T, KM, SBK, SHORT, true>(g, b, nwk, smem_raw, q, k, v, o, dout, lse,
+                                                 ndelta, dk, dv, scale_log2, scale);
+    } else if constexpr (ROLE == 2) {
+        dq_role<R, D, T, QM, SBQ, SHORT>(g, b, smem_raw, q, k, v, o, dout, lse, dq, scale_log2,
+                                         scale);
+    } else {
+        if (b < nwk)
+            dkdv_role<R, D, T, KM, SBK, SHORT, false>(g, b, nwk, smem_raw, q, k, v, o, dout, lse,
+                                                      nullptr, dk, dv, scale_log2, scale);
+        else
+            dq_role<R, D, T, QM, SBQ, SHORT>(g, b - nwk, smem_raw, q, k, v, o, dout, lse, dq,
+                                             scale_log2, scale);
+    }
 }
 
 // ---------------------------------------------------------------------------
@@ -847,30 +876,107 @@ static int box_blocks(const int* e, int rank) {
     return nb;
 }
 
+// Delta pre-pass of the split backward: nd[row] = -sum_c dO[row, c] O[row, c]
+// in fp32, the lanes of a 16-byte segment group sharing a row.
+template <typename T, int D>
+__global__ __launch_bounds__(256) void na_delta_kernel(const T* __restrict__ o,
+                                                       const T* __restrict__ dout,
+                                                       float* __restrict__ nd, int64_t rows) {
+    using L = Rows<T, D>;
+    constexpr int kSegs = L::kSegs;  // lanes per row (a power of two dividing 64)
+    const int seg = threadIdx.x % kSegs;
+    const int64_t step = (int64_t)gridDim.x * (256 / kSegs);
+    for (int64_t row = (int64_t)blockIdx.x * (256 / kSegs) + threadIdx.x / kSegs; row < rows;
+         row += step) {
+        const i32x4 a = ld16<i32x4>(o + row * D + seg * L::kVec);
+        const i32x4 b = ld16<i32x4>(dout + row * D + seg * L::kVec);
+        float acc;
+        if constexpr (sizeof(T) == 2) {
+            using x8 = typename Tr<T>::x8;
+            acc = dot8<T>(__builtin_bit_cast(x8, a), __builtin_bit_cast(x8, b), 0.f);
+        } else {
+            const f32x4 x = __builtin_bit_cast(f32x4, a), y = __builtin_bit_cast(f32x4, b);
+            acc = fmaf(x[3], y[3], fmaf(x[2], y[2], fmaf(x[1], y[1], x[0] * y[0])));
+        }
+#pragma unroll
+        for (int w = 1; w < kSegs; w <<= 1) acc += __shfl_xor(acc, w, kWave);
+        if (seg == 0) nd[row] = -acc;
+    }
+}
+
 // hq / hk: most blocks in any dQ halo / dK-dV query box; a role whose boxes
 // all fit in one stage gets a single LDS buffer.
+//
+// One launch runs both roles (dK/dV workgroups first).  The split form, for
+// large 16-bit problems at D <= 64, runs three launches instead: a Delta
+// pre-pass writing -Delta of every query into dq (scratch until the last
+// launch overwrites it), the dK/dV role reading it (no O rows, no Delta pass,
+// one barrier per stage, stages of SBS blocks), then the dQ role; each role
+// runs at the occupancy its own register count allows.
 template <int R, int D, typename T, int QM, int KM, int SBQ, int SBK>
-static hipError_t launch_bwd_sb(const Geo& g, bool short_rows, int hq, int hk, const void* q,
-                                const void* k, const void* v, const void* o, const float* lse,
-                                const void* dout, void* dq, void* dk, void* dv, float scale,
-                                hipStream_t stream) {
-    auto kern = na_bwd_kernel<R, D, T, QM, KM, SBQ, SBK, 0>;
-    if constexpr (R > 1)  // (1-D boxes have one row: never short)
-        if (short_rows) kern = na_bwd_kernel<R, D, T, QM, KM, SBQ, SBK, 1>;
-    const size_t lds = std::max((hq > SBQ ? 2 : 1) * DqCfg<R, D, T, QM, SBQ>::kBufBytes,
-                                (hk > SBK ? 2 : 1) * DkvCfg<R, D, T, KM, SBK>::kBufBytes);
-    if (lds > 65536) {
-        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
-                                           hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-        if (e != hipSuccess) return e;
-    }
+static hipError_t launch_bwd_sb(const Geo& g, bool short_rows, bool split, int hq, int hk,
+                                const void* q, const void* k, const void* v, const void* o,
+                                const float* lse, const void* dout, void* dq, void* dk, void* dv,
+                                float scale, hipStream_t stream) {
+    const size_t lds_q = (hq > SBQ ? 2 : 1) * DqCfg<R, D, T, QM, SBQ>::kBufBytes;
+    const size_t lds_k = (hk > SBK ? 2 : 1) * DkvCfg<R, D, T, KM, SBK>::kBufBytes;
     const int nwk = (g.nwg + 7) & ~7;
-    hipLaunchKernelGGL(kern, dim3((unsigned)(nwk + g.nwg)), dim3(4 * kWave), lds, stream, g, nwk,
-                       static_cast<const T*>(q), static_cast<const T*>(k),
-                       static_cast<const T*>(v), static_cast<const T*>(o),
-                       static_cast<const T*>(dout), lse, static_cast<T*>(dq), static_cast<T*>(dk),
-                       static_cast<T*>(dv), scale * kLog2e, scale);
-    return hipGetLastError();
+    auto launch = [&](auto kern, size_t lds, int grid, const float* nd) -> hipError_t {
+        if (lds > 65536) {
+            hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                                               hipFuncAttributeMaxDynamicSharedMemorySize,
+                                               (int)lds);
+            if (e != hipSuccess) return e;
+        }
+        hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(4 * kWave), lds, stream, g, nwk,
+                           static_cast<const T*>(q), static_cast<const T*>(k),
+                           static_cast<const T*>(v), static_cast<const T*>(o),
+                           static_cast<const T*>(dout), lse, nd, static_cast<T*>(dq),
+                           static_cast<T*>(dk), static_cast<T*>(dv), scale * kLog2e, scale);
+        return hipGetLastError();
+    };
+    if constexpr (sizeof(T) == 2 && D <= 64) {
+        if (split) {
+            constexpr int SBS = D == 32 ? 16 : 8;
+            const size_t lds_ks = (hk > SBS ? 2 : 1) * DkvCfg<R, D, T, KM, SBS, true>::kBufBytes;
+            auto kk = na_bwd_kernel<R, D, T, QM, KM, SBQ, SBS, 0, 1>;
+            auto kq = na_bwd_kernel<R, D, T, QM, KM, SBQ, SBK, 0, 2>;
+            if constexpr (R > 1)
+                if (short_rows) {
+                    kk = na_bwd_kernel<R, D, T, QM, KM, SBQ, SBS, 1, 1>;
+                    kq = na_bwd_kernel<R, D, T, QM, KM, SBQ, SBK, 1, 2>;
+                }
+            float* nd = static_cast<float*>(dq);
+            const int64_t rows = (int64_t)g.BH * g.N;
+            constexpr int kRowsPerBlock = 256 / Rows<T, D>::kSegs;
+            const int64_t blocks = std::min<int64_t>((rows + kRowsPerBlock - 1) / kRowsPerBlock,
+                                                     int64_t(1) << 18);
+            hipLaunchKernelGGL((na_delta_kernel<T, D>), dim3((unsigned)blocks), dim3(256), 0,
+                               stream, static_cast<const T*>(o), static_cast<const T*>(dout), nd,
+                               rows);
+            hipError_t e = hipGetLastError();
+            if (e != hipSuccess) return e;
+            e = launch(kk, lds_ks, nwk, nd);
+            if (e != hipSuccess) return e;
+            return launch(kq, lds_q, g.nwg, nullptr);
+        }
+    }
+    (void)split;
+    auto kern = na_bwd_kernel<R, D, T, QM, KM, SBQ, SBK, 0, 0>;
+    if constexpr (R > 1)  // (1-D boxes have one row: never short)
+        if (short_rows) kern = na_bwd_kernel<R, D, T, QM, KM, SBQ, SBK, 1, 0>;
+    return launch(kern, std::max(lds_q, lds_k), nwk + g.nwg, nullptr);
+}
+
+// Whether a backward runs as the split form: large 3-D problems with two
+// blocks per wave, whose dK/dV role otherwise holds the dQ role to its own
+// occupancy.  NA_BWD_SPLIT=0|1 forces the choice.
+static bool use_split(const Geo& g, int rank, int qm) {
+    if (const char* env = std::getenv("NA_BWD_SPLIT")) {
+        if (env[0] == '0') return false;
+        if (env[0] == '1') return true;
+    }
+    return rank == 3 && qm == 2;
 }
 
 template <int R, int D, typename T, int QM, int KM>
@@ -885,16 +991,17 @@ static hipError_t launch_bwd_inst(const Geo& g, const void* q, const void* k, co
     const int hq = box_blocks(eq, R), hk = box_blocks(ek, R);
     // rows of every halo (dQ) and query box (dK/dV) hold at most 2 blocks
     const bool short_rows = R > 1 && (eq[R - 1] + 15) / 16 <= 2 && (ek[R - 1] + 15) / 16 <= 2;
+    const bool split = use_split(g, R, QM);
     // D = 32, 16-bit: boxes of up to 16 blocks are staged whole (one stage)
     if constexpr (sizeof(T) == 2 && D == 32) {
         if (hq <= 16 && hk <= 16)
-            return launch_bwd_sb<R, D, T, QM, KM, 16, 16>(g, short_rows, hq, hk, q, k, v, o, lse,
-                                                          dout, dq, dk, dv, scale, stream);
+            return launch_bwd_sb<R, D, T, QM, KM, 16, 16>(g, short_rows, split, hq, hk, q, k, v,
+                                                          o, lse, dout, dq, dk, dv, scale, stream);
     }
     constexpr int SBQ = sizeof(T) == 4 ? 2 : 4;
     constexpr int SBK = (sizeof(T) == 4 || D == 128) ? 2 : 4;
-    return launch_bwd_sb<R, D, T, QM, KM, SBQ, SBK>(g, short_rows, hq, hk, q, k, v, o, lse, dout,
-                                                    dq, dk, dv, scale, stream);
+    return launch_bwd_sb<R, D, T, QM, KM, SBQ, SBK>(g, short_rows, split, hq, hk, q, k, v, o, lse,
+                                                    dout, dq, dk, dv, scale, stream);
 }
 
 template <int R, int D, typename T>

@@ -398,6 +398,44 @@ def test_backward_small(na, ext, ks, ds, D, dtype, B, H):
     assert max(e) <= TOL[dtype]
 
 
+# The backward runs as one launch of both roles, or split into a Delta pre-pass, a dK/dV launch
+# and a dQ launch (large 3-D problems with two blocks per wave by default); the environment
+# forces each form on problems the other would take.
+SPLIT_CASES = [
+    # (extents, kernel, dilation, causal, head_dim, dtype, blocks per wave, split)
+    ((300,), (13,), (3,), None, 64, "fp16", 2, 1),
+    ((257,), (64,), (4,), (True,), 64, "bf16", 1, 1),
+    ((37, 45), (7, 5), (2, 1), None, 32, "fp16", 2, 1),
+    ((33, 31), (13, 13), (2, 2), (True, False), 64, "bf16", 1, 1),
+    ((5, 40), (3, 17), (1, 1), None, 32, "fp16", 1, 1),
+    ((6, 20, 22), (3, 7, 5), (1, 2, 2), None, 64, "fp16", 2, 1),
+    ((8, 12, 12), (7, 7, 7), (1, 1, 1), (True, False, False), 32, "bf16", 2, 1),
+    ((3, 4, 64), (3, 3, 25), (1, 1, 1), None, 64, "fp16", 1, 1),
+    ((6, 20, 22), (3, 7, 5), (1, 2, 2), None, 64, "fp16", 2, 0),
+    ((8, 12, 12), (7, 7, 7), (1, 1, 1), (True, False, False), 32, "bf16", 2, 0),
+]
+
+
+@pytest.mark.parametrize("ext,ks,ds,cs,D,dtype,m,split", SPLIT_CASES)
+def test_backward_split_and_single_launch(na, monkeypatch, ext, ks, ds, cs, D, dtype, m, split):
+    monkeypatch.setenv("NA_WAVE_BLOCKS", str(m))
+    monkeypatch.setenv("NA_BWD_SPLIT", str(split))
+    shape = (1, 2) + ext + (D,)
+    q, k, v, g = _inputs(shape, dtype, 24, 4)
+    qd, kd, vd, gd = _dev(q, k, v, g)
+    sc = 1.0 / math.sqrt(D)
+    out, lse = na.forward(qd, kd, vd, ks, ds, causal=cs)
+    dq, dk, dv = na.backward(qd, kd, vd, out, lse, gd, ks, ds, causal=cs)
+    rq, rk, rv = oracle.backward(_f64(q), _f64(k), _f64(v), _f64(g), ks, ds, sc, causal=cs)
+    e = [_maxerr(dq, rq), _maxerr(dk, rk), _maxerr(dv, rv)]
+    _log(f"bwd {'split' if split else 'single launch'} {ext} k={ks} d={ds} c={cs} D={D} {dtype} "
+         f"m={m}: max err dq/dk/dv = {[f'{x:.3g}' for x in e]}")
+    assert max(e) <= TOL[dtype]
+    again = na.backward(qd, kd, vd, out, lse, gd, ks, ds, causal=cs)
+    for a, b in zip((dq, dk, dv), again):
+        assert torch.equal(a, b)
+
+
 def test_backward_deterministic(na):
     shape = (1, 2, 30, 27, 64)
     q, k, v, g = _dev(*_inputs(shape, "bf16", 22, 4))
