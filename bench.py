@@ -15,6 +15,14 @@ with events (which adds the event overhead of one launch).  So are the K
 forwards and K backwards replayed from HIP graphs (fwd_ms_graph,
 bwd_ms_graph), as a serving loop that captures its launches would run them.
 
+Beside the headline it reports, for every workload (bounded, about a minute in
+all): the fused forward and backward against the unfused baseline of separate
+PN / softmax / NN / IN launches that store the attention weights (the
+paper's own comparison, with its A100 ratios as context), and the fp64 CPU
+oracle's time per workload (median of 3).  Two measured ceilings stand beside
+the spec peaks: a device-to-device copy's bandwidth and a large fp16 GEMM's
+rate.
+
 Prints one JSON line.  --gpus above 1 is refused: the benchmark runs on one GPU.
 """
 import argparse
@@ -117,6 +125,146 @@ def cpu_baseline(problem, x, budget_s, single_thread_s):
     return out
 
 
+def oracle_per_config(max_run_s=5.0):
+    """The fp64 oracle on every workload's full tensors: forward (and backward for the
+    fwd+bwd workloads), median of 3 runs (one run when a run takes longer than max_run_s)."""
+    import oracle
+
+    rows = []
+    for name in workloads.CONFIG_ORDER:
+        p = workloads.CONFIGS[name]
+        x = workloads.make_inputs(p, seed=0, with_grad=p.backward)
+        f = {n: t.double().numpy() for n, t in x.items()}
+        args = (p.kernel_size, p.dilation, p.softmax_scale)
+        cz = p.causal_axes
+
+        def med3(fn):
+            ts = []
+            for _ in range(3):
+                t0 = time.perf_counter()
+                fn()
+                ts.append(time.perf_counter() - t0)
+                if ts[-1] > max_run_s:
+                    break
+            ts.sort()
+            return ts[len(ts) // 2] * 1e3, len(ts)
+
+        fwd_ms, nf = med3(lambda: oracle.forward(f["q"], f["k"], f["v"], *args, causal=cz))
+        row = {"workload": name, "fwd_ms": round(fwd_ms, 2), "fwd_runs": nf,
+               "fwd_tflops": round(p.fwd_flops() / (fwd_ms * 1e-3) / 1e12, 4)}
+        if p.backward:
+            bwd_ms, nb = med3(lambda: oracle.backward(f["q"], f["k"], f["v"], f["dout"], *args,
+                                                      causal=cz))
+            row.update({"bwd_ms": round(bwd_ms, 2), "bwd_runs": nb})
+        rows.append(row)
+    return rows
+
+
+# The paper's fused-over-naive speedups on an A100 (FP16, averages over its
+# problem sweep; Tables "runtime_breakdown" and "runtime_breakdown_backward"),
+# as the ratio t_naive / t_fused: context for the MI355X ratios, not a target.
+PAPER_A100_FUSED_OVER_NAIVE = {
+    1: {"fwd": 18.59, "fwd_bwd": 9.44},
+    2: {"fwd": 10.58, "fwd_bwd": 4.85},
+    3: {"fwd": 12.35, "fwd_bwd": 5.47},
+}
+
+
+def fused_vs_unfused(na, dev, spc, K=20, reps=3):
+    """Fused forward/backward against the unfused baseline (separate PN, softmax, NN and IN
+    launches storing the attention weights) on every workload: ms per call, median of reps
+    regions of K back-to-back calls."""
+    rows = []
+    for name in workloads.CONFIG_ORDER:
+        p = workloads.CONFIGS[name]
+        x = workloads.make_inputs(p, seed=0, with_grad=True)
+        q, k, v, g = (x[n].to(dev) for n in ("q", "k", "v", "dout"))
+        del x
+        args = (p.kernel_size, p.dilation, p.softmax_scale)
+        cz = p.causal_axes if any(p.causal_axes) else None
+        out, lse = torch.empty_like(q), torch.empty(q.shape[:-1], dtype=torch.float32, device=dev)
+        dq, dk, dv = torch.empty_like(q), torch.empty_like(q), torch.empty_like(q)
+        w = torch.empty(tuple(q.shape[:-1]) + (p.window,), dtype=q.dtype, device=dev)
+        gw = torch.empty_like(w)
+        probs = {}
+
+        def f_fwd():
+            na.forward(q, k, v, *args, out=out, lse=lse, causal=cz)
+
+        def f_bwd():
+            na.backward(q, k, v, out, lse, g, *args, dq=dq, dk=dk, dv=dv, causal=cz)
+
+        def u_fwd():
+            o_, l_, probs["p"] = na.unfused_forward(q, k, v, *args, causal=cz, weights=w)
+
+        def u_bwd():
+            na.unfused_backward(q, k, v, probs["p"], g, *args, causal=cz, grad_weights=gw)
+
+        def timed(fn):
+            fn()
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            fn()
+            torch.cuda.synchronize()
+            one = time.perf_counter() - t0
+            ts = []
+            for _ in range(reps):
+                torch.cuda._sleep(int(min(K * max(one, 50e-6) + 1e-3, 2.0) / spc))
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                e0.record()
+                for _ in range(K):
+                    fn()
+                e1.record()
+                torch.cuda.synchronize()
+                ts.append(e0.elapsed_time(e1) / K)
+            return sorted(ts)[len(ts) // 2]
+
+        ff, uf = timed(f_fwd), timed(u_fwd)
+        f_fwd()
+        fb, ub = timed(f_bwd), timed(u_bwd)
+        ctx = PAPER_A100_FUSED_OVER_NAIVE[p.rank]
+        rows.append({
+            "workload": name,
+            "fused_fwd_ms": round(ff, 5), "unfused_fwd_ms": round(uf, 5),
+            "fused_bwd_ms": round(fb, 5), "unfused_bwd_ms": round(ub, 5),
+            "fwd_speedup": round(uf / ff, 2), "fwd_bwd_speedup": round((uf + ub) / (ff + fb), 2),
+            "paper_a100_fp16_avg_speedup": ctx,
+            "weights_bytes": w.numel() * w.element_size(),
+        })
+        del q, k, v, g, out, lse, dq, dk, dv, w, gw, probs
+        torch.cuda.empty_cache()
+    return rows
+
+
+def measured_ceilings(dev):
+    """Measured beside the spec peaks: a 1 GiB device copy (bytes read + written per
+    second) and a 8192^3 fp16 GEMM (torch.matmul, the vendor library), each the best of 5."""
+    n = 1 << 30
+    src = torch.ones(n, dtype=torch.uint8, device=dev)
+    dst = torch.empty_like(src)
+    a = torch.randn(8192, 8192, device=dev, dtype=torch.float16)
+    b = torch.randn(8192, 8192, device=dev, dtype=torch.float16)
+    copy_ms, gemm_ms = [], []
+    for _ in range(5):
+        dst.copy_(src)
+        torch.matmul(a, b)
+    torch.cuda.synchronize()
+    for _ in range(5):
+        e0, e1, e2 = (torch.cuda.Event(enable_timing=True) for _ in range(3))
+        e0.record()
+        dst.copy_(src)
+        e1.record()
+        torch.matmul(a, b)
+        e2.record()
+        torch.cuda.synchronize()
+        copy_ms.append(e0.elapsed_time(e1))
+        gemm_ms.append(e1.elapsed_time(e2))
+    del src, dst, a, b
+    torch.cuda.empty_cache()
+    return {"copy_gbs": round(2 * n / (min(copy_ms) * 1e-3) / 1e9, 1),
+            "fp16_gemm_tflops": round(2 * 8192 ** 3 / (min(gemm_ms) * 1e-3) / 1e12, 1)}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -136,6 +284,9 @@ def main():
                          "line is defined on the default one)")
     ap.add_argument("--no-graphs", dest="graphs", action="store_false",
                     help="skip the HIP-graph replay side measurement")
+    ap.add_argument("--no-compare", dest="compare", action="store_false",
+                    help="skip the per-workload fused-versus-unfused comparison, the measured "
+                         "ceilings and the per-workload oracle timing")
     ap.add_argument("--tune", action="store_true",
                     help="run the library's tiling tuner (na_tune) on the workload before the "
                          "timed regions, so they use the tuned tilings")
@@ -348,11 +499,22 @@ def main():
             "algorithmic_bytes_per_launch": fwd_bytes,
         },
     }
+    if args.compare:
+        ceil = measured_ceilings(dev)
+        result["measured_ceilings"] = ceil
+        result["roofline"]["frac_of_measured_copy"] = round(achieved_gbs / ceil["copy_gbs"], 4)
+        result["fused_vs_unfused"] = fused_vs_unfused(na, dev, spin_s_per_cycle)
     if not args.no_cpu_baseline:
         if p.name == workloads.BENCH_WORKLOAD:
             result["mfma_bound"] = mfma_bound_forward(na, dev, head_start, host_step_s)
+            if args.compare:
+                mb = result["mfma_bound"]
+                mb["frac_of_measured_gemm"] = round(mb["tflops"] / ceil["fp16_gemm_tflops"], 4)
         result["cpu_baseline"] = cpu_baseline(p, x, args.cpu_seconds,
                                               args.cpu_single_thread_seconds)
+        if args.compare:
+            result["cpu_baseline"]["per_config"] = oracle_per_config()
+            result["cpu_baseline"]["nproc"] = os.cpu_count()
     print(json.dumps(result), flush=True)
 
 

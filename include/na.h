@@ -142,7 +142,9 @@ na_status na_forward(int rank, const int64_t* extents, const int32_t* kernel_siz
  * dQ = scale * NN(dA, K) over each query's neighbourhood, and dK = scale *
  * IN(dA, Q), dV = IN(P, dO) over each key's inverse neighbourhood.
  *   Delta = rowsum(dO * O) is formed inside the kernels, so no workspace is
- *   needed.  dq, dk, dv are fully overwritten and must not alias the inputs.
+ *   needed (for large 3-D problems a first launch writes -Delta into dq,
+ *   which later launches of the same call read and then overwrite).  dq, dk,
+ *   dv are fully overwritten and must not alias the inputs or each other.
  *   Deterministic: the same inputs give bit-identical gradients.
  */
 na_status na_backward(int rank, const int64_t* extents, const int32_t* kernel_size,

@@ -608,18 +608,22 @@ constexpr int kAutotuneRepeats = 3;
 bool ugeo_from_problem(int rank, const int64_t* extents, const int32_t* ks, const int32_t* ds,
                        const int32_t* causal, int64_t BH, na::UGeo& u) {
     std::memset(&u, 0, sizeof(u));
+    // the problem's axes are the last `rank` of the three, so that the
+    // kernels' innermost neighbour loop runs along its innermost axis
+    const int off = 3 - rank;
     int64_t ell = 1;
     for (int a = 0; a < 3; ++a) {
-        u.L[a] = a < rank ? (int)extents[a] : 1;
-        u.k[a] = a < rank ? ks[a] : 1;
-        u.d[a] = a < rank ? ds[a] : 1;
-        u.causal[a] = a < rank && causal && causal[a] ? 1 : 0;
+        const bool real = a >= off;
+        u.L[a] = real ? (int)extents[a - off] : 1;
+        u.k[a] = real ? ks[a - off] : 1;
+        u.d[a] = real ? ds[a - off] : 1;
+        u.causal[a] = real && causal && causal[a - off] ? 1 : 0;
         ell *= u.k[a];
     }
     if (ell >= (int64_t(1) << 31)) return false;
     int s = 1, ks_ = 1;
     for (int a = 2; a >= 0; --a) {
-        u.ts[a] = a < rank ? s : 0;
+        u.ts[a] = a >= off ? s : 0;
         s *= u.L[a];
         u.kst[a] = ks_;
         ks_ *= u.k[a];

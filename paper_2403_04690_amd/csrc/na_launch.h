@@ -18,8 +18,9 @@ hipError_t launch_backward(const Geo& g, int rank, int D, int dtype, int m, cons
                            const void* dout, void* dq, void* dk, void* dv, float scale,
                            hipStream_t s);
 
-// Geometry of the unfused operators (filled on the host; axes beyond the
-// problem's rank are inert: extent, window and dilation 1).
+// Geometry of the unfused operators (filled on the host).  A rank-r problem
+// occupies the last r axes; the leading ones are inert (extent, window and
+// dilation 1, token stride 0).
 struct UGeo {
     int L[kMaxRank], k[kMaxRank], d[kMaxRank], causal[kMaxRank];
     int ts[kMaxRank];   // token stride of each axis (0 for inert axes)

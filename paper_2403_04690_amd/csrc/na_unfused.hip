@@ -232,6 +232,7 @@ __global__ __launch_bounds__(kUThreads) void nn_kernel(UGeo u, const T* __restri
             for (int t1 = 0; t1 < c[1]; ++t1) {
                 const int j1 = j0 + (ax[1].g + u.d[1] * (s[1] + t1)) * u.ts[1];
                 const int e1 = t0 * u.kst[0] + t1 * u.kst[1];
+#pragma unroll 8
                 for (int t2 = 0; t2 < c[2]; ++t2) {
                     const int j = j1 + (ax[2].g + u.d[2] * (s[2] + t2)) * u.ts[2];
                     const float w = to_f(wrow[e1 + t2]);
@@ -277,6 +278,7 @@ __global__ __launch_bounds__(kUThreads) void in_kernel(UGeo u, const T* __restri
                 const int i1 = i0 + (ax[1].g + u.d[1] * p1) * u.ts[1];
                 const int e1 =
                     e0 + (ax[1].p - win_start(p1, ax[1].n, u.k[1], u.causal[1] != 0)) * u.kst[1];
+#pragma unroll 8
                 for (int p2 = lo[2]; p2 <= hi[2]; ++p2) {
                     const int i = i1 + (ax[2].g + u.d[2] * p2) * u.ts[2];
                     const int e =
