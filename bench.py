@@ -292,6 +292,8 @@ def main():
                          "timed regions, so they use the tuned tilings")
     ap.add_argument("--tune-report", action="store_true",
                     help="only run the tuner on the workload and print its choice and timings")
+    ap.add_argument("--tune-thorough", action="store_true",
+                    help="let the tuner time every candidate tiling (not only the first 64)")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="counter calibration: only run 5 device-to-device copies of this many "
                          "MiB (the HBM traffic of each is known) and exit")
@@ -327,13 +329,14 @@ def main():
     if args.tune or args.tune_report:
         na.tune_clear()
         bf, bb, tms = na.tune(q, k, v, g, ks, ds, sc, causal=cz, repeats=10, out=out, lse=lse,
-                              dq=dq, dk=dk, dv=dv)
+                              dq=dq, dk=dk, dv=dv, thorough=args.tune_thorough)
         tuning = {"forward_tiling": list(bf), "backward_tiling": list(bb),
                   "fwd_ms_tuned": round(tms[0], 5), "bwd_ms_tuned": round(tms[1], 5),
                   "fwd_ms_heuristic": round(tms[2], 5), "bwd_ms_heuristic": round(tms[3], 5),
                   "candidates": [len(na.candidate_tilings(p.extents, ks, ds, p.batch, p.heads,
                                                           p.head_dim, q.dtype, forward=f))
-                                 for f in (True, False)]}
+                                 for f in (True, False)],
+                  "thorough": args.tune_thorough}
         if args.tune_report:
             print(json.dumps({"workload": p.name, **tuning}), flush=True)
             return
