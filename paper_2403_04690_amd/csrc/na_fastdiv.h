@@ -8,8 +8,9 @@
 //   mul = floor(2^32 (2^s - d) / d) + 1
 //   n / d = (umulhi(n, mul) + n) >> s
 // (umulhi(n, mul) < 2^31, so the sum stays below 2^32.)  The multiplier is
-// formed on the host in 64-bit integers; on the device, for d < 2^20, with
-// one double division instead (2^32 (2^s - d) < 2^52 is exact in a double,
+// formed on the host in 64-bit integers; on the device it is 1 for a power of
+// two (2^s - d = 0) and otherwise, for d < 2^20, comes from one double
+// division (2^32 (2^s - d) < 2^52 is exact in a double,
 // the division is correctly rounded, and the quotient's fractional part is at
 // least 1/d > 2^-20, far above the rounding error of a quotient below 2^32, so
 // its floor is exact).  Both paths are plain C++ here so that a host build
@@ -25,10 +26,8 @@ namespace na {
 struct FastDiv {
     uint32_t mul, shr;
 
-    static NA_HD uint32_t shift_for(int d) {
-        uint32_t s = 0;
-        while ((1u << s) < (uint32_t)d) ++s;
-        return s;
+    static NA_HD uint32_t shift_for(int d) {  // ceil(log2 d)
+        return d <= 1 ? 0u : 32u - (uint32_t)__builtin_clz((uint32_t)d - 1u);
     }
     // multiplier from 64-bit integers (any 1 <= d < 2^31)
     static NA_HD uint32_t mul_int(int d, uint32_t s) {
@@ -44,6 +43,12 @@ struct FastDiv {
     NA_HD void init(int d) {
         shr = shift_for(d);
 #if defined(__HIP_DEVICE_COMPILE__)
+        // a power of two (2^s - d = 0): the multiplier is 1, so no division at
+        // all -- the common case of the per-workgroup divisors
+        if ((d & (d - 1)) == 0) {
+            mul = 1;
+            return;
+        }
         if (d < (1 << 20)) {
             mul = mul_double(d, shr);
             return;

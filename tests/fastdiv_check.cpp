@@ -1,7 +1,8 @@
 // Host check of na::FastDiv (paper_2403_04690_amd/csrc/na_fastdiv.h), built and
 // run by tests/test_fastdiv.py with the host compiler.
 //   * every divisor 1 <= d < 2^20: the device's double-division multiplier
-//     equals the host's integer one;
+//     equals the host's integer one, and for powers of two both are 1 (the
+//     device takes that value without dividing);
 //   * for those divisors and sampled larger ones up to 2^31 - 1: n / d is exact
 //     for dividends at the edges (0, 1, d - 1, d, d + 1, multiples of d and
 //     their neighbours, 2^31 - 1) and for pseudo-random n < 2^31.
@@ -63,6 +64,10 @@ int main() {
         const uint32_t mi = na::FastDiv::mul_int(d, s), md = na::FastDiv::mul_double(d, s);
         if (mi != md) {
             std::printf("FAIL multiplier d=%d int %u double %u\n", d, mi, md);
+            return 1;
+        }
+        if ((d & (d - 1)) == 0 && (mi != 1u || (1 << s) != d)) {  // the device's power-of-two path
+            std::printf("FAIL power of two d=%d mul %u shift %u\n", d, mi, s);
             return 1;
         }
         if (!check_divisor(d, 16)) return 1;
