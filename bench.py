@@ -43,7 +43,7 @@ WORKLOAD = workloads.BENCH_WORKLOAD
 PEAK_FP16_TFLOPS = 2516.6   # MI355X dense fp16 MFMA
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
 PMC_FILE = os.path.join(ROOT, "profiles", "na_fwd_kernel.2d_fp16_56x56_k7.pmc.txt")
-FWD_SOURCES = ["na_fwd.hip", "na_common.h", "na_stage.h", "na_index.h"]
+FWD_SOURCES = ["na_fwd.hip", "na_common.h", "na_stage.h", "na_index.h", "na_fastdiv.h"]
 
 
 def fwd_source_digest():
@@ -170,12 +170,12 @@ PAPER_A100_FUSED_OVER_NAIVE = {
 }
 
 
-def fused_vs_unfused(na, dev, spc, K=20, reps=3):
+def fused_vs_unfused(na, dev, spc, K=20, reps=3, names=None):
     """Fused forward/backward against the unfused baseline (separate PN, softmax, NN and IN
-    launches storing the attention weights) on every workload: ms per call, median of reps
-    regions of K back-to-back calls."""
+    launches storing the attention weights) on every workload (or those named): ms per call,
+    median of reps regions of K back-to-back calls."""
     rows = []
-    for name in workloads.CONFIG_ORDER:
+    for name in names or workloads.CONFIG_ORDER:
         p = workloads.CONFIGS[name]
         x = workloads.make_inputs(p, seed=0, with_grad=True)
         q, k, v, g = (x[n].to(dev) for n in ("q", "k", "v", "dout"))
@@ -294,6 +294,9 @@ def main():
                     help="only run the tuner on the workload and print its choice and timings")
     ap.add_argument("--tune-thorough", action="store_true",
                     help="let the tuner time every candidate tiling (not only the first 64)")
+    ap.add_argument("--compare-workload", choices=workloads.CONFIG_ORDER, default=None,
+                    help="profiling aid: only run the fused-versus-unfused comparison on this "
+                         "workload and print its row")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="counter calibration: only run 5 device-to-device copies of this many "
                          "MiB (the HBM traffic of each is known) and exit")
@@ -316,6 +319,16 @@ def main():
 
     na.load_library()
     dev = torch.device("cuda", 0)
+    if args.compare_workload:
+        s0, s1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        s0.record()
+        torch.cuda._sleep(1_000_000)
+        s1.record()
+        torch.cuda.synchronize()
+        spc = s0.elapsed_time(s1) * 1e-3 / 1_000_000
+        print(json.dumps(fused_vs_unfused(na, dev, spc, names=[args.compare_workload])[0]),
+              flush=True)
+        return
     p = workloads.CONFIGS[args.workload]
     x = workloads.make_inputs(p, seed=0, with_grad=True)
     q, k, v, g = (x[n].to(dev) for n in ("q", "k", "v", "dout"))
