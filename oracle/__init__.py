@@ -21,7 +21,8 @@ import os
 import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-_LIB_PATH = os.path.join(_HERE, "libna_ref.so")
+# NA_REF_LIBRARY selects another build of the same source (the sanitizer build)
+_LIB_PATH = os.environ.get("NA_REF_LIBRARY") or os.path.join(_HERE, "libna_ref.so")
 _lib = None
 
 _STATUS = {

@@ -23,6 +23,18 @@ constexpr int kVersion = 400;  // 0.4.0
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
+// A C caller may pass any int where the interface declares an enum, while C++
+// allows an enum object only the values of its enumerators' bit range.  Enum
+// arguments are therefore handed on by reference until they are validated, and
+// read through their bytes, so that an out-of-range value is rejected as such.
+template <class E>
+int enum_bits(const E& e) {
+    static_assert(sizeof(E) == sizeof(int), "C enums are int-sized here");
+    int v;
+    std::memcpy(&v, &e, sizeof v);
+    return v;
+}
+
 int ilog2(int x) {  // x is a power of two
     int l = 0;
     while ((1 << l) < x) ++l;
@@ -114,7 +126,7 @@ bool geo_from_tiling(int rank, const int64_t* extents, const int32_t* ks, const 
 }
 
 na_status check_problem(int rank, const int64_t* extents, const int32_t* ks, const int32_t* ds,
-                        int64_t batch, int64_t heads, int64_t head_dim, na_dtype dtype,
+                        int64_t batch, int64_t heads, int64_t head_dim, const na_dtype& dtype,
                         float scale) {
     if (rank < 1 || rank > 3) return NA_ERR_RANK;
     if (!extents || !ks || !ds) return NA_ERR_NULL;
@@ -126,7 +138,8 @@ na_status check_problem(int rank, const int64_t* extents, const int32_t* ks, con
     }
     if (batch < 0 || heads < 0) return NA_ERR_SHAPE;
     if (head_dim != 32 && head_dim != 64 && head_dim != 128) return NA_ERR_HEAD_DIM;
-    if (dtype != NA_FP32 && dtype != NA_FP16 && dtype != NA_BF16) return NA_ERR_DTYPE;
+    const int dt = enum_bits(dtype);
+    if (dt != NA_FP32 && dt != NA_FP16 && dt != NA_BF16) return NA_ERR_DTYPE;
     if (!std::isfinite(scale)) return NA_ERR_SCALE;
     const int64_t N = token_count(rank, extents);
     if (N < 0 || N * head_dim >= (int64_t(1) << 31)) return NA_ERR_SHAPE;
@@ -388,7 +401,8 @@ na_status check_launchable(int rank, const int64_t* extents, const int32_t* ks, 
 }
 
 na_status check_all(int rank, const int64_t* extents, const int32_t* ks, const int32_t* ds,
-                    int64_t batch, int64_t heads, int64_t head_dim, na_dtype dtype, float scale) {
+                    int64_t batch, int64_t heads, int64_t head_dim, const na_dtype& dtype,
+                    float scale) {
     na_status st = check_problem(rank, extents, ks, ds, batch, heads, head_dim, dtype, scale);
     if (st != NA_OK) return st;
     return check_launchable(rank, extents, ks, ds, batch, heads, head_dim, dtype);
@@ -644,8 +658,8 @@ bool ugeo_from_problem(int rank, const int64_t* extents, const int32_t* ks, cons
 // which of x, y, z (and lse) the operator reads or writes.
 na_status run_unfused(int rank, const int64_t* extents, const int32_t* ks, const int32_t* ds,
                       const int32_t* causal, int64_t batch, int64_t heads, int64_t head_dim,
-                      na_dtype dtype, float scale, int op, const void* x, const void* y, void* z,
-                      float* lse, na_stream_t stream) {
+                      const na_dtype& dtype, float scale, int op, const void* x, const void* y,
+                      void* z, float* lse, na_stream_t stream) {
     na_status st = check_problem(rank, extents, ks, ds, batch, heads, head_dim, dtype, scale);
     if (st != NA_OK) return st;
     if (empty_problem(rank, extents, batch, heads)) return NA_OK;
@@ -668,7 +682,7 @@ na_status run_unfused(int rank, const int64_t* extents, const int32_t* ks, const
 extern "C" {
 
 const char* na_status_string(na_status status) {
-    switch (status) {
+    switch (enum_bits(status)) {
         case NA_OK: return "ok";
         case NA_ERR_NULL: return "a required pointer is NULL";
         case NA_ERR_RANK: return "rank must be 1, 2 or 3";

@@ -74,7 +74,8 @@ def test_validate_statuses(lib):
         assert _validate(lib, D=D) == NA_ERR_HEAD_DIM
     for D in (32, 64, 128):
         assert _validate(lib, D=D) == NA_OK
-    assert _validate(lib, dt=3) == NA_ERR_DTYPE
+    for dt in (3, 99, -1, 1 << 30):  # any int may come through the C interface
+        assert _validate(lib, dt=dt) == NA_ERR_DTYPE
     assert _validate(lib, scale=float("inf")) == NA_ERR_SCALE
     assert _validate(lib, scale=float("nan")) == NA_ERR_SCALE
     assert _validate(lib, B=-1) == NA_ERR_SHAPE
@@ -96,7 +97,7 @@ def test_status_strings(lib):
     for s in list(range(10)) + [11, 12]:
         text = lib.na_status_string(s).decode()
         assert text and text != "unknown status"
-    for s in (10, 99):  # 10 is not a status code
+    for s in (10, 14, 99, -1):  # 10 is not a status code
         assert lib.na_status_string(s).decode() == "unknown status"
     assert lib.na_version() >= 100
 
