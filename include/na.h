@@ -188,7 +188,16 @@ na_status na_backward(int rank, const int64_t* extents, const int32_t* kernel_si
  * forward, best backward, heuristic forward, heuristic backward} in
  * milliseconds per launch.
  *
- * na_tune_clear: empties the cache.
+ * na_tune_clear: empties the cache, and drops every plan (below).
+ *
+ * Plans: na_forward and na_backward keep, per calling thread, the last few
+ * problems they validated with the tiling and launch geometry chosen for each,
+ * and launch a repeated problem from its plan (checking only the scale and the
+ * pointers).  Recording a tuned tiling, na_tune_clear and na_set_autotune
+ * retire every plan.  The forcing variables NA_WAVE_BLOCKS=1|2 (blocks per
+ * wave), NA_FWD_WAVES=4|8 (1-D forward workgroup size) and NA_BWD_SPLIT=0|1
+ * (backward form) are read when a plan is made: after changing one, call
+ * na_tune_clear for it to take effect on problems already planned.
  *
  * na_set_autotune (tune on first use, App. A): mode 1 makes na_forward and
  * na_backward tune a problem whose tiling is not cached yet (forward and

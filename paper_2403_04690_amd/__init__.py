@@ -13,6 +13,7 @@ be causal (``causal``, one flag per axis): there a query attends only to the
 k nearest positions not after it.
 """
 import ctypes
+import functools
 import math
 import os
 
@@ -139,7 +140,8 @@ def _per_axis(value, rank, name):
     return vals
 
 
-def _problem_arrays(extents, kernel_size, dilation, causal=None):
+@functools.lru_cache(maxsize=256)
+def _problem_arrays_of(extents, kernel_size, dilation, causal):
     rank = len(extents)
     ext = (ctypes.c_int64 * rank)(*[int(e) for e in extents])
     ks = (ctypes.c_int32 * rank)(*_per_axis(kernel_size, rank, "kernel_size"))
@@ -149,8 +151,24 @@ def _problem_arrays(extents, kernel_size, dilation, causal=None):
     return rank, ext, ks, ds, cs
 
 
+def _hashable(value):
+    return tuple(value) if isinstance(value, (list, tuple)) else value
+
+
+def _problem_arrays(extents, kernel_size, dilation, causal=None):
+    """The problem as ctypes arrays (read only by the library; cached per problem)."""
+    return _problem_arrays_of(tuple(extents), _hashable(kernel_size), _hashable(dilation),
+                              None if causal is None else _hashable(causal))
+
+
+# the current stream's handle without building a Stream object (where torch has it)
+_raw_stream = getattr(torch._C, "_cuda_getCurrentRawStream", None)
+
+
 def _stream(device):
-    return _vp(torch.cuda.current_stream(device).cuda_stream)
+    if _raw_stream is not None:
+        return _raw_stream(device.index)
+    return torch.cuda.current_stream(device).cuda_stream
 
 
 def _check_tensors(ref, *others):

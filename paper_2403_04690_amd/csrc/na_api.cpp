@@ -420,6 +420,18 @@ na_status run_forward(int rank, const int64_t* extents, const int32_t* ks, const
     return e == hipSuccess ? NA_OK : NA_ERR_HIP;
 }
 
+// Whether a backward runs as the split form (a Delta pre-pass, then the dK/dV
+// and the dQ workgroups as two launches): large 3-D problems with two blocks
+// per wave, whose dK/dV role otherwise holds the dQ role to its own occupancy.
+// NA_BWD_SPLIT=0|1 forces the choice.
+int bwd_split(int rank, const na_tiling& t) {
+    if (const char* env = std::getenv("NA_BWD_SPLIT")) {
+        if (env[0] == '0') return 0;
+        if (env[0] == '1') return 1;
+    }
+    return rank == 3 && t.blocks_per_wave == 2 ? 1 : 0;
+}
+
 na_status run_backward(int rank, const int64_t* extents, const int32_t* ks, const int32_t* ds,
                        const int32_t* causal, int64_t BH, int64_t head_dim, na_dtype dtype,
                        float scale, const na_tiling& t, const void* q, const void* k,
@@ -427,6 +439,7 @@ na_status run_backward(int rank, const int64_t* extents, const int32_t* ks, cons
                        void* dq, void* dk, void* dv, hipStream_t s) {
     na::Geo g;
     if (!geo_from_tiling(rank, extents, ks, ds, causal, BH, t, g, false)) return NA_ERR_SHAPE;
+    g.bwd_split = bwd_split(rank, t);
     hipError_t e = na::launch_backward(g, rank, (int)head_dim, (int)dtype, t.blocks_per_wave, q,
                                        k, v, out, lse, dout, dq, dk, dv, scale, s);
     return e == hipSuccess ? NA_OK : NA_ERR_HIP;
@@ -569,7 +582,73 @@ na_status tune_backward(int rank, const int64_t* extents, const int32_t* ks, con
                         out, lse, dout, dq, dk, dv, s);
 }
 
+// ---- per-thread plans ----
+// A problem's validation, tiling and launch geometry depend only on its shape,
+// the tuner's cache, the autotune mode and the forcing variables (NA_WAVE_BLOCKS,
+// NA_FWD_WAVES, NA_BWD_SPLIT), so each thread keeps the last few it made and
+// launches from them directly.  A plan belongs to the generation it was made
+// in; storing a tuned tiling, na_tune_clear and na_set_autotune start a new
+// one (na_tune_clear is also how a changed forcing variable takes effect).
+std::atomic<unsigned> g_generation{1};
+
+void new_generation() { g_generation.fetch_add(1, std::memory_order_acq_rel); }
+
+struct PlanKey {
+    int32_t rank, dtype, forward, causal[3], k[3], d[3];
+    int64_t L[3], batch, heads, head_dim;
+};
+struct Plan {
+    PlanKey key;
+    unsigned gen;  // 0: never filled
+    na_tiling t;
+    na::Geo g;
+};
+constexpr int kPlans = 8;
+thread_local Plan t_plans[kPlans];
+thread_local int t_plan_next = 0;
+
+// The key of a problem whose arrays can be read (false: the full validation
+// reports the problem).
+bool plan_key(int rank, const int64_t* extents, const int32_t* ks, const int32_t* ds,
+              const int32_t* causal, int64_t batch, int64_t heads, int64_t head_dim,
+              const na_dtype& dtype, bool forward, PlanKey& key) {
+    if (rank < 1 || rank > 3 || !extents || !ks || !ds) return false;
+    std::memset(&key, 0, sizeof(key));
+    key.rank = rank;
+    key.dtype = enum_bits(dtype);
+    key.forward = forward ? 1 : 0;
+    for (int a = 0; a < rank; ++a) {
+        key.L[a] = extents[a];
+        key.k[a] = ks[a];
+        key.d[a] = ds[a];
+        key.causal[a] = causal && causal[a] ? 1 : 0;
+    }
+    key.batch = batch;
+    key.heads = heads;
+    key.head_dim = head_dim;
+    return true;
+}
+
+const Plan* find_plan(const PlanKey& key) {
+    const unsigned gen = g_generation.load(std::memory_order_acquire);
+    for (const Plan& p : t_plans)
+        if (p.gen == gen && std::memcmp(&p.key, &key, sizeof(key)) == 0) return &p;
+    return nullptr;
+}
+
+// gen: the generation read before the plan's tiling was chosen (a plan made
+// across a change of generation is never found again)
+void store_plan(const PlanKey& key, unsigned gen, const na_tiling& t, const na::Geo& g) {
+    Plan& p = t_plans[t_plan_next];
+    t_plan_next = (t_plan_next + 1) % kPlans;
+    p.key = key;
+    p.gen = gen;
+    p.t = t;
+    p.g = g;
+}
+
 void cache_store(const std::vector<int64_t>& key, const na_tiling* fwd, const na_tiling* bwd) {
+    new_generation();
     std::lock_guard<std::mutex> lock(g_cache_mu);
     Tuned& e = tiling_cache()[key];
     if (fwd) {
@@ -713,6 +792,22 @@ na_status na_forward(int rank, const int64_t* extents, const int32_t* kernel_siz
                      const int32_t* dilation, const int32_t* causal, int64_t batch, int64_t heads,
                      int64_t head_dim, na_dtype dtype, float scale, const void* q, const void* k,
                      const void* v, void* out, float* logsumexp, na_stream_t stream) {
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    PlanKey pk;
+    const bool keyed = plan_key(rank, extents, kernel_size, dilation, causal, batch, heads,
+                                head_dim, dtype, true, pk);
+    if (keyed) {
+        if (const Plan* p = find_plan(pk)) {
+            if (!std::isfinite(scale)) return NA_ERR_SCALE;
+            const na_status st = forward_pointers(q, k, v, out, logsumexp);
+            if (st != NA_OK) return st;
+            const hipError_t e = na::launch_forward(p->g, rank, (int)head_dim, (int)dtype,
+                                                    p->t.blocks_per_wave, q, k, v, out, logsumexp,
+                                                    scale, s);
+            return e == hipSuccess ? NA_OK : NA_ERR_HIP;
+        }
+    }
+    const unsigned gen = g_generation.load(std::memory_order_acquire);
     na_status st = check_all(rank, extents, kernel_size, dilation, batch, heads, head_dim, dtype,
                              scale);
     if (st != NA_OK) return st;
@@ -720,25 +815,33 @@ na_status na_forward(int rank, const int64_t* extents, const int32_t* kernel_siz
     st = forward_pointers(q, k, v, out, logsumexp);
     if (st != NA_OK) return st;
     const int64_t BH = batch * heads;
-    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    bool planned = keyed;
     const int mode = autotune_mode();
     if (mode) {
         const auto key = problem_key(rank, extents, kernel_size, dilation, causal, BH, head_dim,
                                      dtype);
-        if (!cache_has(key, true) && !stream_capturing(s)) {
-            na_tiling t;
-            float tb = 0.f, th = 0.f;
-            st = tune_forward(rank, extents, kernel_size, dilation, causal, BH, head_dim, dtype,
-                              scale, q, k, v, out, logsumexp, kAutotuneRepeats, mode == 2, s, t,
-                              tb, th);
-            if (st == NA_OK) cache_store(key, &t, nullptr);
-            return st;
+        if (!cache_has(key, true)) {
+            if (!stream_capturing(s)) {
+                na_tiling t;
+                float tb = 0.f, th = 0.f;
+                st = tune_forward(rank, extents, kernel_size, dilation, causal, BH, head_dim,
+                                  dtype, scale, q, k, v, out, logsumexp, kAutotuneRepeats,
+                                  mode == 2, s, t, tb, th);
+                if (st == NA_OK) cache_store(key, &t, nullptr);
+                return st;
+            }
+            planned = false;  // tuned by a later call, outside the capture
         }
     }
     const na_tiling t = current_tiling(rank, extents, kernel_size, dilation, causal, BH, head_dim,
                                        dtype, true);
-    return run_forward(rank, extents, kernel_size, dilation, causal, BH, head_dim, dtype, scale, t,
-                       q, k, v, out, logsumexp, s);
+    na::Geo g;
+    if (!geo_from_tiling(rank, extents, kernel_size, dilation, causal, BH, t, g, true))
+        return NA_ERR_SHAPE;
+    if (planned) store_plan(pk, gen, t, g);
+    const hipError_t e = na::launch_forward(g, rank, (int)head_dim, (int)dtype, t.blocks_per_wave,
+                                            q, k, v, out, logsumexp, scale, s);
+    return e == hipSuccess ? NA_OK : NA_ERR_HIP;
 }
 
 na_status na_backward(int rank, const int64_t* extents, const int32_t* kernel_size,
@@ -746,6 +849,22 @@ na_status na_backward(int rank, const int64_t* extents, const int32_t* kernel_si
                       int64_t head_dim, na_dtype dtype, float scale, const void* q, const void* k,
                       const void* v, const void* out, const float* logsumexp, const void* dout,
                       void* dq, void* dk, void* dv, na_stream_t stream) {
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    PlanKey pk;
+    const bool keyed = plan_key(rank, extents, kernel_size, dilation, causal, batch, heads,
+                                head_dim, dtype, false, pk);
+    if (keyed) {
+        if (const Plan* p = find_plan(pk)) {
+            if (!std::isfinite(scale)) return NA_ERR_SCALE;
+            const na_status st = backward_pointers(q, k, v, out, logsumexp, dout, dq, dk, dv);
+            if (st != NA_OK) return st;
+            const hipError_t e = na::launch_backward(p->g, rank, (int)head_dim, (int)dtype,
+                                                     p->t.blocks_per_wave, q, k, v, out, logsumexp,
+                                                     dout, dq, dk, dv, scale, s);
+            return e == hipSuccess ? NA_OK : NA_ERR_HIP;
+        }
+    }
+    const unsigned gen = g_generation.load(std::memory_order_acquire);
     na_status st = check_all(rank, extents, kernel_size, dilation, batch, heads, head_dim, dtype,
                              scale);
     if (st != NA_OK) return st;
@@ -753,25 +872,35 @@ na_status na_backward(int rank, const int64_t* extents, const int32_t* kernel_si
     st = backward_pointers(q, k, v, out, logsumexp, dout, dq, dk, dv);
     if (st != NA_OK) return st;
     const int64_t BH = batch * heads;
-    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    bool planned = keyed;
     const int mode = autotune_mode();
     if (mode) {
         const auto key = problem_key(rank, extents, kernel_size, dilation, causal, BH, head_dim,
                                      dtype);
-        if (!cache_has(key, false) && !stream_capturing(s)) {
-            na_tiling t;
-            float tb = 0.f, th = 0.f;
-            st = tune_backward(rank, extents, kernel_size, dilation, causal, BH, head_dim, dtype,
-                               scale, q, k, v, out, logsumexp, dout, dq, dk, dv, kAutotuneRepeats,
-                               mode == 2, s, t, tb, th);
-            if (st == NA_OK) cache_store(key, nullptr, &t);
-            return st;
+        if (!cache_has(key, false)) {
+            if (!stream_capturing(s)) {
+                na_tiling t;
+                float tb = 0.f, th = 0.f;
+                st = tune_backward(rank, extents, kernel_size, dilation, causal, BH, head_dim,
+                                   dtype, scale, q, k, v, out, logsumexp, dout, dq, dk, dv,
+                                   kAutotuneRepeats, mode == 2, s, t, tb, th);
+                if (st == NA_OK) cache_store(key, nullptr, &t);
+                return st;
+            }
+            planned = false;  // tuned by a later call, outside the capture
         }
     }
     const na_tiling t = current_tiling(rank, extents, kernel_size, dilation, causal, BH, head_dim,
                                        dtype, false);
-    return run_backward(rank, extents, kernel_size, dilation, causal, BH, head_dim, dtype, scale,
-                        t, q, k, v, out, logsumexp, dout, dq, dk, dv, s);
+    na::Geo g;
+    if (!geo_from_tiling(rank, extents, kernel_size, dilation, causal, BH, t, g, false))
+        return NA_ERR_SHAPE;
+    g.bwd_split = bwd_split(rank, t);
+    if (planned) store_plan(pk, gen, t, g);
+    const hipError_t e = na::launch_backward(g, rank, (int)head_dim, (int)dtype,
+                                             t.blocks_per_wave, q, k, v, out, logsumexp, dout, dq,
+                                             dk, dv, scale, s);
+    return e == hipSuccess ? NA_OK : NA_ERR_HIP;
 }
 
 int na_candidate_tilings(int rank, const int64_t* extents, const int32_t* kernel_size,
@@ -875,6 +1004,7 @@ na_status na_tune(int rank, const int64_t* extents, const int32_t* kernel_size,
 }
 
 void na_tune_clear(void) {
+    new_generation();
     std::lock_guard<std::mutex> lock(g_cache_mu);
     tiling_cache().clear();
 }
@@ -920,7 +1050,10 @@ na_status na_unfused_softmax_backward(int rank, const int64_t* extents,
                        1.0f, na::kUnfusedSoftmaxBwd, probs, nullptr, grad, nullptr, stream);
 }
 
-void na_set_autotune(int mode) { g_autotune.store(mode == 1 || mode == 2 ? mode : 0); }
+void na_set_autotune(int mode) {
+    g_autotune.store(mode == 1 || mode == 2 ? mode : 0);
+    new_generation();
+}
 
 int na_autotune(void) { return autotune_mode(); }
 

@@ -18,7 +18,6 @@
 // The roles are independent, so they share the GPU instead of running as
 // consecutive launches.
 #include <algorithm>
-#include <cstdlib>
 #include <type_traits>
 
 #include "na_launch.h"
@@ -315,7 +314,7 @@ __device__ __forceinline__ void dq_role(const Geo& g, int braw, unsigned char* s
 #pragma unroll
                     for (int m = 0; m < QM; ++m) dqacc[m][db] = Tr<T>::mma(kf, dsf[m], dqacc[m][db]);
                 }
-                        };
+            };
             // the specialised tiles first (the order of tiles does not matter)
             const uint64_t pairs = short_rows ? ofullm & (ofullm >> 1) : fullm & (fullm >> 1);
             uint64_t fast_tiles = pairs & tiles;
@@ -968,17 +967,6 @@ static hipError_t launch_bwd_sb(const Geo& g, bool short_rows, bool split, int h
     return launch(kern, std::max(lds_q, lds_k), nwk + g.nwg, nullptr);
 }
 
-// Whether a backward runs as the split form: large 3-D problems with two
-// blocks per wave, whose dK/dV role otherwise holds the dQ role to its own
-// occupancy.  NA_BWD_SPLIT=0|1 forces the choice.
-static bool use_split(const Geo& g, int rank, int qm) {
-    if (const char* env = std::getenv("NA_BWD_SPLIT")) {
-        if (env[0] == '0') return false;
-        if (env[0] == '1') return true;
-    }
-    return rank == 3 && qm == 2;
-}
-
 template <int R, int D, typename T, int QM, int KM>
 static hipError_t launch_bwd_inst(const Geo& g, const void* q, const void* k, const void* v,
                                   const void* o, const float* lse, const void* dout, void* dq,
@@ -991,7 +979,7 @@ static hipError_t launch_bwd_inst(const Geo& g, const void* q, const void* k, co
     const int hq = box_blocks(eq, R), hk = box_blocks(ek, R);
     // rows of every halo (dQ) and query box (dK/dV) hold at most 2 blocks
     const bool short_rows = R > 1 && (eq[R - 1] + 15) / 16 <= 2 && (ek[R - 1] + 15) / 16 <= 2;
-    const bool split = use_split(g, R, QM);
+    const bool split = g.bwd_split != 0;  // chosen on the host with the tiling
     // D = 32, 16-bit: boxes of up to 16 blocks are staged whole (one stage)
     if constexpr (sizeof(T) == 2 && D == 32) {
         if (hq <= 16 && hk <= 16)

@@ -216,6 +216,7 @@ struct Geo {
     int lgWT[kMaxRank];  // log2 WT (wave tiles are powers of two)
     int lgWGd[kMaxRank]; // log2 WGd
     FastDiv fd_ntiles, fd_ngroups, fd_d[kMaxRank], fd_nt[kMaxRank];
+    int bwd_split;       // backward only: run as the split form (chosen on the host)
 };
 
 // Brings the Geo fields of the problem's R axes into scalar registers in one

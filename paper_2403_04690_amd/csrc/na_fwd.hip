@@ -56,15 +56,21 @@ struct FwdCfg {
     static_assert(SB % 2 == 0 && SB <= 32, "stage blocks are tested by one lane each");
 };
 
+// Workgroups per CU the register allocation must allow: four waves per SIMD
+// for the 16-bit kernels that fit 128 VGPRs (every one at D <= 64, and the
+// one-block ones at D = 128); the others take what they need.
+template <int D, typename T, int QM, int W>
+constexpr int fwd_min_blocks() {
+    return sizeof(T) == 2 && (D <= 64 || QM == 1) ? 16 / W : 1;
+}
+
 // c = scale * log2(e): scores are kept in base 2.  SHORT = 1: every halo row
 // holds at most two 16-key blocks (rank >= 2), so the inner-axis mask is a
 // per-lane constant; SHORT = 0: general masking with mask-free full blocks.
 template <int R, int D, typename T, int QM, int SB, int SHORT, int W>
-__global__ __launch_bounds__(W * kWave) void na_fwd_kernel(Geo g, const T* __restrict__ qg,
-                                                           const T* __restrict__ kg,
-                                                           const T* __restrict__ vg,
-                                                           T* __restrict__ og,
-                                                           float* __restrict__ lseg, float c) {
+__global__ __launch_bounds__(W * kWave, (fwd_min_blocks<D, T, QM, W>())) void na_fwd_kernel(
+    Geo g, const T* __restrict__ qg, const T* __restrict__ kg, const T* __restrict__ vg,
+    T* __restrict__ og, float* __restrict__ lseg, float c) {
     using C = FwdCfg<R, D, T, QM, SB, W>;
     using x8 = typename Tr<T>::x8;
     extern __shared__ __align__(16) unsigned char smem_raw[];
@@ -98,6 +104,18 @@ __global__ __launch_bounds__(W * kWave) void na_fwd_kernel(Geo g, const T* __res
     const T* kb = kg + slice;
     const T* vb = vg + slice;
     const int tstep = g.d[R - 1];  // token step along the innermost axis
+
+    // ---- staging: K and V rows straight to LDS, one address set for both ----
+    // The first stage is issued as soon as the halo is known, so that its
+    // loads are in flight during the per-wave and per-lane set-up below.
+    typename C::Ld ld;
+    auto issue_stage = [&](int s, int buf) {
+        ld.compute(halo, g, gc, s * SB, tstep, wave, lane);
+        unsigned char* tile = smem_raw + buf * C::kBufBytes;
+        ld.issue(kb, tile, wave);
+        ld.issue(vb, tile + C::kTileBytes, wave);
+    };
+    issue_stage(0, 0);
 
     // ---- this wave's query sub-box: its halo and the keys inside all of its windows ----
     int wc[kMaxRank], wo[kMaxRank];
@@ -146,14 +164,6 @@ __global__ __launch_bounds__(W * kWave) void na_fwd_kernel(Geo g, const T* __res
         for (int s = 0; s < C::kKS; ++s) qf[m][s] = ld_x8<T>(qg + qoff[m] + s * 32 + grp * 8);
     }
 
-    // ---- staging: K and V rows straight to LDS, one address set for both ----
-    typename C::Ld ld;
-    auto issue_stage = [&](int s, int buf) {
-        ld.compute(halo, g, gc, s * SB, tstep, wave, lane);
-        unsigned char* tile = smem_raw + buf * C::kBufBytes;
-        ld.issue(kb, tile, wave);
-        ld.issue(vb, tile + C::kTileBytes, wave);
-    };
     RowFrag<T, D> kfr;
     ColFrag<T, D> vfr;
     kfr.init(lane);
@@ -224,7 +234,6 @@ __global__ __launch_bounds__(W * kWave) void na_fwd_kernel(Geo g, const T* __res
     }
 
     const int nst = (halo.nb + SB - 1) / SB;
-    issue_stage(0, 0);
     wait_vmem();
     __syncthreads();
     // kFoldAdd: Q scaled once by c = scale*log2(e) and rounded to T, so the
@@ -414,7 +423,7 @@ __global__ __launch_bounds__(W * kWave) void na_fwd_kernel(Geo g, const T* __res
 #pragma unroll
                     for (int m = 0; m < QM; ++m) lsum[m] = Tr<T>::mma(ones, pf[m], lsum[m]);
                 }
-                        };
+            };
             // Tiles of two full blocks (kind 1, rows of more than two blocks) or
             // of two outer-full blocks (kind 2, short rows) are visited first, by
             // bodies without per-block branches; the order of tiles is free in

@@ -24,21 +24,27 @@ NA_HD int group_len(int L, int d, int g) { return (L - g + d - 1) / d; }
 
 // First and last (inclusive) window positions of the query at group position
 // p (group of n tokens, window k, causal axis or not).
+// Both forms are one clamp, min(max(p - h, 0), n - k), with h = k - 1 on a
+// causal axis and k / 2 otherwise (a causal start p - k + 1 never exceeds
+// n - k, as p <= n - 1); written without branches.
+NA_HD int win_half(int k, bool causal) { return causal ? k - 1 : k >> 1; }
 NA_HD int win_start(int p, int n, int k, bool causal) {
-    if (causal) return p - k + 1 < 0 ? 0 : p - k + 1;
-    int s = p - k / 2;
-    s = s < 0 ? 0 : s;
-    return s > n - k ? n - k : s;
+    const int s = p - win_half(k, causal);
+    const int c = s < 0 ? 0 : s;
+    return c > n - k ? n - k : c;
 }
 NA_HD int win_last(int p, int n, int k, bool causal) {
-    return causal ? p : win_start(p, n, k, false) + k - 1;
+    const int e = win_start(p, n, k, causal) + k - 1;
+    return causal ? p : e;
 }
 
 // Start of the window as the kernels' mask tests use it, (unsigned)(j - s) < k:
 // along a causal axis the unclamped p - k + 1, which with j >= 0 admits exactly
 // the positions max(0, p - k + 1) .. p.
 NA_HD int mask_start(int p, int n, int k, bool causal) {
-    return causal ? p - k + 1 : win_start(p, n, k, false);
+    const int s = p - win_half(k, causal);
+    const int c = s < 0 && !causal ? 0 : s;
+    return c > n - k ? n - k : c;
 }
 
 // Inverse neighbourhood of key position j (Sec. 3.1, operator IN): the

@@ -40,6 +40,7 @@ const char* c_status_string(int status);
 namespace {
 
 long g_checks = 0, g_launches = 0;
+na_tiling g_last{};  // tiling of the last fused launch
 bool g_fail_launch = false;
 bool g_capturing = false;
 double g_clock = 0.0;  // modelled device time, ms
@@ -136,7 +137,14 @@ void check_geo(const na::Geo& g, bool forward, int qm) {
     }
     check_fastdiv(g.fd_ntiles, g.ntiles, g.nwg);
     check_fastdiv(g.fd_ngroups, g.ngroups, g.nwg);
+    // the split form: large 3-D backwards with two blocks per wave
+    if (!forward) CHECK(g.bwd_split == (p.rank == 3 && qm == 2 ? 1 : 0));
     const int wta[3] = {g.WT[0], g.WT[1], g.WT[2]}, wga[3] = {g.WGd[0], g.WGd[1], g.WGd[2]};
+    g_last.blocks_per_wave = qm;
+    for (int a = 0; a < 3; ++a) {
+        g_last.wave_tile[a] = wta[a];
+        g_last.waves[a] = wga[a];
+    }
     g_clock += tiling_cost(qm, wta, wga);
 }
 
@@ -353,15 +361,23 @@ void drive_valid(const Problem& p) {
         CHECK(g_launches == before);
     }
     // default entry points: one launch each, NULL and misaligned pointers refused
+    // (the second calls take the per-thread plan the first made)
     na_set_autotune(0);
     long before = g_launches;
     CHECK(fwd(p) == NA_OK && bwd(p) == NA_OK && g_launches == before + 2);
+    CHECK(fwd(p) == NA_OK && bwd(p) == NA_OK && g_launches == before + 4);
+    before = g_launches;
+    CHECK(na_forward(p.rank, p.L, p.k, p.d, causal_of(p), p.B, p.H, p.D, p.dt, INFINITY, fake(0),
+                     fake(1), fake(2), fake(3), (float*)fake(4), nullptr) == NA_ERR_SCALE);
+    CHECK(na_backward(p.rank, p.L, p.k, p.d, causal_of(p), p.B, p.H, p.D, p.dt, NAN, fake(0),
+                      fake(1), fake(2), fake(3), (float*)fake(4), fake(5), fake(6), fake(7),
+                      fake(8), nullptr) == NA_ERR_SCALE);
     CHECK(na_forward(p.rank, p.L, p.k, p.d, causal_of(p), p.B, p.H, p.D, p.dt, 0.5f, fake(0),
                      nullptr, fake(2), fake(3), (float*)fake(4), nullptr) == NA_ERR_NULL);
     CHECK(na_backward(p.rank, p.L, p.k, p.d, causal_of(p), p.B, p.H, p.D, p.dt, 0.5f, fake(0),
                       fake(1), fake(2), fake(3), (float*)fake(4), fake(5), fake(6),
                       (char*)fake(7) + 8, fake(8), nullptr) == NA_ERR_ALIGNMENT);
-    CHECK(g_launches == before + 2);
+    CHECK(g_launches == before);
     // a failed launch is reported, also from inside the tuner
     g_fail_launch = true;
     CHECK(fwd(p) == NA_ERR_HIP && bwd(p) == NA_ERR_HIP);
@@ -370,9 +386,14 @@ void drive_valid(const Problem& p) {
     // the tuner's choice under the modelled clock, default and thorough
     for (int flags = 0; flags <= NA_TUNE_THOROUGH; ++flags) {
         na_tune_clear();
+        CHECK(fwd(p) == NA_OK && bwd(p) == NA_OK);  // plans with the heuristic tilings
         na_tiling bf, bb;
         float tm[4] = {-1.f, -1.f, -1.f, -1.f};
         CHECK(tune(p, flags, &bf, &bb, tm) == NA_OK);
+        // storing the tuned tilings retires those plans
+        CHECK(fwd(p) == NA_OK && same(g_last, bf));
+        CHECK(bwd(p) == NA_OK && same(g_last, bb));
+        CHECK(fwd(p) == NA_OK && same(g_last, bf));
         CHECK(same(bf, expected_choice(cands(p, true), flags != 0)));
         CHECK(same(bb, expected_choice(cands(p, false), flags != 0)));
         for (float t : tm) CHECK(t > 0.f);

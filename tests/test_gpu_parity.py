@@ -34,6 +34,20 @@ def na():
     return lib
 
 
+@pytest.fixture
+def force(monkeypatch, na):
+    """Sets forcing variables (NA_WAVE_BLOCKS, NA_FWD_WAVES, NA_BWD_SPLIT) for one test.
+    The library reads them when it makes a problem's plan, so plans are dropped
+    (na.tune_clear) when they are set and again once they are restored."""
+    def set_(**env):
+        for name, value in env.items():
+            monkeypatch.setenv(name, str(value))
+        na.tune_clear()
+    yield set_
+    monkeypatch.undo()
+    na.tune_clear()
+
+
 def _inputs(shape, dtype, seed, n=4):
     gen = torch.Generator().manual_seed(seed)
     return [torch.randn(shape, generator=gen).to(TDT[dtype]) for _ in range(n)]
@@ -147,9 +161,8 @@ EIGHT_WAVE_CASES = [
 
 
 @pytest.mark.parametrize("ext,ks,ds,cs,D,dtype,B,H,m", EIGHT_WAVE_CASES)
-def test_forward_eight_wave_workgroups(na, monkeypatch, ext, ks, ds, cs, D, dtype, B, H, m):
-    monkeypatch.setenv("NA_FWD_WAVES", "8")
-    monkeypatch.setenv("NA_WAVE_BLOCKS", str(m))
+def test_forward_eight_wave_workgroups(na, force, ext, ks, ds, cs, D, dtype, B, H, m):
+    force(NA_FWD_WAVES=8, NA_WAVE_BLOCKS=m)
     shape = (B, H) + ext + (D,)
     q, k, v = _inputs(shape, dtype, 13, 3)
     out, lse = na.forward(*_dev(q, k, v), ks, ds, causal=cs)
@@ -265,8 +278,8 @@ STEEP_CASES = [
 
 
 @pytest.mark.parametrize("ext,ks,D,dtype,a,m", STEEP_CASES)
-def test_steep_scores_raise_the_reference(na, monkeypatch, ext, ks, D, dtype, a, m):
-    monkeypatch.setenv("NA_WAVE_BLOCKS", str(m))
+def test_steep_scores_raise_the_reference(na, force, ext, ks, D, dtype, a, m):
+    force(NA_WAVE_BLOCKS=m)
     (q, k, v, g), scale = _steep_inputs(ext, D, dtype, a)
     ds = (1,) * len(ext)
     ell = int(np.prod(ks))
@@ -417,9 +430,8 @@ SPLIT_CASES = [
 
 
 @pytest.mark.parametrize("ext,ks,ds,cs,D,dtype,m,split", SPLIT_CASES)
-def test_backward_split_and_single_launch(na, monkeypatch, ext, ks, ds, cs, D, dtype, m, split):
-    monkeypatch.setenv("NA_WAVE_BLOCKS", str(m))
-    monkeypatch.setenv("NA_BWD_SPLIT", str(split))
+def test_backward_split_and_single_launch(na, force, ext, ks, ds, cs, D, dtype, m, split):
+    force(NA_WAVE_BLOCKS=m, NA_BWD_SPLIT=split)
     shape = (1, 2) + ext + (D,)
     q, k, v, g = _inputs(shape, dtype, 24, 4)
     qd, kd, vd, gd = _dev(q, k, v, g)
@@ -701,12 +713,12 @@ D128_CASES = [
 
 
 @pytest.mark.parametrize("ext,ks,ds,dtype,B,H,m,eight", D128_CASES)
-def test_head_dim_128_two_blocks_per_wave(na, monkeypatch, ext, ks, ds, dtype, B, H, m, eight):
+def test_head_dim_128_two_blocks_per_wave(na, force, ext, ks, ds, dtype, B, H, m, eight):
     D = 128
     if m is not None:
-        monkeypatch.setenv("NA_WAVE_BLOCKS", str(m))
+        force(NA_WAVE_BLOCKS=m)
     if eight:
-        monkeypatch.setenv("NA_FWD_WAVES", "8")
+        force(NA_FWD_WAVES=8)
     t = na.current_tiling(ext, ks, ds, B, H, D, TDT[dtype], forward=True)
     assert t.blocks_per_wave == 2 and (not eight or t.waves[0] == 8), t
     shape = (B, H) + ext + (D,)
