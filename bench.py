@@ -367,12 +367,6 @@ def main():
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
-    # host cost of enqueueing one step (no synchronisation inside)
-    t0 = time.perf_counter()
-    for _ in range(max(args.warmup, 5)):
-        step()
-    host_step_s = (time.perf_counter() - t0) / max(args.warmup, 5)
-    torch.cuda.synchronize()
     # rate of the GPU-side spin used to give the host a head start
     s0, s1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     s0.record()
@@ -380,6 +374,15 @@ def main():
     s1.record()
     torch.cuda.synchronize()
     spin_s_per_cycle = s0.elapsed_time(s1) * 1e-3 / 1_000_000
+    # host cost of enqueueing one step: 100 steps behind a GPU-side spin, so
+    # that the calls only enqueue (no synchronisation inside)
+    n_host = 100
+    torch.cuda._sleep(int(0.05 / max(spin_s_per_cycle, 1e-12)))
+    t0 = time.perf_counter()
+    for _ in range(n_host):
+        step()
+    host_step_s = (time.perf_counter() - t0) / n_host
+    torch.cuda.synchronize()
 
     K = args.steps
     torch.cuda.synchronize()

@@ -421,15 +421,19 @@ na_status run_forward(int rank, const int64_t* extents, const int32_t* ks, const
 }
 
 // Whether a backward runs as the split form (a Delta pre-pass, then the dK/dV
-// and the dQ workgroups as two launches): large 3-D problems with two blocks
-// per wave, whose dK/dV role otherwise holds the dQ role to its own occupancy.
-// NA_BWD_SPLIT=0|1 forces the choice.
-int bwd_split(int rank, const na_tiling& t) {
+// and the dQ workgroups as two launches; 16-bit types at D <= 64, ignored
+// elsewhere): large 3-D problems with two blocks per wave, whose dK/dV role
+// otherwise holds the dQ role to its own occupancy, and 1-D windows of 512
+// keys or more, where each launch's smaller working set (Q and dO, or K and V,
+// of the slices in flight) stays in L2 (C4: 650 -> 628 us; 2-D problems lose
+// 14-47 %).  NA_BWD_SPLIT=0|1 forces the choice.
+int bwd_split(int rank, const int32_t* ks, const na_tiling& t) {
     if (const char* env = std::getenv("NA_BWD_SPLIT")) {
         if (env[0] == '0') return 0;
         if (env[0] == '1') return 1;
     }
-    return rank == 3 && t.blocks_per_wave == 2 ? 1 : 0;
+    if (rank == 3 && t.blocks_per_wave == 2) return 1;
+    return rank == 1 && ks[0] >= 512 ? 1 : 0;
 }
 
 na_status run_backward(int rank, const int64_t* extents, const int32_t* ks, const int32_t* ds,
@@ -439,7 +443,7 @@ na_status run_backward(int rank, const int64_t* extents, const int32_t* ks, cons
                        void* dq, void* dk, void* dv, hipStream_t s) {
     na::Geo g;
     if (!geo_from_tiling(rank, extents, ks, ds, causal, BH, t, g, false)) return NA_ERR_SHAPE;
-    g.bwd_split = bwd_split(rank, t);
+    g.bwd_split = bwd_split(rank, ks, t);
     hipError_t e = na::launch_backward(g, rank, (int)head_dim, (int)dtype, t.blocks_per_wave, q,
                                        k, v, out, lse, dout, dq, dk, dv, scale, s);
     return e == hipSuccess ? NA_OK : NA_ERR_HIP;
@@ -895,7 +899,7 @@ na_status na_backward(int rank, const int64_t* extents, const int32_t* kernel_si
     na::Geo g;
     if (!geo_from_tiling(rank, extents, kernel_size, dilation, causal, BH, t, g, false))
         return NA_ERR_SHAPE;
-    g.bwd_split = bwd_split(rank, t);
+    g.bwd_split = bwd_split(rank, kernel_size, t);
     if (planned) store_plan(pk, gen, t, g);
     const hipError_t e = na::launch_backward(g, rank, (int)head_dim, (int)dtype,
                                              t.blocks_per_wave, q, k, v, out, logsumexp, dout, dq,

@@ -137,8 +137,9 @@ void check_geo(const na::Geo& g, bool forward, int qm) {
     }
     check_fastdiv(g.fd_ntiles, g.ntiles, g.nwg);
     check_fastdiv(g.fd_ngroups, g.ngroups, g.nwg);
-    // the split form: large 3-D backwards with two blocks per wave
-    if (!forward) CHECK(g.bwd_split == (p.rank == 3 && qm == 2 ? 1 : 0));
+    // the split form: 3-D backwards with two blocks per wave, 1-D windows of 512 or more
+    if (!forward)
+        CHECK(g.bwd_split == ((p.rank == 3 && qm == 2) || (p.rank == 1 && p.k[0] >= 512) ? 1 : 0));
     const int wta[3] = {g.WT[0], g.WT[1], g.WT[2]}, wga[3] = {g.WGd[0], g.WGd[1], g.WGd[2]};
     g_last.blocks_per_wave = qm;
     for (int a = 0; a < 3; ++a) {

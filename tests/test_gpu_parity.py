@@ -4,9 +4,8 @@ All calls go through libna.so's C ABI (paper_2403_04690_amd binding).  The
 bar: neighbour sets bit-exact; outputs, logsumexp and gradients within 2e-2
 max-abs for fp16/bf16 and 1e-4 for fp32 of the oracle evaluated on the same
 (already rounded) inputs.  Small problems are compared element by element
-(they span several tiles and ragged tails); the five full-size workloads are
-compared in full where the oracle is fast and on sampled rows (borders
-included) otherwise.
+(they span several tiles and ragged tails); every full-size workload is
+compared element by element too, forward and backward (fused and unfused).
 """
 import math
 
@@ -418,6 +417,7 @@ SPLIT_CASES = [
     # (extents, kernel, dilation, causal, head_dim, dtype, blocks per wave, split)
     ((300,), (13,), (3,), None, 64, "fp16", 2, 1),
     ((257,), (64,), (4,), (True,), 64, "bf16", 1, 1),
+    ((1500,), (600,), (2,), None, 64, "fp16", 2, 1),  # the 1-D split of long windows
     ((37, 45), (7, 5), (2, 1), None, 32, "fp16", 2, 1),
     ((33, 31), (13, 13), (2, 2), (True, False), 64, "bf16", 1, 1),
     ((5, 40), (3, 17), (1, 1), None, 32, "fp16", 1, 1),
