@@ -860,3 +860,67 @@ def test_graph_capture_replays_match_eager(na):
             assert torch.equal(got, ref), (rep, name)
         step()  # eager work between replays
         torch.cuda.synchronize()
+
+
+# ---------------------------------------------------------------- per-thread plans
+PLAN_PROBLEMS = [
+    # (extents, kernel, dilation, causal, head_dim, dtype): more problems than a thread keeps plans
+    ((64,), (7,), (1,), None, 32, "fp16"), ((90,), (9,), (2,), (True,), 64, "bf16"),
+    ((50,), (5,), (3,), None, 32, "fp32"), ((12, 14), (3, 5), (1, 1), None, 32, "fp16"),
+    ((12, 14), (3, 5), (1, 1), (True, False), 32, "fp16"), ((20, 9), (5, 3), (2, 1), None, 64, "bf16"),
+    ((6, 7, 8), (3, 3, 3), (1, 1, 2), None, 32, "fp16"), ((6, 7, 8), (3, 3, 3), (1, 1, 2), None, 64, "fp16"),
+    ((33,), (7,), (1,), None, 128, "bf16"), ((10, 10), (10, 10), (1, 1), None, 32, "fp16"),
+]
+
+
+def _plan_case(na, i, seed):
+    ext, ks, ds, cs, D, dtype = PLAN_PROBLEMS[i]
+    shape = (1, 2) + ext + (D,)
+    q, k, v, g = _inputs(shape, dtype, seed, 4)
+    qd, kd, vd, gd = _dev(q, k, v, g)
+    out, lse = na.forward(qd, kd, vd, ks, ds, causal=cs)
+    dq, dk, dv = na.backward(qd, kd, vd, out, lse, gd, ks, ds, causal=cs)
+    torch.cuda.synchronize()
+    sc = 1.0 / math.sqrt(D)
+    ro, rl = oracle.forward(_f64(q), _f64(k), _f64(v), ks, ds, sc, causal=cs)
+    rq, rk, rv = oracle.backward(_f64(q), _f64(k), _f64(v), _f64(g), ks, ds, sc, causal=cs)
+    e = [_maxerr(out, ro), _maxerr(lse, rl), _maxerr(dq, rq), _maxerr(dk, rk), _maxerr(dv, rv)]
+    return max(e) <= TOL[dtype], e
+
+
+def test_plans_of_many_problems_and_threads(na):
+    """Each thread keeps the last few problems' plans: cycling through more problems than
+    that, twice (plans evicted, made again and reused, on fresh inputs), from one thread and
+    then from two at once, every result still matches the oracle."""
+    import threading
+
+    na.tune_clear()
+    for rnd in range(2):
+        for i in range(len(PLAN_PROBLEMS)):
+            ok, e = _plan_case(na, i, 60 + rnd)
+            _log(f"plans round {rnd} problem {i}: max err {max(e):.3g}")
+            assert ok, (rnd, i, e)
+    results, errors = {}, []
+
+    def worker(tid):
+        try:
+            for rnd in range(2):
+                for i in range(tid, len(PLAN_PROBLEMS), 2):
+                    results[(tid, rnd, i)] = _plan_case(na, i, 70 + tid + rnd)
+        except Exception as ex:  # reported below, in the test's thread
+            errors.append(repr(ex))
+
+    threads = [threading.Thread(target=worker, args=(t,)) for t in (0, 1)]
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join()
+    assert not errors, errors
+    assert len(results) == 2 * len(PLAN_PROBLEMS)
+    for key, (ok, e) in results.items():
+        assert ok, (key, e)
+    # a plan made before na.tune_clear is not used after it (same result either way)
+    ok, _ = _plan_case(na, 0, 80)
+    na.tune_clear()
+    ok2, _ = _plan_case(na, 0, 80)
+    assert ok and ok2
