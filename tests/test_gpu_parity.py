@@ -924,3 +924,59 @@ def test_plans_of_many_problems_and_threads(na):
     na.tune_clear()
     ok2, _ = _plan_case(na, 0, 80)
     assert ok and ok2
+
+
+# ---------------------------------------------------------------- random problems
+def _random_problems(n, seed):
+    """Seeded random problems of every rank: extents, windows (odd and even), dilations,
+    causal axes, head dims and types, kept small enough for the oracle."""
+    rng = np.random.default_rng(seed)
+    out = []
+    while len(out) < n:
+        rank = int(rng.integers(1, 4))
+        budget = {1: 400, 2: 900, 3: 1200}[rank]
+        ext, ks, ds, cs = [], [], [], []
+        for _ in range(rank):
+            L = int(rng.integers(2, {1: 400, 2: 40, 3: 14}[rank]))
+            d = int(rng.integers(1, min(4, L) + 1))
+            k = int(rng.integers(1, L // d + 1))
+            ext.append(L), ds.append(d), ks.append(k), cs.append(bool(rng.random() < 0.25))
+        if int(np.prod(ext)) > budget:
+            continue
+        D = int(rng.choice([32, 64, 128]))
+        dtype = str(rng.choice(["fp16", "bf16", "fp32"]))
+        B, H = int(rng.integers(1, 3)), int(rng.integers(1, 3))
+        out.append((tuple(ext), tuple(ks), tuple(ds), tuple(cs) if any(cs) else None, D, dtype,
+                    B, H))
+    return out
+
+
+@pytest.mark.parametrize("case", range(24))
+def test_random_problems_match_the_oracle(na, case):
+    """Forward within the flat tolerance.  The backward within the bound derived from its
+    arithmetic (_end_to_end_bound: the flat tolerance plus roundings relative to the terms'
+    magnitudes), since small windows give gradients large enough that storing them in bf16
+    alone moves them by more than 2e-2 (|dQ| in [4, 8) has a half-ulp of 1/64)."""
+    ext, ks, ds, cs, D, dtype, B, H = _random_problems(24, 2026)[case]
+    shape = (B, H) + ext + (D,)
+    q, k, v, g = _inputs(shape, dtype, 90 + case, 4)
+    qd, kd, vd, gd = _dev(q, k, v, g)
+    fq, fk, fv, fg = (_f64(t) for t in (q, k, v, g))
+    sc = 1.0 / math.sqrt(D)
+    out, lse = na.forward(qd, kd, vd, ks, ds, causal=cs)
+    dq, dk, dv = na.backward(qd, kd, vd, out, lse, gd, ks, ds, causal=cs)
+    ro, rl = oracle.forward(fq, fk, fv, ks, ds, sc, causal=cs)
+    full = oracle.backward_given(fq, fk, fv, ro, rl, fg, ks, ds, sc, causal=cs, abs_sums=True)
+    ef = [_maxerr(out, ro), _maxerr(lse, rl)]
+    eb = [_maxerr(x, r) for x, r in zip((dq, dk, dv), full[:3])]
+    e_s = _score_error(dtype, D, fq, fk, ks, ds, sc, cs)
+    bound = _end_to_end_bound(dtype, D, int(np.prod(ks)), e_s, fq, fk, fv, fg, ks, ds, sc, cs,
+                              full[:3], full[3:])
+    worst = [float((np.abs(_f64(x) - r) / b).max()) for x, r, b in zip((dq, dk, dv), full[:3],
+                                                                         bound)]
+    _log(f"random {case}: {ext} k={ks} d={ds} c={cs} D={D} {dtype} B={B} H={H}: "
+         f"max err o/lse = {[f'{x:.3g}' for x in ef]}, dq/dk/dv = {[f'{x:.3g}' for x in eb]} "
+         f"(/ bound {[f'{x:.3g}' for x in worst]}, max |ref| "
+         f"{[f'{float(np.abs(r).max()):.3g}' for r in full[:3]]})")
+    assert max(ef) <= TOL[dtype]
+    assert max(worst) <= 1.0
