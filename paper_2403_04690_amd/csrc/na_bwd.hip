@@ -54,7 +54,7 @@ __device__ __forceinline__ void dq_role(const Geo& g, int braw, unsigned char* s
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
-    const int wave = uniform(tid >> 6);
+    const int wave = uniform((tid >> 6) & (C::kThreads / kWave - 1));  // (bounds the staging loops)
     const int col = lane & 15;
     const int grp = lane >> 4;
 
@@ -384,7 +384,7 @@ __device__ __forceinline__ void dkdv_role(const Geo& g, int braw, int nwk,
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
-    const int wave = uniform(tid >> 6);
+    const int wave = uniform((tid >> 6) & (C::kThreads / kWave - 1));  // (bounds the staging loops)
     const int col = lane & 15;  // key column of this lane
     const int grp = lane >> 4;
 

@@ -77,7 +77,9 @@ __global__ __launch_bounds__(W * kWave, (fwd_min_blocks<D, T, QM, W>())) void na
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
-    const int wave = uniform(tid >> 6);
+    // (masked: the launch has W waves, which lets the compiler drop the
+    // staging loops' bounds tests)
+    const int wave = uniform((tid >> 6) & (W - 1));
     const int col = lane & 15;  // query column of this lane
     const int grp = lane >> 4;  // 16-lane group
 
