@@ -25,13 +25,18 @@ struct Box {
         nb = nbr;
 #pragma unroll
         for (int a = 0; a < R - 1; ++a) nb *= E[a];
-        fd_nbr.init(nbr);
+        if constexpr (R > 1) fd_nbr.init(nbr);  // (1-D boxes are one row)
 #pragma unroll
         for (int a = 1; a < R - 1; ++a) fd_E[a].init(E[a]);
     }
 
-    // Outer coordinates (relative to lo) and first inner coordinate of block b.
+    // Outer coordinates (relative to lo) and first inner coordinate of block b
+    // (blocks past the box get coordinates past it too).
     __device__ __forceinline__ void block_coords(int b, int* oc, int& inner0) const {
+        if constexpr (R == 1) {  // one row: no division
+            inner0 = b * 16;
+            return;
+        }
         int row = fd_nbr.div(b);
         inner0 = (b - row * nbr) * 16;
 #pragma unroll
