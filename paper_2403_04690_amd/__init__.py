@@ -30,6 +30,10 @@ _PKG = os.path.dirname(os.path.abspath(__file__))
 # of kernel variants); by default the in-tree build is used.
 _LIB_PATH = os.environ.get("NA_LIBRARY") or os.path.join(_PKG, "libna.so")
 _lib = None
+# the optional argument-marshalling extension (csrc/na_pyext.c) and the addresses of the
+# two functions it calls; without it the calls go through ctypes
+_fast = None
+_fast_fn = {}
 
 DTYPES = {torch.float32: 0, torch.float16: 1, torch.bfloat16: 2}
 
@@ -123,8 +127,22 @@ def load_library():
     for name in ("na_unfused_softmax", "na_unfused_softmax_backward"):
         getattr(lib, name).argtypes = prob[:-1] + [_vp] * 3
         getattr(lib, name).restype = ctypes.c_int
+    _load_fast(lib)
     _lib = lib
     return lib
+
+
+def _load_fast(lib):
+    """Use _na_fast (built beside libna.so) for na_forward / na_backward when it is there."""
+    global _fast
+    try:
+        from . import _na_fast
+    except ImportError:
+        _fast = None
+        return
+    _fast_fn["fwd"] = ctypes.cast(lib.na_forward, ctypes.c_void_p).value
+    _fast_fn["bwd"] = ctypes.cast(lib.na_backward, ctypes.c_void_p).value
+    _fast = _na_fast
 
 
 def _check(status):
@@ -142,23 +160,31 @@ def _per_axis(value, rank, name):
 
 @functools.lru_cache(maxsize=256)
 def _problem_arrays_of(extents, kernel_size, dilation, causal):
+    """(rank, extents, kernel_size, dilation, causal-or-None as ctypes arrays, and their
+    addresses); the tuple keeps the arrays alive while a caller uses the addresses."""
     rank = len(extents)
     ext = (ctypes.c_int64 * rank)(*[int(e) for e in extents])
     ks = (ctypes.c_int32 * rank)(*_per_axis(kernel_size, rank, "kernel_size"))
     ds = (ctypes.c_int32 * rank)(*_per_axis(dilation, rank, "dilation"))
     cs = None if causal is None else (ctypes.c_int32 * rank)(
         *[int(bool(c)) for c in _per_axis(causal, rank, "causal")])
-    return rank, ext, ks, ds, cs
+    addrs = (ctypes.addressof(ext), ctypes.addressof(ks), ctypes.addressof(ds),
+             0 if cs is None else ctypes.addressof(cs))
+    return rank, ext, ks, ds, cs, addrs
 
 
 def _hashable(value):
     return tuple(value) if isinstance(value, (list, tuple)) else value
 
 
-def _problem_arrays(extents, kernel_size, dilation, causal=None):
-    """The problem as ctypes arrays (read only by the library; cached per problem)."""
+def _problem(extents, kernel_size, dilation, causal=None):
     return _problem_arrays_of(tuple(extents), _hashable(kernel_size), _hashable(dilation),
                               None if causal is None else _hashable(causal))
+
+
+def _problem_arrays(extents, kernel_size, dilation, causal=None):
+    """The problem as ctypes arrays (read only by the library; cached per problem)."""
+    return _problem(extents, kernel_size, dilation, causal)[:5]
 
 
 # the current stream's handle without building a Stream object (where torch has it)
@@ -273,7 +299,8 @@ def forward(q, k, v, kernel_size, dilation=1, scale=None, out=None, lse=None, ca
     _check_tensors(q, k, v)
     B, H, D = q.shape[0], q.shape[1], q.shape[-1]
     extents = tuple(q.shape[2:-1])
-    rank, ext, ks, ds, cs = _problem_arrays(extents, kernel_size, dilation, causal)
+    prob = _problem(extents, kernel_size, dilation, causal)
+    rank, ext, ks, ds, cs, addrs = prob
     if scale is None:
         scale = 1.0 / math.sqrt(D)
     if out is None:
@@ -285,7 +312,10 @@ def forward(q, k, v, kernel_size, dilation=1, scale=None, out=None, lse=None, ca
         raise ValueError("lse must be a contiguous fp32 tensor of shape q.shape[:-1]")
     args = (q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(), lse.data_ptr(),
             _stream(q.device))
-    if tiling is None:
+    if tiling is None and _fast is not None:
+        _check(_fast.forward(_fast_fn["fwd"], rank, *addrs, B, H, D, DTYPES[q.dtype],
+                             float(scale), *args))
+    elif tiling is None:
         _check(lib.na_forward(rank, ext, ks, ds, cs, B, H, D, DTYPES[q.dtype], float(scale), *args))
     else:
         _check(lib.na_forward_tiled(rank, ext, ks, ds, cs, B, H, D, DTYPES[q.dtype], float(scale),
@@ -301,7 +331,8 @@ def backward(q, k, v, out, lse, dout, kernel_size, dilation=1, scale=None, dq=No
     _check_tensors(q, k, v, out, dout)
     B, H, D = q.shape[0], q.shape[1], q.shape[-1]
     extents = tuple(q.shape[2:-1])
-    rank, ext, ks, ds, cs = _problem_arrays(extents, kernel_size, dilation, causal)
+    prob = _problem(extents, kernel_size, dilation, causal)
+    rank, ext, ks, ds, cs, addrs = prob
     if scale is None:
         scale = 1.0 / math.sqrt(D)
     if lse.dtype != torch.float32 or lse.shape != q.shape[:-1] or not lse.is_contiguous():
@@ -312,7 +343,10 @@ def backward(q, k, v, out, lse, dout, kernel_size, dilation=1, scale=None, dq=No
     _check_tensors(q, dq, dk, dv)
     args = (q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(), lse.data_ptr(),
             dout.data_ptr(), dq.data_ptr(), dk.data_ptr(), dv.data_ptr(), _stream(q.device))
-    if tiling is None:
+    if tiling is None and _fast is not None:
+        _check(_fast.backward(_fast_fn["bwd"], rank, *addrs, B, H, D, DTYPES[q.dtype],
+                              float(scale), *args))
+    elif tiling is None:
         _check(lib.na_backward(rank, ext, ks, ds, cs, B, H, D, DTYPES[q.dtype], float(scale),
                                *args))
     else:

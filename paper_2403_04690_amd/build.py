@@ -41,6 +41,21 @@ def _compile(src, verbose, extra=()):
     return obj
 
 
+def build_pyext(verbose=False):
+    """Compile the binding's optional argument-marshalling extension (_na_fast, host C only)."""
+    import sysconfig
+
+    out = os.path.join(PKG, "_na_fast" + sysconfig.get_config_var("EXT_SUFFIX"))
+    cmd = ["gcc", "-O2", "-std=c11", "-fPIC", "-shared", "-Wall", "-Wextra", "-Werror",
+           "-I", sysconfig.get_paths()["include"], "-I", INCLUDE,
+           os.path.join(CSRC, "na_pyext.c"), "-o", out + ".tmp"]
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    subprocess.check_call(cmd)
+    os.replace(out + ".tmp", out)
+    return out
+
+
 def build(verbose=False, jobs=None, out=None, extra_flags=()):
     """Compile every source and link libna.so (or `out`); extra_flags go to every hipcc call."""
     global BUILD
@@ -68,3 +83,4 @@ def _build(verbose, jobs, lib, extra):
 
 if __name__ == "__main__":
     build(verbose="-v" in sys.argv)
+    build_pyext(verbose="-v" in sys.argv)

@@ -339,3 +339,29 @@ def test_launches_beyond_the_grid_limit_are_rejected(lib, B, H, ok):
     if not ok:  # refused before any pointer is read
         assert lib.na_forward(r, e, k, d, None, B, H, 32, 1, 0.125, *([fake] * 5), None) == want
         assert lib.na_backward(r, e, k, d, None, B, H, 32, 1, 0.125, *([fake] * 9), None) == want
+
+
+def test_fast_marshalling_matches_ctypes(lib):
+    """The binding's argument-marshalling extension (_na_fast, built beside libna.so) calls
+    the same entry points: on invalid and empty problems (no launch) it returns exactly the
+    statuses the ctypes calls return."""
+    import paper_2403_04690_amd as na
+
+    if na._fast is None:
+        pytest.skip("_na_fast is not built")
+    cases = [  # (extents, kernel, dilation, B, H, D, dtype)
+        ((10, 12), (3, 5), (2, 1), 2, 3, 48, 1), ((10, 12), (6, 5), (2, 1), 2, 3, 64, 1),
+        ((10, 12), (3, 5), (2, 1), 2, 3, 64, 7), ((10, 12), (3, 5), (2, 1), 0, 3, 64, 1),
+        ((40,), (7,), (1,), -1, 1, 32, 0), ((4, 4, 4), (3, 3, 3), (1, 1, 1), 1, 1, 32, 2),
+    ]
+    for ext, ks, ds, B, H, D, dt in cases:
+        rank, e, k, d, cs, addrs = na._problem(ext, ks, ds)
+        want_f = lib.na_forward(rank, e, k, d, cs, B, H, D, dt, 0.5, None, None, None, None,
+                                None, None)
+        want_b = lib.na_backward(rank, e, k, d, cs, B, H, D, dt, 0.5, *([None] * 10))
+        got_f = na._fast.forward(na._fast_fn["fwd"], rank, *addrs, B, H, D, dt, 0.5, *([0] * 6))
+        got_b = na._fast.backward(na._fast_fn["bwd"], rank, *addrs, B, H, D, dt, 0.5,
+                                  *([0] * 10))
+        assert (got_f, got_b) == (want_f, want_b), (ext, ks, ds, B, H, D, dt)
+    with pytest.raises(TypeError):
+        na._fast.forward(na._fast_fn["fwd"], 1)
