@@ -142,7 +142,15 @@ def _load_fast(lib):
         return
     _fast_fn["fwd"] = ctypes.cast(lib.na_forward, ctypes.c_void_p).value
     _fast_fn["bwd"] = ctypes.cast(lib.na_backward, ctypes.c_void_p).value
+    _fast_fn["lib"] = lib
     _fast = _na_fast
+
+
+def _fast_for(lib):
+    """The function addresses for `lib` (re-read when another build has been swapped in)."""
+    if _fast_fn.get("lib") is not lib:
+        _load_fast(lib)
+    return _fast_fn
 
 
 def _check(status):
@@ -313,7 +321,7 @@ def forward(q, k, v, kernel_size, dilation=1, scale=None, out=None, lse=None, ca
     args = (q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(), lse.data_ptr(),
             _stream(q.device))
     if tiling is None and _fast is not None:
-        _check(_fast.forward(_fast_fn["fwd"], rank, *addrs, B, H, D, DTYPES[q.dtype],
+        _check(_fast.forward(_fast_for(lib)["fwd"], rank, *addrs, B, H, D, DTYPES[q.dtype],
                              float(scale), *args))
     elif tiling is None:
         _check(lib.na_forward(rank, ext, ks, ds, cs, B, H, D, DTYPES[q.dtype], float(scale), *args))
@@ -344,7 +352,7 @@ def backward(q, k, v, out, lse, dout, kernel_size, dilation=1, scale=None, dq=No
     args = (q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(), lse.data_ptr(),
             dout.data_ptr(), dq.data_ptr(), dk.data_ptr(), dv.data_ptr(), _stream(q.device))
     if tiling is None and _fast is not None:
-        _check(_fast.backward(_fast_fn["bwd"], rank, *addrs, B, H, D, DTYPES[q.dtype],
+        _check(_fast.backward(_fast_for(lib)["bwd"], rank, *addrs, B, H, D, DTYPES[q.dtype],
                               float(scale), *args))
     elif tiling is None:
         _check(lib.na_backward(rank, ext, ks, ds, cs, B, H, D, DTYPES[q.dtype], float(scale),

@@ -365,3 +365,12 @@ def test_fast_marshalling_matches_ctypes(lib):
         assert (got_f, got_b) == (want_f, want_b), (ext, ks, ds, B, H, D, dt)
     with pytest.raises(TypeError):
         na._fast.forward(na._fast_fn["fwd"], 1)
+    # another build swapped in (as A/B comparisons do): the addresses follow it
+    saved = na._lib
+    try:
+        other = ctypes.CDLL(na.library_path(), mode=ctypes.RTLD_LOCAL)
+        na._lib = other
+        assert na._fast_for(other)["fwd"] == ctypes.cast(other.na_forward, ctypes.c_void_p).value
+    finally:
+        na._lib = saved
+        na._fast_for(saved)
