@@ -36,7 +36,7 @@ struct DqCfg {
     static constexpr size_t kBufBytes = 2 * kTileBytes;  // K rows, then V rows
     static constexpr int kKS = D / 32;
     static constexpr int kDB = D / 16;
-    using Ld = DirectRows<T, D, kKeys>;
+    using Ld = DirectRows<T, D, kKeys, 4, (R > 1)>;
 };
 
 // SHORT = 1: every halo row holds at most two 16-key blocks (rank >= 2), so
@@ -72,7 +72,7 @@ __device__ __forceinline__ void dq_role(const Geo& g, int braw, unsigned char* s
         halo.lo[a] = win_start(to[a], n[a], g.k[a], ca);
         halo.E[a] = win_last(last, n[a], g.k[a], ca) + 1 - halo.lo[a];
     }
-    halo.finish();
+    halo.finish(g, gc);
 
     const size_t slice = (size_t)bh * g.N * D;
     const T* kb = kg + slice;
@@ -91,10 +91,7 @@ __device__ __forceinline__ void dq_role(const Geo& g, int braw, unsigned char* s
         const bool ca = g.causal[a] != 0;
         const int sf = win_start(f, n[a], g.k[a], ca), sl = win_start(l, n[a], g.k[a], ca);
         const int ef = win_last(f, n[a], g.k[a], ca), el = win_last(l, n[a], g.k[a], ca);
-        wr.lo[a] = sf - halo.lo[a];
-        wr.hi[a] = el + 1 - halo.lo[a];
-        wr.flo[a] = sl - halo.lo[a];
-        wr.fhi[a] = ef + 1 - halo.lo[a];
+        wr.set(a, sf - halo.lo[a], el + 1 - halo.lo[a], sl - halo.lo[a], ef + 1 - halo.lo[a]);
     }
 
     int qs[QM][kMaxRank];
@@ -132,7 +129,7 @@ __device__ __forceinline__ void dq_role(const Geo& g, int braw, unsigned char* s
     const int tstep = g.d[R - 1];
     typename C::Ld ld;
     auto issue_stage = [&](int s, int buf) {
-        ld.compute(halo, g, gc, s * SB, tstep, wave, lane);
+        ld.compute(halo, s * SB, tstep, wave, lane);
         unsigned char* tile = smem_raw + buf * C::kBufBytes;
         ld.issue(kb, tile, wave);
         ld.issue(vb, tile + C::kTileBytes, wave);
@@ -364,7 +361,7 @@ struct DkvCfg {
     static constexpr size_t kBufBytes = kFloatOff + 2 * kRows * sizeof(float);
     static constexpr int kKS = D / 32;
     static constexpr int kDB = D / 16;
-    using Ld = DirectRows<T, D, kRows>;
+    using Ld = DirectRows<T, D, kRows, 4, (R > 1)>;
 };
 
 // SHORT = 1: every query-box row holds at most two 16-query blocks (rank >= 2).
@@ -404,7 +401,7 @@ __device__ __forceinline__ void dkdv_role(const Geo& g, int braw, int nwk,
         ibox.lo[a] = inv_lo(to[a], n[a], g.k[a], ca);
         ibox.E[a] = inv_hi(last, n[a], g.k[a], ca) + 1 - ibox.lo[a];
     }
-    ibox.finish();
+    ibox.finish(g, gc);
 
     const size_t slice = (size_t)bh * g.N * D;
     const T* qb = qg + slice;
@@ -425,10 +422,10 @@ __device__ __forceinline__ void dkdv_role(const Geo& g, int braw, int nwk,
         const int f = min(wo[a], n[a] - 1);
         const int l = min(wo[a] + g.WT[a], n[a]) - 1;
         const bool ca = g.causal[a] != 0;
-        wr.lo[a] = inv_lo(f, n[a], g.k[a], ca) - ibox.lo[a];
-        wr.hi[a] = inv_hi(l, n[a], g.k[a], ca) + 1 - ibox.lo[a];
-        wr.flo[a] = inv_lo(l, n[a], g.k[a], ca) - ibox.lo[a];
-        wr.fhi[a] = inv_hi(f, n[a], g.k[a], ca) + 1 - ibox.lo[a];
+        wr.set(a, inv_lo(f, n[a], g.k[a], ca) - ibox.lo[a],
+               inv_hi(l, n[a], g.k[a], ca) + 1 - ibox.lo[a],
+               inv_lo(l, n[a], g.k[a], ca) - ibox.lo[a],
+               inv_hi(f, n[a], g.k[a], ca) + 1 - ibox.lo[a]);
     }
 
     // per-lane keys: group coordinates, K and V fragments
@@ -500,14 +497,14 @@ __device__ __forceinline__ void dkdv_role(const Geo& g, int braw, int nwk,
     float lse_reg = 0.f, ndl_reg = 0.f;
     i32x4 orow[L::kSegs];  // kRegDelta: this thread's O row
     auto issue_stage = [&](int s, int buf) {
-        ld.compute(ibox, g, gc, s * SB, tstep, wave, lane);
+        ld.compute(ibox, s * SB, tstep, wave, lane);
         unsigned char* tile = smem_raw + buf * C::kBufBytes;
         ld.issue(qb, tile, wave);
         ld.issue(gb, tile + C::kTileBytes, wave);
         if constexpr (!DIN && !C::kRegDelta) ld.issue(ob, tile + 2 * C::kTileBytes, wave);
         if (tid < C::kRows) {
             int valid;
-            const int tok0 = ibox.block_token(g, gc, s * SB + (tid >> 4), valid);
+            const int tok0 = ibox.block_token(s * SB + (tid >> 4), valid);
             const bool ok = (tid & 15) < valid;
             const int tk = ok ? tok0 + (tid & 15) * tstep : 0;  // token 0: safe stand-in
             const float lv = lb[tk];

@@ -52,7 +52,7 @@ struct FwdCfg {
     static constexpr size_t kBufBytes = 2 * kTileBytes;  // K rows, then V rows
     static constexpr int kKS = D / 32;  // contraction steps over D
     static constexpr int kDB = D / 16;  // 16-wide blocks of D
-    using Ld = DirectRows<T, D, kKeys, W>;
+    using Ld = DirectRows<T, D, kKeys, W, (R > 1)>;
     static_assert(SB % 2 == 0 && SB <= 32, "stage blocks are tested by one lane each");
 };
 
@@ -100,7 +100,7 @@ __global__ __launch_bounds__(W * kWave, (fwd_min_blocks<D, T, QM, W>())) void na
         halo.lo[a] = win_start(to[a], n[a], g.k[a], ca);
         halo.E[a] = win_last(last, n[a], g.k[a], ca) + 1 - halo.lo[a];
     }
-    halo.finish();
+    halo.finish(g, gc);
 
     const size_t slice = (size_t)bh * g.N * D;
     const T* kb = kg + slice;
@@ -112,7 +112,7 @@ __global__ __launch_bounds__(W * kWave, (fwd_min_blocks<D, T, QM, W>())) void na
     // loads are in flight during the per-wave and per-lane set-up below.
     typename C::Ld ld;
     auto issue_stage = [&](int s, int buf) {
-        ld.compute(halo, g, gc, s * SB, tstep, wave, lane);
+        ld.compute(halo, s * SB, tstep, wave, lane);
         unsigned char* tile = smem_raw + buf * C::kBufBytes;
         ld.issue(kb, tile, wave);
         ld.issue(vb, tile + C::kTileBytes, wave);
@@ -133,10 +133,7 @@ __global__ __launch_bounds__(W * kWave, (fwd_min_blocks<D, T, QM, W>())) void na
         const bool ca = g.causal[a] != 0;
         const int sf = win_start(f, n[a], g.k[a], ca), sl = win_start(l, n[a], g.k[a], ca);
         const int ef = win_last(f, n[a], g.k[a], ca), el = win_last(l, n[a], g.k[a], ca);
-        wr.lo[a] = sf - halo.lo[a];
-        wr.hi[a] = el + 1 - halo.lo[a];
-        wr.flo[a] = sl - halo.lo[a];
-        wr.fhi[a] = ef + 1 - halo.lo[a];
+        wr.set(a, sf - halo.lo[a], el + 1 - halo.lo[a], sl - halo.lo[a], ef + 1 - halo.lo[a]);
     }
 
     // ---- per-lane queries: validity, window starts (relative to the halo), Q ----

@@ -19,8 +19,13 @@ struct Box {
     int nb;   // total blocks
     FastDiv fd_nbr;
     FastDiv fd_E[kMaxRank];
+    // token (within the (batch, head) slice) of the box's first position, and
+    // the token distance of one step along each axis in group coordinates
+    int tok_lo;
+    int tstride[kMaxRank];
 
-    __device__ __forceinline__ void finish() {
+    // Block counts and divisors; gc[] is the dilation group of each axis.
+    __device__ __forceinline__ void finish(const Geo& g, const int* gc) {
         nbr = (E[R - 1] + 15) >> 4;
         nb = nbr;
 #pragma unroll
@@ -28,6 +33,12 @@ struct Box {
         if constexpr (R > 1) fd_nbr.init(nbr);  // (1-D boxes are one row)
 #pragma unroll
         for (int a = 1; a < R - 1; ++a) fd_E[a].init(E[a]);
+        tok_lo = 0;
+#pragma unroll
+        for (int a = 0; a < R; ++a) {
+            tstride[a] = g.d[a] * g.ts[a];
+            tok_lo += (gc[a] + g.d[a] * lo[a]) * g.ts[a];
+        }
     }
 
     // Outer coordinates (relative to lo) and first inner coordinate of block b
@@ -51,17 +62,16 @@ struct Box {
     // Token (within the (batch, head) slice) of slot 0 of block b, and how many
     // slots of the block hold a token of the box (0 for blocks past the end).
     // Slot j of the block is token + j * g.d[R-1].
-    __device__ __forceinline__ int block_token(const Geo& g, const int* gc, int b,
-                                               int& valid) const {
+    __device__ __forceinline__ int block_token(int b, int& valid) const {
         int oc[kMaxRank];
         int inner0;
         block_coords(b, oc, inner0);
         oc[R - 1] = inner0;
         const int left = E[R - 1] - inner0;
         valid = b < nb ? (left > 16 ? 16 : left) : 0;
-        int tok = 0;
+        int tok = tok_lo;
 #pragma unroll
-        for (int a = 0; a < R; ++a) tok += (gc[a] + g.d[a] * (lo[a] + oc[a])) * g.ts[a];
+        for (int a = 0; a < R; ++a) tok += oc[a] * tstride[a];
         return tok;
     }
 };
@@ -69,9 +79,25 @@ struct Box {
 // Per-wave block tests against a box of the other side: a block is relevant
 // when it intersects [lo, hi) on every axis, and full when it lies inside
 // [flo, fhi) on every axis (all its pairs with the wave's tokens are valid).
+// Each range is kept as its start and its length (0 when empty), so that
+// every test is one unsigned comparison.
 template <int R>
 struct WaveRange {
-    int lo[kMaxRank], hi[kMaxRank], flo[kMaxRank], fhi[kMaxRank];
+    int lo[kMaxRank], rlen[kMaxRank], flo[kMaxRank], flen[kMaxRank];
+    int ilen;  // inner axis: blocks [i0, i0 + 16) meeting [lo, hi) have i0 - lo + 15 < ilen
+    int iflen;  // inner axis: blocks inside [flo, fhi) have i0 - flo < iflen
+
+    // Axis a: relevant range [lo_, hi_) (never empty), full range [flo_, fhi_).
+    __device__ __forceinline__ void set(int a, int lo_, int hi_, int flo_, int fhi_) {
+        lo[a] = lo_;
+        rlen[a] = hi_ - lo_;
+        flo[a] = flo_;
+        flen[a] = fhi_ > flo_ ? fhi_ - flo_ : 0;
+        if (a == R - 1) {
+            ilen = hi_ - lo_ + 15;
+            iflen = fhi_ - flo_ > 15 ? fhi_ - flo_ - 15 : 0;
+        }
+    }
 
     // rel: block b meets some window of the wave's queries; full: it lies
     // inside all of them; outer_full: inside all of them along the outer axes
@@ -79,17 +105,16 @@ struct WaveRange {
     __device__ __forceinline__ void test(const Box<R>& box, int b, int* oc, int& inner0, bool& rel,
                                          bool& full, bool& outer_full) const {
         box.block_coords(b, oc, inner0);
-        bool r_ = b < box.nb, f_ = b < box.nb;
+        const bool in_box = b < box.nb;
+        bool r_ = in_box, f_ = in_box;
 #pragma unroll
         for (int a = 0; a < R - 1; ++a) {
-            r_ = r_ && oc[a] >= lo[a] && oc[a] < hi[a];
-            f_ = f_ && oc[a] >= flo[a] && oc[a] < fhi[a];
+            r_ = r_ & ((unsigned)(oc[a] - lo[a]) < (unsigned)rlen[a]);
+            f_ = f_ & ((unsigned)(oc[a] - flo[a]) < (unsigned)flen[a]);
         }
         outer_full = f_;
-        r_ = r_ && inner0 < hi[R - 1] && inner0 + 16 > lo[R - 1];
-        f_ = f_ && inner0 >= flo[R - 1] && inner0 + 16 <= fhi[R - 1];
-        rel = r_;
-        full = f_;
+        rel = r_ & ((unsigned)(inner0 - lo[R - 1] + 15) < (unsigned)ilen);
+        full = f_ & ((unsigned)(inner0 - flo[R - 1]) < (unsigned)iflen);
     }
     __device__ __forceinline__ void test(const Box<R>& box, int b, int* oc, int& inner0, bool& rel,
                                          bool& full) const {
@@ -142,30 +167,37 @@ typedef __attribute__((address_space(3))) void lds_void;
 // lane l loads the segment that the swizzle puts at position 64 t + l.
 // Tokens missing from the box are replaced by token 0 of the slice (finite
 // data that the masks exclude).  Several tensors with the same rows share one
-// set of per-lane source offsets.  The W waves of the workgroup take the
-// instructions round-robin.
-template <typename T, int D, int ROWS, int W = 4>
+// set of per-lane source offsets.  With BLOCKWISE, when a block takes several
+// instructions, wave w of the W takes the consecutive ones [w * kPerWave,
+// (w + 1) * kPerWave), so that one block decode serves all of a block's
+// instructions (2-D / 3-D boxes, whose decode has divisions); otherwise the
+// waves take the instructions round-robin (measured faster for 1-D boxes).
+template <typename T, int D, int ROWS, int W = 4, bool BLOCKWISE = false>
 struct DirectRows {
     using L = Rows<T, D>;
     static constexpr int kRowsPerInstr = 64 / L::kSegs;
     static constexpr int kInstr = ROWS * L::kSegs / 64;  // wave instructions per tensor
     static constexpr int kPerWave = (kInstr + W - 1) / W;
+    // wave instruction u of this wave
+    __device__ __forceinline__ static int instr(int wave, int u) {
+        return BLOCKWISE && kRowsPerInstr < 16 ? wave * kPerWave + u : wave + W * u;
+    }
     static_assert(ROWS % 16 == 0 && kInstr >= 1, "whole blocks per stage");
     int src[kPerWave];  // element offset (within the slice) of this lane's segment
 
     // Rows of stage-local blocks b0, b0 + 1, ... of the box; tstep is the token
     // distance between consecutive slots of a block.
     template <int R>
-    __device__ __forceinline__ void compute(const Box<R>& box, const Geo& g, const int* gc, int b0,
-                                            int tstep, int wave, int lane) {
+    __device__ __forceinline__ void compute(const Box<R>& box, int b0, int tstep, int wave,
+                                            int lane) {
 #pragma unroll
         for (int u = 0; u < kPerWave; ++u) {
-            const int t = wave + W * u;
+            const int t = instr(wave, u);
             src[u] = 0;
             if (t < kInstr) {
                 const int row0 = t * kRowsPerInstr;  // first stage-local row (uniform)
                 int valid;
-                const int tok0 = box.block_token(g, gc, b0 + (row0 >> 4), valid);
+                const int tok0 = box.block_token(b0 + (row0 >> 4), valid);
                 const int j = (row0 & 15) + lane / L::kSegs;
                 const int seg = (lane % L::kSegs) ^ L::swz(j);
                 const int tok = j < valid ? tok0 + j * tstep : 0;
@@ -177,7 +209,7 @@ struct DirectRows {
     __device__ __forceinline__ void issue(const T* base, unsigned char* tile, int wave) const {
 #pragma unroll
         for (int u = 0; u < kPerWave; ++u) {
-            const int t = wave + W * u;
+            const int t = instr(wave, u);
             if (t < kInstr)
                 __builtin_amdgcn_global_load_lds(static_cast<const void*>(base + src[u]),
                                                  (lds_void*)(tile + t * 1024), 16, 0, 0);
