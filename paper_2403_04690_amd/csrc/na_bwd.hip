@@ -189,20 +189,20 @@ __device__ __forceinline__ void dq_role(const Geo& g, int braw, unsigned char* s
 #pragma unroll
             for (int j = 0; j < 8; ++j) qf[m][st][j] = Tr<T>::cvt((float)qf[m][st][j] * scale_log2);
 
+    ChunkTests<R, SB> ct;  // this wave's block tests, 64 blocks at a time
     for (int s = 0; s < nst; ++s) {
         if (s + 1 < nst) issue_stage(s + 1, (s + 1) & 1);
         const unsigned char* ks = smem_raw + (s & 1) * C::kBufBytes;
         const unsigned char* vs = ks + C::kTileBytes;
 
         if (wave_live) {
-            // lane j < SB tests block s*SB + j; only tiles with a relevant
-            // block are visited, their coordinates read back from the lanes
-            int loc[kMaxRank], lin0;
-            bool lrel, lfull, lofull;
-            wr.test(halo, s * SB + (lane < SB ? lane : 0), loc, lin0, lrel, lfull, lofull);
-            const uint64_t relm = __builtin_amdgcn_ballot_w64(lane < SB && lrel);
-            const uint64_t fullm = __builtin_amdgcn_ballot_w64(lane < SB && lfull);
-            const uint64_t ofullm = __builtin_amdgcn_ballot_w64(lane < SB && lofull);
+            // blocks are tested one per lane, 64 at a time; only tiles with a
+            // relevant block are visited, their coordinates read back from the
+            // lanes
+            ct.stage(wr, halo, s, lane);
+            const uint64_t relm = ct.rel_bits();
+            const uint64_t fullm = ct.full_bits();
+            const uint64_t ofullm = ct.ofull_bits();
             uint64_t tiles = (relm | (relm >> 1)) & 0x5555555555555555ull;
             // The body of one tile (block pair tp), by kind, as in the forward:
             // 0 general; 1 both blocks inside every window of the wave's queries;
@@ -218,9 +218,9 @@ __device__ __forceinline__ void dq_role(const Geo& g, int braw, unsigned char* s
                     const int j = tp * 2 + bi;
                     rel[bi] = kFull || kOuterFull || ((relm >> j) & 1);
                     full[bi] = kFull || ((fullm >> j) & 1);
-                    bin0[bi] = __builtin_amdgcn_readlane(lin0, j);
+                    bin0[bi] = ct.inner0(j);
 #pragma unroll
-                    for (int a = 0; a < R - 1; ++a) boc[bi][a] = __builtin_amdgcn_readlane(loc[a], j);
+                    for (int a = 0; a < R - 1; ++a) boc[bi][a] = ct.outer(j, a);
                 }
 
                 // Y^T = c K Q^T + A (A: -lse2 on valid pairs, -inf on masked; with
@@ -599,6 +599,7 @@ __device__ __forceinline__ void dkdv_role(const Geo& g, int braw, int nwk,
             for (int j = 0; j < 8; ++j) kf[m][st][j] = Tr<T>::cvt((float)kf[m][st][j] * scale_log2);
     __syncthreads();
 
+    ChunkTests<R, SB> ct;  // this wave's block tests, 64 blocks at a time
     for (int s = 0; s < nst; ++s) {
         if (s + 1 < nst) issue_stage(s + 1, (s + 1) & 1);
         const unsigned char* qs = smem_raw + (s & 1) * C::kBufBytes;
@@ -607,14 +608,13 @@ __device__ __forceinline__ void dkdv_role(const Geo& g, int braw, int nwk,
         const float* dls = ls + C::kRows;
 
         if (wave_live) {
-            // lane j < SB tests block s*SB + j; only tiles with a relevant
-            // block are visited, their coordinates read back from the lanes
-            int loc[kMaxRank], lin0;
-            bool lrel, lfull, lofull;
-            wr.test(ibox, s * SB + (lane < SB ? lane : 0), loc, lin0, lrel, lfull, lofull);
-            const uint64_t relm = __builtin_amdgcn_ballot_w64(lane < SB && lrel);
-            const uint64_t fullm = __builtin_amdgcn_ballot_w64(lane < SB && lfull);
-            const uint64_t ofullm = __builtin_amdgcn_ballot_w64(lane < SB && lofull);
+            // blocks are tested one per lane, 64 at a time; only tiles with a
+            // relevant block are visited, their coordinates read back from the
+            // lanes
+            ct.stage(wr, ibox, s, lane);
+            const uint64_t relm = ct.rel_bits();
+            const uint64_t fullm = ct.full_bits();
+            const uint64_t ofullm = ct.ofull_bits();
             uint64_t tiles = (relm | (relm >> 1)) & 0x5555555555555555ull;
             // The body of one tile (block pair tp), by kind: 0 general; 1 both
             // query blocks attend every key of the wave; 2 short rows, both
@@ -630,9 +630,9 @@ __device__ __forceinline__ void dkdv_role(const Geo& g, int braw, int nwk,
                     const int j = tp * 2 + bi;
                     rel[bi] = kFull || kOuterFull || ((relm >> j) & 1);
                     full[bi] = kFull || ((fullm >> j) & 1);
-                    bin0[bi] = __builtin_amdgcn_readlane(lin0, j);
+                    bin0[bi] = ct.inner0(j);
 #pragma unroll
-                    for (int a = 0; a < R - 1; ++a) boc[bi][a] = __builtin_amdgcn_readlane(loc[a], j);
+                    for (int a = 0; a < R - 1; ++a) boc[bi][a] = ct.outer(j, a);
                 }
 
                 // -lse2 and -Delta of the 2 x 4 queries this lane holds

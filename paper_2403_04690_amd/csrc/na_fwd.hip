@@ -246,21 +246,21 @@ __global__ __launch_bounds__(W * kWave, (fwd_min_blocks<D, T, QM, W>())) void na
 #pragma unroll
             for (int j = 0; j < 8; ++j) qf[m][st][j] = Tr<T>::cvt((float)qf[m][st][j] * c);
 
+    ChunkTests<R, SB> ct;  // this wave's block tests, 64 blocks at a time
     for (int s = 0; s < nst; ++s) {
         if (s + 1 < nst) issue_stage(s + 1, (s + 1) & 1);
         const unsigned char* ks = smem_raw + (s & 1) * C::kBufBytes;
         const unsigned char* vs = ks + C::kTileBytes;
 
         if (wave_live) {
-            // lane j < SB tests block s*SB + j of the halo against this wave's
-            // queries; the wave then visits only the tiles (block pairs) with
-            // a relevant block, reading their coordinates back from the lanes
-            int loc[kMaxRank], lin0;
-            bool lrel, lfull, lofull;
-            wr.test(halo, s * SB + (lane < SB ? lane : 0), loc, lin0, lrel, lfull, lofull);
-            const uint64_t relm = __builtin_amdgcn_ballot_w64(lane < SB && lrel);
-            const uint64_t fullm = __builtin_amdgcn_ballot_w64(lane < SB && lfull);
-            const uint64_t ofullm = __builtin_amdgcn_ballot_w64(lane < SB && lofull);
+            // the halo's blocks are tested against this wave's queries (one
+            // block per lane, 64 at a time); the wave then visits only the
+            // tiles (block pairs) with a relevant block, reading their
+            // coordinates back from the lanes
+            ct.stage(wr, halo, s, lane);
+            const uint64_t relm = ct.rel_bits();
+            const uint64_t fullm = ct.full_bits();
+            const uint64_t ofullm = ct.ofull_bits();
             uint64_t tiles = (relm | (relm >> 1)) & 0x5555555555555555ull;
             // The body of one tile (block pair tp), by kind: 0 general; 1 both
             // blocks inside every window of the wave's queries (no mask); 2 short
@@ -277,9 +277,9 @@ __global__ __launch_bounds__(W * kWave, (fwd_min_blocks<D, T, QM, W>())) void na
                     const int j = tp * 2 + bi;
                     rel[bi] = kFull || kOuterFull || ((relm >> j) & 1);
                     full[bi] = kFull || ((fullm >> j) & 1);
-                    bin0[bi] = __builtin_amdgcn_readlane(lin0, j);
+                    bin0[bi] = ct.inner0(j);
 #pragma unroll
-                    for (int a = 0; a < R - 1; ++a) boc[bi][a] = __builtin_amdgcn_readlane(loc[a], j);
+                    for (int a = 0; a < R - 1; ++a) boc[bi][a] = ct.outer(j, a);
                 }
 
                 // ---- S^T = K Q^T for both blocks ----

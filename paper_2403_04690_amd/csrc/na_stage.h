@@ -123,6 +123,45 @@ struct WaveRange {
     }
 };
 
+// A wave's block tests taken 64 blocks at a time, one block per lane, instead
+// of once per stage: a stage of SB blocks (SB divides 64) reads its bits from
+// the chunk's masks, and a block's coordinates back from the lane that tested
+// it.  Stages of 16 blocks or more (a whole halo, staged once) are tested
+// stage by stage, with no chunk bookkeeping.
+template <int R, int SB>
+struct ChunkTests {
+    static_assert(64 % SB == 0, "stages tile the 64-block chunks");
+    static constexpr int kChunk = SB >= 16 ? SB : 64;  // blocks tested at a time
+    static constexpr uint64_t kSel = SB == 64 ? ~0ull : (1ull << SB) - 1;
+    int loc[kMaxRank], lin0;  // this lane's block: outer coordinates, first inner coordinate
+    uint64_t rel, full, ofull;  // the chunk's blocks: relevant, full, full along the outer axes
+    int j0;  // the stage's first block within the chunk
+
+    // Stage s (stages are visited in order from 0).
+    __device__ __forceinline__ void stage(const WaveRange<R>& wr, const Box<R>& box, int s,
+                                          int lane) {
+        j0 = (s * SB) & (kChunk - 1);
+        if (j0 == 0) {
+            bool r, f, o;
+            wr.test(box, s * SB + lane, loc, lin0, r, f, o);
+            rel = __builtin_amdgcn_ballot_w64(r);
+            full = __builtin_amdgcn_ballot_w64(f);
+            ofull = __builtin_amdgcn_ballot_w64(o);
+        }
+    }
+    // bit j: block s * SB + j of the stage
+    __device__ __forceinline__ uint64_t rel_bits() const { return (rel >> j0) & kSel; }
+    __device__ __forceinline__ uint64_t full_bits() const { return (full >> j0) & kSel; }
+    __device__ __forceinline__ uint64_t ofull_bits() const { return (ofull >> j0) & kSel; }
+    // first inner coordinate and outer coordinate a of the stage's block j
+    __device__ __forceinline__ int inner0(int j) const {
+        return __builtin_amdgcn_readlane(lin0, j0 + j);
+    }
+    __device__ __forceinline__ int outer(int j, int a) const {
+        return __builtin_amdgcn_readlane(loc[a], j0 + j);
+    }
+};
+
 // ---------------------------------------------------------------------------
 // LDS rows: D elements of T per token, row-major and unpadded, cut into
 // 16-byte segments; segment s of row r is stored at position s ^ swz(r).
