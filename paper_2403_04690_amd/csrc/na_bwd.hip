@@ -494,7 +494,10 @@ __device__ __forceinline__ void dkdv_role(const Geo& g, int braw, int nwk,
     const int tstep = g.d[R - 1];
     typename C::Ld ld;
     using L = Rows<T, D>;
-    float lse_reg = 0.f, ndl_reg = 0.f;
+    // the stage's per-query values as loaded (row tid of the stage), and
+    // whether the row holds a query; combined only where they are stored
+    float lse_raw = 0.f, ndl_raw = 0.f;
+    bool row_ok = false;
     i32x4 orow[L::kSegs];  // kRegDelta: this thread's O row
     auto issue_stage = [&](int s, int buf) {
         ld.compute(ibox, s * SB, tstep, wave, lane);
@@ -502,14 +505,18 @@ __device__ __forceinline__ void dkdv_role(const Geo& g, int braw, int nwk,
         ld.issue(qb, tile, wave);
         ld.issue(gb, tile + C::kTileBytes, wave);
         if constexpr (!DIN && !C::kRegDelta) ld.issue(ob, tile + 2 * C::kTileBytes, wave);
-        if (tid < C::kRows) {
+        // Every thread loads (threads past the stage's rows read a real token
+        // too, whose values are never stored), with nothing computed from the
+        // loaded values here: they are combined only in put_floats, so that
+        // no wait for them (nor for the staging loads above) is needed before
+        // the stage's tiles run.
+        {
             int valid;
             const int tok0 = ibox.block_token(s * SB + (tid >> 4), valid);
-            const bool ok = (tid & 15) < valid;
-            const int tk = ok ? tok0 + (tid & 15) * tstep : 0;  // token 0: safe stand-in
-            const float lv = lb[tk];
-            lse_reg = ok ? -lv * kLog2e : 0.f;  // staged negated: -lse2
-            if constexpr (DIN) ndl_reg = ok ? nb_[tk] : 0.f;  // already -Delta
+            row_ok = (tid & 15) < valid;
+            const int tk = row_ok ? tok0 + (tid & 15) * tstep : 0;  // token 0: safe stand-in
+            lse_raw = lb[tk];
+            if constexpr (DIN) ndl_raw = nb_[tk];  // already -Delta
             if constexpr (C::kRegDelta) {
 #pragma unroll
                 for (int sg = 0; sg < L::kSegs; ++sg)
@@ -580,8 +587,8 @@ __device__ __forceinline__ void dkdv_role(const Geo& g, int braw, int nwk,
     // the per-query floats of a stage: -lse2, and -Delta when it comes from memory
     auto put_floats = [&](int buf) {
         if (tid < C::kRows) {
-            floats(buf)[tid] = lse_reg;
-            if constexpr (DIN) floats(buf)[C::kRows + tid] = ndl_reg;
+            floats(buf)[tid] = row_ok ? -lse_raw * kLog2e : 0.f;  // staged negated: -lse2
+            if constexpr (DIN) floats(buf)[C::kRows + tid] = row_ok ? ndl_raw : 0.f;
         }
     };
     issue_stage(0, 0);
