@@ -206,17 +206,19 @@ __device__ __forceinline__ void dq_role(const Geo& g, int braw, unsigned char* s
             uint64_t tiles = (relm | (relm >> 1)) & 0x5555555555555555ull;
             // The body of one tile (block pair tp), by kind, as in the forward:
             // 0 general; 1 both blocks inside every window of the wave's queries;
-            // 2 short rows, both blocks inside every window along the outer axes.
+            // 2 short rows, both blocks inside every window along the outer axes;
+            // 3 / 4 short rows, only the first / second block so.
             auto tile = [&](int tp, auto tile_kind) {
                 constexpr int kKind = decltype(tile_kind)::value;
                 constexpr bool kFull = kKind == 1;
-                constexpr bool kOuterFull = kKind == 2;
+                // block bi inside every range along the outer axes
+                constexpr bool kOF[2] = {kKind == 2 || kKind == 3, kKind == 2 || kKind == 4};
                 bool rel[2], full[2];
                 int boc[2][kMaxRank], bin0[2];
 #pragma unroll
                 for (int bi = 0; bi < 2; ++bi) {
                     const int j = tp * 2 + bi;
-                    rel[bi] = kFull || kOuterFull || ((relm >> j) & 1);
+                    rel[bi] = kFull || kOF[bi] || ((relm >> j) & 1);
                     full[bi] = kFull || ((fullm >> j) & 1);
                     bin0[bi] = ct.inner0(j);
 #pragma unroll
@@ -232,7 +234,7 @@ __device__ __forceinline__ void dq_role(const Geo& g, int braw, unsigned char* s
                         add = f32x4{-lse2[m], -lse2[m], -lse2[m], -lse2[m]};
                     } else {
                         bool outer_ok = rel[bi];
-                        if (!kOuterFull) {
+                        if (!kOF[bi]) {
 #pragma unroll
                             for (int a = 0; a < R - 1; ++a)
                                 outer_ok = outer_ok &&
@@ -263,7 +265,7 @@ __device__ __forceinline__ void dq_role(const Geo& g, int braw, unsigned char* s
                                     sacc[m][bi] = Tr<T>::mma(kf, qf[m][st], sacc[m][bi]);
                                 else if (kFoldAdd && !short_rows && full[bi])
                                     sacc[m][bi] = Tr<T>::mma(kf, qf[m][0], nlse4[m]);  // in place
-                                else if (kFoldAdd && short_rows && kOuterFull)
+                                else if (kFoldAdd && short_rows && kOF[bi])
                                     sacc[m][bi] = Tr<T>::mma(kf, qf[m][0], ain[m][bi]);  // in place
                                 else
                                     sacc[m][bi] = Tr<T>::mma(kf, qf[m][0],
@@ -313,14 +315,7 @@ __device__ __forceinline__ void dq_role(const Geo& g, int braw, unsigned char* s
                 }
             };
             // the specialised tiles first (the order of tiles does not matter)
-            const uint64_t pairs = short_rows ? ofullm & (ofullm >> 1) : fullm & (fullm >> 1);
-            uint64_t fast_tiles = pairs & tiles;
-            tiles &= ~fast_tiles;
-            while (fast_tiles) {
-                const int tp = __builtin_ctzll(fast_tiles) >> 1;
-                fast_tiles &= fast_tiles - 1;
-                tile(tp, std::integral_constant<int, short_rows ? 2 : 1>{});
-            }
+            run_tile_kinds<short_rows>(tiles, fullm, ofullm, tile);
             while (tiles) {
                 const int tp = __builtin_ctzll(tiles) >> 1;
                 tiles &= tiles - 1;
@@ -625,17 +620,19 @@ __device__ __forceinline__ void dkdv_role(const Geo& g, int braw, int nwk,
             uint64_t tiles = (relm | (relm >> 1)) & 0x5555555555555555ull;
             // The body of one tile (block pair tp), by kind: 0 general; 1 both
             // query blocks attend every key of the wave; 2 short rows, both
-            // blocks inside the wave's inverse ranges along the outer axes.
+            // blocks inside the wave's inverse ranges along the outer axes; 3 / 4
+            // short rows, only the first / second block so.
             auto tile = [&](int tp, auto tile_kind) {
                 constexpr int kKind = decltype(tile_kind)::value;
                 constexpr bool kFull = kKind == 1;
-                constexpr bool kOuterFull = kKind == 2;
+                // block bi inside every range along the outer axes
+                constexpr bool kOF[2] = {kKind == 2 || kKind == 3, kKind == 2 || kKind == 4};
                 bool rel[2], full[2];
                 int boc[2][kMaxRank], bin0[2];
 #pragma unroll
                 for (int bi = 0; bi < 2; ++bi) {
                     const int j = tp * 2 + bi;
-                    rel[bi] = kFull || kOuterFull || ((relm >> j) & 1);
+                    rel[bi] = kFull || kOF[bi] || ((relm >> j) & 1);
                     full[bi] = kFull || ((fullm >> j) & 1);
                     bin0[bi] = ct.inner0(j);
 #pragma unroll
@@ -661,7 +658,7 @@ __device__ __forceinline__ void dkdv_role(const Geo& g, int braw, int nwk,
                         add = nlse[bi];
                     } else {
                         bool outer_ok = rel[bi];
-                        if (!kOuterFull) {
+                        if (!kOF[bi]) {
 #pragma unroll
                             for (int a = 0; a < R - 1; ++a)
                                 outer_ok = outer_ok && (unsigned)(boc[bi][a] - ilo[m][a]) <=
@@ -751,17 +748,8 @@ __device__ __forceinline__ void dkdv_role(const Geo& g, int braw, int nwk,
                         };
             // the specialised tiles first (the order of tiles does not matter);
             // 16-bit types at D <= 64 only (the compiler fails on the others)
-            if constexpr (sizeof(T) == 2 && D <= 64) {
-                const uint64_t pairs =
-                    short_rows ? ofullm & (ofullm >> 1) : fullm & (fullm >> 1);
-                uint64_t fast_tiles = pairs & tiles;
-                tiles &= ~fast_tiles;
-                while (fast_tiles) {
-                    const int tp = __builtin_ctzll(fast_tiles) >> 1;
-                    fast_tiles &= fast_tiles - 1;
-                    tile(tp, std::integral_constant<int, short_rows ? 2 : 1>{});
-                }
-            }
+            if constexpr (sizeof(T) == 2 && D <= 64)
+                run_tile_kinds<short_rows>(tiles, fullm, ofullm, tile);
             while (tiles) {
                 const int tp = __builtin_ctzll(tiles) >> 1;
                 tiles &= tiles - 1;

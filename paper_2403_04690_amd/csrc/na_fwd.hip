@@ -265,17 +265,19 @@ __global__ __launch_bounds__(W * kWave, (fwd_min_blocks<D, T, QM, W>())) void na
             // The body of one tile (block pair tp), by kind: 0 general; 1 both
             // blocks inside every window of the wave's queries (no mask); 2 short
             // rows, both blocks inside every window along the outer axes (the
-            // mask is the per-lane inner-axis addend alone, used in place).
+            // mask is the per-lane inner-axis addend alone, used in place); 3 / 4
+            // short rows, only the first / second block so.
             auto tile = [&](int tp, auto tile_kind) {
                 constexpr int kKind = decltype(tile_kind)::value;
                 constexpr bool kFull = kKind == 1;
-                constexpr bool kOuterFull = kKind == 2;
+                // block bi inside every window along the outer axes
+                constexpr bool kOF[2] = {kKind == 2 || kKind == 3, kKind == 2 || kKind == 4};
                 bool rel[2], full[2];
                 int boc[2][kMaxRank], bin0[2];
 #pragma unroll
                 for (int bi = 0; bi < 2; ++bi) {
                     const int j = tp * 2 + bi;
-                    rel[bi] = kFull || kOuterFull || ((relm >> j) & 1);
+                    rel[bi] = kFull || kOF[bi] || ((relm >> j) & 1);
                     full[bi] = kFull || ((fullm >> j) & 1);
                     bin0[bi] = ct.inner0(j);
 #pragma unroll
@@ -313,7 +315,7 @@ __global__ __launch_bounds__(W * kWave, (fwd_min_blocks<D, T, QM, W>())) void na
                         add = f32x4{negm[m], negm[m], negm[m], negm[m]};
                     } else {
                         bool outer_ok = rel[bi];
-                        if (!kOuterFull) {
+                        if (!kOF[bi]) {
 #pragma unroll
                             for (int a = 0; a < R - 1; ++a)
                                 outer_ok = outer_ok &&
@@ -339,7 +341,7 @@ __global__ __launch_bounds__(W * kWave, (fwd_min_blocks<D, T, QM, W>())) void na
                         // outer-full tile of short rows the inner addends)
                         if (kFoldAdd && !short_rows && full[bi])
                             sacc[m][bi] = Tr<T>::mma(kf[bi][0], qf[m][0], negm4[m]);
-                        else if (kFoldAdd && short_rows && kOuterFull)
+                        else if (kFoldAdd && short_rows && kOF[bi])
                             sacc[m][bi] = Tr<T>::mma(kf[bi][0], qf[m][0], ain[m][bi]);
                         else
                             sacc[m][bi] = Tr<T>::mma(kf[bi][0], qf[m][0],
@@ -425,16 +427,9 @@ __global__ __launch_bounds__(W * kWave, (fwd_min_blocks<D, T, QM, W>())) void na
             };
             // Tiles of two full blocks (kind 1, rows of more than two blocks) or
             // of two outer-full blocks (kind 2, short rows) are visited first, by
-            // bodies without per-block branches; the order of tiles is free in
-            // the online softmax.
-            const uint64_t pairs = short_rows ? ofullm & (ofullm >> 1) : fullm & (fullm >> 1);
-            uint64_t fast_tiles = pairs & tiles;
-            tiles &= ~fast_tiles;
-            while (fast_tiles) {
-                const int tp = __builtin_ctzll(fast_tiles) >> 1;
-                fast_tiles &= fast_tiles - 1;
-                tile(tp, std::integral_constant<int, short_rows ? 2 : 1>{});
-            }
+            // bodies without per-block branches, then (short rows) those with one
+            // outer-full block; the order of tiles is free in the online softmax.
+            run_tile_kinds<short_rows>(tiles, fullm, ofullm, tile);
             while (tiles) {
                 const int tp = __builtin_ctzll(tiles) >> 1;
                 tiles &= tiles - 1;

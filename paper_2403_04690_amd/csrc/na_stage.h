@@ -3,6 +3,8 @@
 // those rows come from.
 #pragma once
 
+#include <type_traits>
+
 #include "na_common.h"
 
 namespace na {
@@ -161,6 +163,35 @@ struct ChunkTests {
         return __builtin_amdgcn_readlane(loc[a], j0 + j);
     }
 };
+
+// Runs the tiles (bit 2 tp of `tiles`: block pair tp) whose kind allows a
+// specialised body, removing them from `tiles`, which keeps the general ones
+// (kind 0).  Kinds: 1 both blocks full (rows of more than two blocks); for
+// short rows, 2 both blocks full along the outer axes, 3 / 4 only the first /
+// second.  The order of tiles is free in the online softmax and in the sums.
+template <bool SHORT_ROWS, typename F>
+__device__ __forceinline__ void run_tile_kinds(uint64_t& tiles, uint64_t full, uint64_t ofull,
+                                               F&& tile) {
+    auto run = [&](uint64_t set, auto kind) {
+        while (set) {
+            const int tp = __builtin_ctzll(set) >> 1;
+            set &= set - 1;
+            tile(tp, kind);
+        }
+    };
+    if constexpr (SHORT_ROWS) {
+        const uint64_t of0 = ofull & 0x5555555555555555ull;
+        const uint64_t of1 = (ofull >> 1) & 0x5555555555555555ull;
+        run(tiles & of0 & of1, std::integral_constant<int, 2>{});
+        run(tiles & of0 & ~of1, std::integral_constant<int, 3>{});
+        run(tiles & ~of0 & of1, std::integral_constant<int, 4>{});
+        tiles &= ~(of0 | of1);
+    } else {
+        const uint64_t pairs = full & (full >> 1) & 0x5555555555555555ull;
+        run(tiles & pairs, std::integral_constant<int, 1>{});
+        tiles &= ~pairs;
+    }
+}
 
 // ---------------------------------------------------------------------------
 // LDS rows: D elements of T per token, row-major and unpadded, cut into
