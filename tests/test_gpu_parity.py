@@ -131,6 +131,9 @@ FWD_CASES = [
     ((5, 9, 11), (5, 3, 3), (1, 3, 3), 32, "fp32", 2, 1),
     ((8, 12, 12), (7, 7, 7), (1, 1, 1), 64, "bf16", 1, 1),
     ((4, 4, 4), (4, 4, 4), (1, 1, 1), 128, "fp16", 1, 2),
+    # halos of more than 64 blocks: the per-wave block tests span two 64-block chunks
+    ((10, 24, 24), (7, 9, 7), (1, 1, 1), 64, "fp16", 1, 1),
+    ((48, 60), (21, 33), (1, 1), 32, "bf16", 1, 1),
 ]
 
 
@@ -394,6 +397,9 @@ BWD_CASES = [
     ((5, 40), (3, 17), (1, 1), 32, "fp16", 1, 1),
     ((3, 4, 64), (3, 3, 25), (1, 1, 1), 32, "bf16", 1, 1),
     ((4, 81), (3, 9), (1, 2), 64, "fp16", 1, 1),
+    # halos and query boxes of more than 64 blocks (two 64-block test chunks)
+    ((10, 24, 24), (7, 9, 7), (1, 1, 1), 64, "fp16", 1, 1),
+    ((48, 60), (21, 33), (1, 1), 32, "bf16", 1, 1),
 ]
 
 
@@ -426,6 +432,7 @@ SPLIT_CASES = [
     ((3, 4, 64), (3, 3, 25), (1, 1, 1), None, 64, "fp16", 1, 1),
     ((6, 20, 22), (3, 7, 5), (1, 2, 2), None, 64, "fp16", 2, 0),
     ((8, 12, 12), (7, 7, 7), (1, 1, 1), (True, False, False), 32, "bf16", 2, 0),
+    ((10, 24, 24), (7, 9, 7), (1, 1, 1), None, 64, "fp16", 2, 1),  # boxes of > 64 blocks
 ]
 
 
