@@ -323,8 +323,10 @@ __device__ __forceinline__ void dq_role(const Geo& g, int braw, unsigned char* s
             }
         }
 
-        if (s + 1 < nst) wait_vmem();
-        __syncthreads();
+        if (s + 1 < nst) {  // (no buffer is reused after the last stage)
+            wait_vmem();
+            __syncthreads();
+        }
     }
 
 #pragma unroll
@@ -757,14 +759,14 @@ __device__ __forceinline__ void dkdv_role(const Geo& g, int braw, int nwk,
             }
         }
 
-        if (s + 1 < nst) {
+        if (s + 1 < nst) {  // (no buffer is reused after the last stage)
             put_floats((s + 1) & 1);
             wait_vmem();
-        }
-        __syncthreads();
-        if (!DIN && s + 1 < nst) {
-            delta_pass((s + 1) & 1);
             __syncthreads();
+            if (!DIN) {
+                delta_pass((s + 1) & 1);
+                __syncthreads();
+            }
         }
     }
 

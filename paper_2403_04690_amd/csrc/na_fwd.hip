@@ -437,8 +437,12 @@ __global__ __launch_bounds__(W * kWave, (fwd_min_blocks<D, T, QM, W>())) void na
             }
         }
 
-        if (s + 1 < nst) wait_vmem();
-        __syncthreads();
+        // the next stage's rows have landed, and this stage's buffer is free for
+        // the loads issued next (no buffer is reused after the last stage)
+        if (s + 1 < nst) {
+            wait_vmem();
+            __syncthreads();
+        }
     }
 
     // ---- epilogue: normalise, store O (rounded once) and the natural-log LSE ----
