@@ -601,7 +601,7 @@ __device__ __forceinline__ void dkdv_role(const Geo& g, int braw, int nwk,
         for (int st = 0; st < C::kKS; ++st)
 #pragma unroll
             for (int j = 0; j < 8; ++j) kf[m][st][j] = Tr<T>::cvt((float)kf[m][st][j] * scale_log2);
-    __syncthreads();
+    if constexpr (!DIN) __syncthreads();  // Delta of the first stage written
 
     ChunkTests<R, SB> ct;  // this wave's block tests, 64 blocks at a time
     for (int s = 0; s < nst; ++s) {
