@@ -78,6 +78,18 @@ __device__ __forceinline__ void dq_role(const Geo& g, int braw, unsigned char* s
     const T* kb = kg + slice;
     const T* vb = vg + slice;
 
+    // The first stage is issued as soon as the halo is known, so that its
+    // loads are in flight during the per-wave and per-lane set-up below.
+    const int tstep = g.d[R - 1];
+    typename C::Ld ld;
+    auto issue_stage = [&](int s, int buf) {
+        ld.compute(halo, s * SB, tstep, wave, lane);
+        unsigned char* tile = smem_raw + buf * C::kBufBytes;
+        ld.issue(kb, tile, wave);
+        ld.issue(vb, tile + C::kTileBytes, wave);
+    };
+    issue_stage(0, 0);
+
     int wc[kMaxRank], wo[kMaxRank];
     unravel_pow2<R>(wave, g.lgWGd, wc);
     bool wave_live = true;
@@ -126,14 +138,6 @@ __device__ __forceinline__ void dq_role(const Geo& g, int braw, unsigned char* s
         lse2[m] = lseg[qoff[m] / D] * kLog2e;
     }
 
-    const int tstep = g.d[R - 1];
-    typename C::Ld ld;
-    auto issue_stage = [&](int s, int buf) {
-        ld.compute(halo, s * SB, tstep, wave, lane);
-        unsigned char* tile = smem_raw + buf * C::kBufBytes;
-        ld.issue(kb, tile, wave);
-        ld.issue(vb, tile + C::kTileBytes, wave);
-    };
     RowFrag<T, D> rfr;
     ColFrag<T, D> cfr;
     rfr.init(lane);
@@ -165,7 +169,6 @@ __device__ __forceinline__ void dq_role(const Geo& g, int braw, unsigned char* s
             }
 
     const int nst = (halo.nb + SB - 1) / SB;
-    issue_stage(0, 0);
     // Delta = dO . O of this lane's queries: 4 lanes hold a query's D slots
 #pragma unroll
     for (int m = 0; m < QM; ++m) {
@@ -407,6 +410,43 @@ __device__ __forceinline__ void dkdv_role(const Geo& g, int braw, int nwk,
     const float* lb = lseg + (size_t)bh * g.N;
     const float* nb_ = DIN ? ndg + (size_t)bh * g.N : nullptr;
 
+    const int tstep = g.d[R - 1];
+    typename C::Ld ld;
+    using L = Rows<T, D>;
+    // the stage's per-query values as loaded (row tid of the stage), and
+    // whether the row holds a query; combined only where they are stored
+    float lse_raw = 0.f, ndl_raw = 0.f;
+    bool row_ok = false;
+    i32x4 orow[L::kSegs];  // kRegDelta: this thread's O row
+    auto issue_stage = [&](int s, int buf) {
+        ld.compute(ibox, s * SB, tstep, wave, lane);
+        unsigned char* tile = smem_raw + buf * C::kBufBytes;
+        ld.issue(qb, tile, wave);
+        ld.issue(gb, tile + C::kTileBytes, wave);
+        if constexpr (!DIN && !C::kRegDelta) ld.issue(ob, tile + 2 * C::kTileBytes, wave);
+        // Every thread loads (threads past the stage's rows read a real token
+        // too, whose values are never stored), with nothing computed from the
+        // loaded values here: they are combined only in put_floats, so that
+        // no wait for them (nor for the staging loads above) is needed before
+        // the stage's tiles run.
+        {
+            int valid;
+            const int tok0 = ibox.block_token(s * SB + (tid >> 4), valid);
+            row_ok = (tid & 15) < valid;
+            const int tk = row_ok ? tok0 + (tid & 15) * tstep : 0;  // token 0: safe stand-in
+            lse_raw = lb[tk];
+            if constexpr (DIN) ndl_raw = nb_[tk];  // already -Delta
+            if constexpr (C::kRegDelta) {
+#pragma unroll
+                for (int sg = 0; sg < L::kSegs; ++sg)
+                    orow[sg] = ld16<i32x4>(ob + (size_t)tk * D + sg * L::kVec);
+            }
+        }
+    };
+    // The first stage is issued as soon as the query box is known, so that
+    // its loads are in flight during the per-wave and per-lane set-up below.
+    issue_stage(0, 0);
+
     // this wave's key sub-box: the queries that attend to any / all of its keys
     int wc[kMaxRank], wo[kMaxRank];
     unravel_pow2<R>(wave, g.lgWGd, wc);
@@ -488,39 +528,6 @@ __device__ __forceinline__ void dkdv_role(const Geo& g, int braw, int nwk,
                                     : -INFINITY;
             }
 
-    const int tstep = g.d[R - 1];
-    typename C::Ld ld;
-    using L = Rows<T, D>;
-    // the stage's per-query values as loaded (row tid of the stage), and
-    // whether the row holds a query; combined only where they are stored
-    float lse_raw = 0.f, ndl_raw = 0.f;
-    bool row_ok = false;
-    i32x4 orow[L::kSegs];  // kRegDelta: this thread's O row
-    auto issue_stage = [&](int s, int buf) {
-        ld.compute(ibox, s * SB, tstep, wave, lane);
-        unsigned char* tile = smem_raw + buf * C::kBufBytes;
-        ld.issue(qb, tile, wave);
-        ld.issue(gb, tile + C::kTileBytes, wave);
-        if constexpr (!DIN && !C::kRegDelta) ld.issue(ob, tile + 2 * C::kTileBytes, wave);
-        // Every thread loads (threads past the stage's rows read a real token
-        // too, whose values are never stored), with nothing computed from the
-        // loaded values here: they are combined only in put_floats, so that
-        // no wait for them (nor for the staging loads above) is needed before
-        // the stage's tiles run.
-        {
-            int valid;
-            const int tok0 = ibox.block_token(s * SB + (tid >> 4), valid);
-            row_ok = (tid & 15) < valid;
-            const int tk = row_ok ? tok0 + (tid & 15) * tstep : 0;  // token 0: safe stand-in
-            lse_raw = lb[tk];
-            if constexpr (DIN) ndl_raw = nb_[tk];  // already -Delta
-            if constexpr (C::kRegDelta) {
-#pragma unroll
-                for (int sg = 0; sg < L::kSegs; ++sg)
-                    orow[sg] = ld16<i32x4>(ob + (size_t)tk * D + sg * L::kVec);
-            }
-        }
-    };
     auto floats = [&](int buf) {
         return reinterpret_cast<float*>(smem_raw + buf * C::kBufBytes + C::kFloatOff);
     };
@@ -588,7 +595,6 @@ __device__ __forceinline__ void dkdv_role(const Geo& g, int braw, int nwk,
             if constexpr (DIN) floats(buf)[C::kRows + tid] = row_ok ? ndl_raw : 0.f;
         }
     };
-    issue_stage(0, 0);
     put_floats(0);
     wait_vmem();
     __syncthreads();
