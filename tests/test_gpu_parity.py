@@ -8,6 +8,7 @@ max-abs for fp16/bf16 and 1e-4 for fp32 of the oracle evaluated on the same
 compared element by element too, forward and backward (fused and unfused).
 """
 import math
+import os
 
 import numpy as np
 import pytest
@@ -958,15 +959,36 @@ def _random_problems(n, seed):
     return out
 
 
-@pytest.mark.parametrize("case", range(24))
-def test_random_problems_match_the_oracle(na, case):
+def _mid_problems(n, seed):
+    """Seeded random 2-D / 3-D problems of up to 4608 / 7000 tokens with windows of at least 40
+    keys, so that many workgroup halos hold more than 64 blocks (several 64-block test chunks)."""
+    rng = np.random.default_rng(seed)
+    out = []
+    while len(out) < n:
+        rank = int(rng.integers(2, 4))
+        ext, ks, ds, cs = [], [], [], []
+        for _ in range(rank):
+            L = int(rng.integers(8, {2: 72, 3: 26}[rank]))
+            d = int(rng.integers(1, 3))
+            k = int(rng.integers(1, L // d + 1))
+            ext.append(L), ds.append(d), ks.append(k), cs.append(bool(rng.random() < 0.2))
+        if int(np.prod(ext)) > {2: 4608, 3: 7000}[rank] or int(np.prod(ks)) < 40:
+            continue
+        D = int(rng.choice([32, 64]))
+        dtype = str(rng.choice(["fp16", "bf16"]))
+        out.append((tuple(ext), tuple(ks), tuple(ds), tuple(cs) if any(cs) else None, D, dtype,
+                    1, 2))
+    return out
+
+
+def _check_random_problem(na, tag, problem, seed):
     """Forward within the flat tolerance.  The backward within the bound derived from its
     arithmetic (_end_to_end_bound: the flat tolerance plus roundings relative to the terms'
     magnitudes), since small windows give gradients large enough that storing them in bf16
     alone moves them by more than 2e-2 (|dQ| in [4, 8) has a half-ulp of 1/64)."""
-    ext, ks, ds, cs, D, dtype, B, H = _random_problems(24, 2026)[case]
+    ext, ks, ds, cs, D, dtype, B, H = problem
     shape = (B, H) + ext + (D,)
-    q, k, v, g = _inputs(shape, dtype, 90 + case, 4)
+    q, k, v, g = _inputs(shape, dtype, seed, 4)
     qd, kd, vd, gd = _dev(q, k, v, g)
     fq, fk, fv, fg = (_f64(t) for t in (q, k, v, g))
     sc = 1.0 / math.sqrt(D)
@@ -981,9 +1003,29 @@ def test_random_problems_match_the_oracle(na, case):
                               full[:3], full[3:])
     worst = [float((np.abs(_f64(x) - r) / b).max()) for x, r, b in zip((dq, dk, dv), full[:3],
                                                                          bound)]
-    _log(f"random {case}: {ext} k={ks} d={ds} c={cs} D={D} {dtype} B={B} H={H}: "
+    _log(f"{tag}: {ext} k={ks} d={ds} c={cs} D={D} {dtype} B={B} H={H}: "
          f"max err o/lse = {[f'{x:.3g}' for x in ef]}, dq/dk/dv = {[f'{x:.3g}' for x in eb]} "
          f"(/ bound {[f'{x:.3g}' for x in worst]}, max |ref| "
          f"{[f'{float(np.abs(r).max()):.3g}' for r in full[:3]]})")
     assert max(ef) <= TOL[dtype]
     assert max(worst) <= 1.0
+
+
+# Case counts of the two random families; a longer sweep raises them, e.g.
+# NA_TEST_RANDOM_PROBLEMS=600 NA_TEST_MID_PROBLEMS=200 pytest -m gpu -k random_problems
+N_RANDOM = int(os.environ.get("NA_TEST_RANDOM_PROBLEMS", "24"))
+N_MID = int(os.environ.get("NA_TEST_MID_PROBLEMS", "12"))
+
+
+@pytest.mark.parametrize("case", range(N_RANDOM))
+def test_random_problems_match_the_oracle(na, case):
+    _check_random_problem(na, f"random {case}", _random_problems(N_RANDOM, 2026)[case], 90 + case)
+
+
+@pytest.mark.parametrize("split", [0, 1])
+@pytest.mark.parametrize("case", range(N_MID))
+def test_mid_size_random_problems_match_the_oracle(na, force, case, split):
+    """Larger halos than the small random problems, under both backward forms."""
+    force(NA_BWD_SPLIT=split)
+    _check_random_problem(na, f"mid {case} split={split}", _mid_problems(N_MID, 4243)[case],
+                          300 + case)
