@@ -798,10 +798,14 @@ __device__ __forceinline__ void dkdv_role(const Geo& g, int braw, int nwk,
 // -7 %).  Ranks 2 and 3 would spill inside the loop.
 // ROLE 0 runs both roles in one grid; ROLE 1 only the dK/dV role (nwk
 // workgroups) and ROLE 2 only the dQ role (g.nwg workgroups), each as a
-// launch of its own with its own register budget.
+// launch of its own with its own register budget.  ROLE 1 stages 128
+// queries (D = 64) or 256 (D = 32) per stage, double-buffered: about 67 KiB
+// of LDS, so two workgroups share a CU, two waves per SIMD whatever the
+// registers, and a tighter bound would only spill.
 template <int R, int D, typename T, int QM, int ROLE>
 constexpr int bwd_min_waves() {
     if constexpr (ROLE == 2) return sizeof(T) == 2 && D <= 64 ? (QM == 1 ? 5 : 3) : 2;
+    if constexpr (ROLE == 1) return 2;
     return sizeof(T) == 2 && D <= 64 ? (R == 1 ? 3 : 2) : 1;
 }
 
