@@ -801,11 +801,12 @@ __device__ __forceinline__ void dkdv_role(const Geo& g, int braw, int nwk,
 // launch of its own with its own register budget.  ROLE 1 stages 128
 // queries (D = 64) or 256 (D = 32) per stage, double-buffered: about 67 KiB
 // of LDS, so two workgroups share a CU, two waves per SIMD whatever the
-// registers, and a tighter bound would only spill.
+// registers, and a tighter bound would only spill.  Rank 1 at D = 64 stages
+// 64 queries instead (about 34 KiB), which leaves room for the third wave.
 template <int R, int D, typename T, int QM, int ROLE>
 constexpr int bwd_min_waves() {
     if constexpr (ROLE == 2) return sizeof(T) == 2 && D <= 64 ? (QM == 1 ? 5 : 3) : 2;
-    if constexpr (ROLE == 1) return 2;
+    if constexpr (ROLE == 1) return R == 1 && D == 64 ? 3 : 2;
     return sizeof(T) == 2 && D <= 64 ? (R == 1 ? 3 : 2) : 1;
 }
 
@@ -940,7 +941,8 @@ static hipError_t launch_bwd_sb(const Geo& g, bool short_rows, bool split, int h
     };
     if constexpr (sizeof(T) == 2 && D <= 64) {
         if (split) {
-            constexpr int SBS = D == 32 ? 16 : 8;
+            // query blocks per stage of the dK/dV launch (see bwd_min_waves)
+            constexpr int SBS = D == 32 ? 16 : (R == 1 ? 4 : 8);
             const size_t lds_ks = (hk > SBS ? 2 : 1) * DkvCfg<R, D, T, KM, SBS, true>::kBufBytes;
             auto kk = na_bwd_kernel<R, D, T, QM, KM, SBQ, SBS, 0, 1>;
             auto kq = na_bwd_kernel<R, D, T, QM, KM, SBQ, SBK, 0, 2>;
