@@ -916,7 +916,7 @@ __global__ __launch_bounds__(256) void na_delta_kernel(const T* __restrict__ o,
 // pre-pass writing -Delta of every query into dq (scratch until the last
 // launch overwrites it), the dK/dV role reading it (no O rows, no Delta pass,
 // one barrier per stage, stages of SBS blocks), then the dQ role; each role
-// runs at the occupancy its own register count allows.
+// runs at the occupancy its own registers and LDS allow.
 template <int R, int D, typename T, int QM, int KM, int SBQ, int SBK>
 static hipError_t launch_bwd_sb(const Geo& g, bool short_rows, bool split, int hq, int hk,
                                 const void* q, const void* k, const void* v, const void* o,
