@@ -924,6 +924,16 @@ static hipError_t launch_bwd_sb(const Geo& g, bool short_rows, bool split, int h
                                 float scale, hipStream_t stream) {
     const size_t lds_q = (hq > SBQ ? 2 : 1) * DqCfg<R, D, T, QM, SBQ>::kBufBytes;
     const size_t lds_k = (hk > SBK ? 2 : 1) * DkvCfg<R, D, T, KM, SBK>::kBufBytes;
+    // No register bound asks for more waves per SIMD (workgroups of four
+    // waves per CU) than a CU's 160 KiB of LDS holds, with double buffers
+    // (stages of 16 blocks are used only when every box fits in one: single).
+    constexpr size_t kCuLds = 160 * 1024;
+    constexpr size_t kLdsQ = (SBQ >= 16 ? 1 : 2) * DqCfg<R, D, T, QM, SBQ>::kBufBytes;
+    constexpr size_t kLdsK = (SBK >= 16 ? 1 : 2) * DkvCfg<R, D, T, KM, SBK>::kBufBytes;
+    static_assert(bwd_min_waves<R, D, T, QM, 0>() * (kLdsQ > kLdsK ? kLdsQ : kLdsK) <= kCuLds,
+                  "one-launch register bound beyond the LDS occupancy");
+    static_assert(bwd_min_waves<R, D, T, QM, 2>() * kLdsQ <= kCuLds,
+                  "dQ-launch register bound beyond the LDS occupancy");
     const int nwk = (g.nwg + 7) & ~7;
     auto launch = [&](auto kern, size_t lds, int grid, const float* nd) -> hipError_t {
         if (lds > 65536) {
@@ -944,6 +954,9 @@ static hipError_t launch_bwd_sb(const Geo& g, bool short_rows, bool split, int h
             // query blocks per stage of the dK/dV launch (see bwd_min_waves)
             constexpr int SBS = D == 32 ? 16 : (R == 1 ? 4 : 8);
             const size_t lds_ks = (hk > SBS ? 2 : 1) * DkvCfg<R, D, T, KM, SBS, true>::kBufBytes;
+            static_assert(bwd_min_waves<R, D, T, QM, 1>() * 2 *
+                                  DkvCfg<R, D, T, KM, SBS, true>::kBufBytes <= kCuLds,
+                          "dK/dV-launch register bound beyond the LDS occupancy");
             auto kk = na_bwd_kernel<R, D, T, QM, KM, SBQ, SBS, 0, 1>;
             auto kq = na_bwd_kernel<R, D, T, QM, KM, SBQ, SBK, 0, 2>;
             if constexpr (R > 1)

@@ -483,6 +483,11 @@ template <int R, int D, typename T, int QM, int SB, int W = 4>
 static hipError_t launch_fwd_inst(const Geo& g, const void* q, const void* k, const void* v,
                                   void* o, float* lse, float scale, hipStream_t stream) {
     using C = FwdCfg<R, D, T, QM, SB, W>;
+    // The register bound asks for no more workgroups per CU than a CU's
+    // 160 KiB of LDS holds, with double buffers (stages of 16 blocks are used
+    // only when the halo fits in one: single).
+    static_assert(fwd_min_blocks<D, T, QM, W>() * (SB >= 16 ? 1 : 2) * C::kBufBytes <= 160 * 1024,
+                  "register bound beyond the LDS occupancy");
     if (g.WGd[0] * g.WGd[1] * g.WGd[2] != W) return hipErrorInvalidConfiguration;
     const bool short_rows = R > 1 && max_row_blocks(g, R) <= 2;
     auto kern = na_fwd_kernel<R, D, T, QM, SB, 0, W>;
@@ -508,10 +513,14 @@ static hipError_t launch_fwd_qm(const Geo& g, int qm, const void* q, const void*
         if (qm == 1) return launch_fwd_inst<R, D, T, 1, 2>(g, q, k, v, o, lse, scale, stream);
         return launch_fwd_inst<R, D, T, 2, 2>(g, q, k, v, o, lse, scale, stream);
     } else {
+        // One block per wave at D = 128: stages of half the keys, so that the
+        // four waves per SIMD the registers allow also fit in LDS.
+        constexpr int kSB1 = D == 128 ? 2 : 4;
         // 1-D: eight waves share each (twice as large) stage
         if constexpr (R == 1) {
             if (g.WGd[0] == 8) {
-                if (qm == 1) return launch_fwd_inst<R, D, T, 1, 8, 8>(g, q, k, v, o, lse, scale, stream);
+                if (qm == 1)
+                    return launch_fwd_inst<R, D, T, 1, kSB1 * 2, 8>(g, q, k, v, o, lse, scale, stream);
                 return launch_fwd_inst<R, D, T, 2, 8, 8>(g, q, k, v, o, lse, scale, stream);
             }
         }
@@ -522,7 +531,7 @@ static hipError_t launch_fwd_qm(const Geo& g, int qm, const void* q, const void*
                 return launch_fwd_inst<R, D, T, 2, 16>(g, q, k, v, o, lse, scale, stream);
             }
         }
-        if (qm == 1) return launch_fwd_inst<R, D, T, 1, 4>(g, q, k, v, o, lse, scale, stream);
+        if (qm == 1) return launch_fwd_inst<R, D, T, 1, kSB1>(g, q, k, v, o, lse, scale, stream);
         return launch_fwd_inst<R, D, T, 2, 4>(g, q, k, v, o, lse, scale, stream);
     }
 }
