@@ -799,14 +799,15 @@ __device__ __forceinline__ void dkdv_role(const Geo& g, int braw, int nwk,
 // ROLE 0 runs both roles in one grid; ROLE 1 only the dK/dV role (nwk
 // workgroups) and ROLE 2 only the dQ role (g.nwg workgroups), each as a
 // launch of its own with its own register budget.  ROLE 1 stages 128
-// queries (D = 64) or 256 (D = 32) per stage, double-buffered: about 67 KiB
+// queries per stage at D = 64, double-buffered: about 67 KiB
 // of LDS, so two workgroups share a CU, two waves per SIMD whatever the
 // registers, and a tighter bound would only spill.  Rank 1 at D = 64 stages
-// 64 queries instead (about 34 KiB), which leaves room for the third wave.
+// 64 queries instead (about 34 KiB), which leaves room for the third wave,
+// and D = 32 stages 128 (about 34 KiB): four waves at rank 1, three above.
 template <int R, int D, typename T, int QM, int ROLE>
 constexpr int bwd_min_waves() {
     if constexpr (ROLE == 2) return sizeof(T) == 2 && D <= 64 ? (QM == 1 ? 5 : 3) : 2;
-    if constexpr (ROLE == 1) return R == 1 && D == 64 ? 3 : 2;
+    if constexpr (ROLE == 1) return R == 1 && D == 64 ? 3 : (D == 32 ? (R == 1 ? 4 : 3) : 2);
     return sizeof(T) == 2 && D <= 64 ? (R == 1 ? 3 : 2) : 1;
 }
 
@@ -952,7 +953,7 @@ static hipError_t launch_bwd_sb(const Geo& g, bool short_rows, bool split, int h
     if constexpr (sizeof(T) == 2 && D <= 64) {
         if (split) {
             // query blocks per stage of the dK/dV launch (see bwd_min_waves)
-            constexpr int SBS = D == 32 ? 16 : (R == 1 ? 4 : 8);
+            constexpr int SBS = D == 32 ? 8 : (R == 1 ? 4 : 8);
             const size_t lds_ks = (hk > SBS ? 2 : 1) * DkvCfg<R, D, T, KM, SBS, true>::kBufBytes;
             static_assert(bwd_min_waves<R, D, T, QM, 1>() * 2 *
                                   DkvCfg<R, D, T, KM, SBS, true>::kBufBytes <= kCuLds,

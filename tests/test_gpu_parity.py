@@ -425,6 +425,7 @@ SPLIT_CASES = [
     ((300,), (13,), (3,), None, 64, "fp16", 2, 1),
     ((257,), (64,), (4,), (True,), 64, "bf16", 1, 1),
     ((1500,), (600,), (2,), None, 64, "fp16", 2, 1),  # the 1-D split of long windows
+    ((1500,), (600,), (2,), None, 32, "bf16", 2, 1),
     ((37, 45), (7, 5), (2, 1), None, 32, "fp16", 2, 1),
     ((33, 31), (13, 13), (2, 2), (True, False), 64, "bf16", 1, 1),
     ((5, 40), (3, 17), (1, 1), None, 32, "fp16", 1, 1),
