@@ -678,6 +678,9 @@ TILING_CASES = [
     ((9, 40), (5, 7), (1, 2), None, 128, "fp16", 1, 2),
     ((300,), (31,), (2,), None, 128, "bf16", 1, 2),
     ((6, 12, 20), (3, 5, 5), (1, 2, 1), None, 128, "fp16", 1, 1),
+    # head dim 128 with long windows: many of the halved one-block stages (2 blocks, 4 with 8 waves)
+    ((1300,), (511,), (2,), None, 128, "fp16", 1, 1),
+    ((40, 48), (13, 21), (1, 1), None, 128, "bf16", 1, 1),
 ]
 
 
