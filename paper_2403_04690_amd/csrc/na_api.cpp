@@ -471,12 +471,16 @@ na_status backward_pointers(const void* q, const void* k, const void* v, const v
 // Candidates timed by default (the heuristic one and the next ones in
 // enumeration order); NA_TUNE_THOROUGH times every candidate.
 constexpr int kDefaultCandidates = 64;
+constexpr int kFinalRounds = 5;  // interleaved timings of each finalist
 
 // Times launches of a candidate list on one stream and picks one: after a
 // warm-up of the heuristic (candidate 0), every candidate is timed once over
 // `reps` launches (after one launch of its own); the three fastest and the
-// heuristic are then timed again back to back, and the heuristic stays
-// unless another finalist beats it by more than 2 %.
+// heuristic are then timed again in kFinalRounds rounds, interleaved, the
+// order reversed every other round, and compared by their medians (one
+// timing of a few launches varies by a few percent from run to run, more
+// than the margin); the heuristic stays unless another finalist beats it by
+// more than 2 %.
 class Tuner {
   public:
     Tuner(hipStream_t s, int reps) : s_(s), reps_(reps < 1 ? 1 : reps) {
@@ -505,15 +509,23 @@ class Tuner {
         std::vector<size_t> fin = {0};
         for (size_t j = 0; j < order.size() && fin.size() < 4; ++j)
             if (order[j] != 0) fin.push_back(order[j]);
+        std::vector<std::vector<float>> tf(fin.size());
+        for (int r = 0; r < kFinalRounds; ++r)
+            for (size_t jj = 0; jj < fin.size(); ++jj) {
+                const size_t j = (r & 1) ? fin.size() - 1 - jj : jj;
+                const float t = time_it([&] { return launch(c[fin[j]]); });
+                if (t < 0.f) return NA_ERR_HIP;
+                tf[j].push_back(t);
+            }
         size_t best = 0;
         float tb = -1.f;
-        for (size_t i : fin) {
-            const float t = time_it([&] { return launch(c[i]); });
-            if (t < 0.f) return NA_ERR_HIP;
-            if (i == 0) t_heur = t;
+        for (size_t j = 0; j < fin.size(); ++j) {
+            std::sort(tf[j].begin(), tf[j].end());
+            const float t = tf[j][tf[j].size() / 2];
+            if (fin[j] == 0) t_heur = t;
             if (tb < 0.f || t < tb) {
                 tb = t;
-                best = i;
+                best = fin[j];
             }
         }
         if (best != 0 && tb > 0.98f * t_heur) {
