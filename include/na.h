@@ -177,8 +177,9 @@ na_status na_backward(int rank, const int64_t* extents, const int32_t* kernel_si
  * warm-up, times the candidate tilings of the forward and, separately, of the
  * backward (the first NA_TUNE_DEFAULT_CANDIDATES, or every one when flags has
  * NA_TUNE_THOROUGH), each over `repeats` launches (>= 1) after one warm-up
- * launch, then times the three fastest and the heuristic tiling again; the
- * heuristic one is kept unless a finalist beats it by more than 2 %.  Runs on
+ * launch, then times the three fastest and the heuristic tiling again in five
+ * interleaved rounds; the heuristic one is kept unless a finalist's median
+ * beats it by more than 2 %.  Runs on
  * the caller's buffers, which end up holding the results of the chosen
  * tilings (out and logsumexp of the forward of q, k, v; dq, dk, dv of the
  * backward with dout).  Records the chosen forward and backward tilings in
